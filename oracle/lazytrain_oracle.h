@@ -1,0 +1,126 @@
+/*
+ * lazytrain_oracle.h -- TEST INFRASTRUCTURE, not part of the product.
+ *
+ * A plain, slow, obviously correct CPU definition of the optimizer-side hot
+ * path of LazyTrain's Hybrid 8-bit operator: the global gradient L2 norm and
+ * clip coefficient, then block-wise 8-bit AdamW over fp32 master weights
+ * (paper Sec. 3.5 "Objective and Execution", the Hybrid 8-bit operator
+ * paragraph; hyperparameters and the non-finite rule from the App. C
+ * training-configuration table; block size from the App. C variant table).
+ *
+ * Only the test suite, the package smoke check and the benchmark's CPU
+ * baseline leg may load this library.  It shares no code, header or constant
+ * with the HIP library; both are written from the same definition.
+ *
+ * Precision: the paper keeps fp32 master weights, so the AdamW update is
+ * fp32 with an explicit operation order (every fmaf is one rounding, every
+ * other operation is a separately rounded IEEE operation, no contraction).
+ * The gradient norm is accumulated in fp64, which the paper's FP32
+ * aggregation does not require but which makes the per-tensor fallback for
+ * unsupported or non-finite cases unnecessary.
+ *
+ * All pointers are host pointers.  Functions never allocate on behalf of the
+ * caller beyond transient scratch and never keep pointers after returning.
+ * n_threads <= 1 runs single-threaded; any thread count gives bitwise the same
+ * results because every partial has a fixed index.
+ */
+#ifndef LAZYTRAIN_ORACLE_H
+#define LAZYTRAIN_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { LTO_F32 = 0, LTO_BF16 = 1 };
+enum { LTO_STATUS_OK = 0, LTO_STATUS_NONFINITE = 1 };
+enum { LTO_OK = 0, LTO_ERR_INVALID_ARG = 1 };
+
+/* Chunk length and lane layout of the fixed sum-of-squares order. */
+#define LTO_CHUNK 8192
+#define LTO_LANES 256
+
+/*
+ * Global sum of squares of a list of gradient tensors (Sec. 3.5: per-tensor
+ * norms, then one global aggregate).  grads[k] points to numels[k] elements of
+ * dtype gdt (LTO_F32 or LTO_BF16).  Writes S_k to sq_per_tensor[k] (may be
+ * NULL), S to *sq_total and LTO_STATUS_NONFINITE to *status when S is not
+ * finite (else LTO_STATUS_OK).  Reduction order: each tensor splits into
+ * 8192-element chunks; a chunk is summed by 256 lanes (lane l owns elements
+ * 8*(l + 256*r) + e, r = 0..3, e = 0..7, in that order), a 64-lane halving
+ * tree per group of 64 lanes, then (W0 + W2) + (W1 + W3); a tensor's chunk
+ * partials go round-robin into 256 accumulators in ascending chunk order,
+ * which a halving tree combines; S sums the S_k in list order.
+ */
+int lto_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_tensors, int gdt,
+                    double* sq_per_tensor, double* sq_total, int32_t* status, int n_threads);
+
+/* Brute force: fp64 sum of (double)x*(double)x in plain index order. */
+double lto_grad_sqnorm_naive(const void* const* grads, const int64_t* numels, int n_tensors,
+                             int gdt);
+
+/*
+ * Clip coefficient (Sec. 3.5 scale step; max grad norm from App. C):
+ * norm = fp32(sqrt(S)), coef = fminf(1, max_norm / (norm + 1e-6f)), all fp32
+ * after the rounding of the fp64 square root.  max_norm = +inf gives 1.
+ */
+void lto_clip_coef(double sq_total, float max_norm, float* total_norm, float* coef);
+
+/*
+ * The fp32 scalars of one AdamW step.  Hyperparameters arrive as doubles (as a
+ * Python or C caller holds them); each scalar is computed in fp64 and rounded
+ * once to fp32: decay = 1 - lr*wd, step_size = lr / (1 - beta1^t),
+ * rbc2 = 1 / sqrt(1 - beta2^t), c1 = 1 - beta1, c2 = 1 - beta2, and beta1,
+ * beta2, eps themselves.  beta^t uses the C library pow().
+ */
+typedef struct {
+    float beta1, beta2, eps, c1, c2, decay, step_size, rbc2;
+} lto_scalars;
+void lto_step_scalars(double lr, double beta1, double beta2, double eps, double weight_decay,
+                      int64_t step, lto_scalars* out);
+
+/*
+ * One Hybrid 8-bit AdamW step over a list of tensors.  For tensor k:
+ * params[k] fp32[n], grads[k] gdt[n] (read only), m_codes[k] int8[n],
+ * v_codes[k] uint8[n], m_absmax[k] / v_absmax[k] fp32[ceil(n / block_size)].
+ * coef may be NULL (no clipping, 1.0f).  status may be NULL (never skip);
+ * when *status == LTO_STATUS_NONFINITE nothing is written.  step is the
+ * 1-based index t of the step being applied.  Returns LTO_OK or
+ * LTO_ERR_INVALID_ARG (block_size < 1, step < 1, n_tensors < 0, a NULL list).
+ * Per element (fp32, scalars from lto_step_scalars):
+ * m0 = q_m*(A_m/127), v0 = q_v*(A_v/255),
+ * g = grad*coef, m1 = fmaf(b1, m0, c1*g), v1 = fmaf(b2, v0, c2*(g*g)),
+ * d = fmaf(sqrtf(v1), rbc2, eps), w1 = fmaf(-step_size, m1/d, w*decay);
+ * per block the new absmax A'_m = max|m1|, A'_v = max v1 and the codes
+ * rint(m1*127/A'_m), rint(v1*255/A'_v) (clamped); a block whose absmax or
+ * reciprocal is not finite stores zero codes and absmax 0.
+ */
+int lto_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int gdt,
+                              int8_t* const* m_codes, float* const* m_absmax,
+                              uint8_t* const* v_codes, float* const* v_absmax,
+                              const int64_t* numels, int n_tensors, int64_t block_size, double lr,
+                              double beta1, double beta2, double eps, double weight_decay,
+                              int64_t step, const float* coef, const int32_t* status,
+                              int n_threads);
+
+/* Block quantizers used by the step (exported for the quantizer tests).
+ * Signed (first moment): A = max|x|, q = clamp(rint(x * (127/A)), -127, 127).
+ * Unsigned (second moment, x >= 0): A = max x, q = clamp(rint(x * (255/A)), 0, 255).
+ * A block whose A or reciprocal is not finite gets q = 0 and A = 0. */
+void lto_quantize_signed(const float* x, int64_t n, int8_t* q, float* absmax);
+void lto_quantize_unsigned(const float* x, int64_t n, uint8_t* q, float* absmax);
+void lto_dequantize_signed(const int8_t* q, int64_t n, float absmax, float* x);
+void lto_dequantize_unsigned(const uint8_t* q, int64_t n, float absmax, float* x);
+
+/* fp32-state AdamW with the same operation order as the 8-bit step (states
+ * m, v stay fp32 and are updated in place).  Used to check that the 8-bit
+ * step reduces to plain AdamW when its states are exactly representable. */
+void lto_adamw_fp32_step(float* w, const void* grad, int gdt, float* m, float* v, int64_t n,
+                         double lr, double beta1, double beta2, double eps, double weight_decay,
+                         int64_t step, float coef);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
