@@ -1,0 +1,286 @@
+"""Benchmark of the Hybrid 8-bit optimizer step on one MI355X.
+
+One "step" is the whole hot path over the resident synthetic workload:
+lt_grad_sqnorm (a1-a2) -> lt_clip_coef (a3) -> lt_hybrid8bit_adamw_step (a4-a10),
+enqueued on one stream.  The default workload is the 3B-class full model
+(tied 151936x2048 embedding + 36 decoder layers: 325 tensors, 3,085,844,480
+fp32 master parameters, bf16 gradients, 8-bit block-wise states, block 2048),
+resident in HBM before timing starts.
+
+Prints ONE JSON line (rank 0): params/s over the timed steps, the achieved HBM
+bandwidth of the whole step and a roofline entry for the dominant kernel (the
+fused step kernel) from HIP events around its launches, and the CPU oracle
+timed on a bounded sample of the same workload on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E peak
+METRIC = "optimizer step params/s + achieved HBM GB/s (% of MI355X peak)"
+WORKLOADS = {"full": "full_3b", "layer": "layer_3b", "tiny": "tiny", "stress": "clip_stress"}
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def grad_bytes(gdt) -> int:
+    import synth
+    return 2 if gdt == synth.BF16 else 4
+
+
+def step_kernel_bytes(numels, block, gbytes) -> int:
+    """Algorithmic HBM bytes of one fused-step launch: per parameter the gradient
+    (read), the fp32 weight (read + write) and the two 8-bit codes (read + write);
+    per block the two fp32 scales (read + write)."""
+    n = sum(numels)
+    nb = sum(-(-x // block) for x in numels)
+    return n * (gbytes + 8 + 2 + 2) + nb * 16
+
+
+def norm_bytes(numels, gbytes) -> int:
+    """Algorithmic bytes of the sum-of-squares pass: one gradient read."""
+    return sum(numels) * gbytes
+
+
+def build_device_workload(w, dev, n_threads):
+    """Generates the workload on the host (pinned staging, one tensor at a time),
+    copies it to HBM and builds the 8-bit states with one step from zero state at
+    t = 1 on an unclipped prior gradient with lr = 0 (weights stay as drawn)."""
+    import torch
+
+    import paper_2608_11919_amd as lt
+    import synth
+
+    K, B = len(w.shapes), w.block_size
+    gdt_torch = torch.bfloat16 if w.grad_dtype == synth.BF16 else torch.float32
+    biggest = max(w.numels)
+    stage_w = torch.empty(biggest, dtype=torch.float32, pin_memory=True)
+    stage_g = torch.empty(biggest, dtype=gdt_torch, pin_memory=True)
+    params, grads = [], []
+    mq, vq, ma, va = [], [], [], []
+    t0 = time.time()
+    for k, n in enumerate(w.numels):
+        synth.fill_ptr(stage_w.data_ptr(), synth.F32, 0, n, w.seed, synth.STREAM_WEIGHTS, k,
+                       w.weight_recipe, n_threads)
+        params.append(stage_w[:n].to(dev, non_blocking=False))
+        synth.fill_ptr(stage_g.data_ptr(), w.grad_dtype, 0, n, w.seed, synth.STREAM_PRIOR_GRAD, k,
+                       w.grad_recipe, n_threads)
+        grads.append(stage_g[:n].to(dev, non_blocking=False))
+        mq.append(torch.zeros(n, dtype=torch.int8, device=dev))
+        vq.append(torch.zeros(n, dtype=torch.uint8, device=dev))
+        ma.append(torch.zeros(-(-n // B), dtype=torch.float32, device=dev))
+        va.append(torch.zeros(-(-n // B), dtype=torch.float32, device=dev))
+        if k % 50 == 0:
+            log(f"generated {k + 1}/{K} tensors ({time.time() - t0:.1f} s)")
+    hyper = dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay)
+    if w.state_init == "prior_step":
+        lt.lt_hybrid8bit_adamw_step(params, grads, mq, ma, vq, va, B, step=1,
+                                    **dict(hyper, lr=0.0))
+        torch.cuda.synchronize()
+    # the gradient of the measured steps replaces the prior gradient in place
+    first = w.step if w.state_init == "prior_step" else 1
+    for k, n in enumerate(w.numels):
+        synth.fill_ptr(stage_g.data_ptr(), w.grad_dtype, 0, n, w.seed, synth.grad_stream(first),
+                       k, w.grad_recipe, n_threads)
+        grads[k].copy_(stage_g[:n])
+    torch.cuda.synchronize()
+    log(f"workload resident in HBM ({time.time() - t0:.1f} s)")
+    return params, grads, mq, ma, vq, va, first
+
+
+def _oracle_pass(w, ks, n_threads):
+    """Generates whole tensors ks of the workload on the host, then times one oracle
+    pass over them: sum of squares + clip + step."""
+    import numpy as np
+
+    import oracle
+    import synth
+
+    B = w.block_size
+    ws = [w.weights(k, n_threads=n_threads) for k in ks]
+    gs = [w.grads(k, synth.grad_stream(w.step), n_threads=n_threads) for k in ks]
+    mq = [np.zeros(x.size, np.int8) for x in ws]
+    vq = [np.zeros(x.size, np.uint8) for x in ws]
+    ma = [np.zeros(-(-x.size // B), np.float32) for x in ws]
+    va = [np.zeros(-(-x.size // B), np.float32) for x in ws]
+    hyper = dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay)
+    t0 = time.perf_counter()
+    _, S, st = oracle.grad_sqnorm(gs, n_threads=n_threads)
+    _, c = oracle.clip_coef(S, w.max_norm)
+    oracle.hybrid8bit_adamw_step(ws, gs, mq, ma, vq, va, B, step=w.step, coef=float(c), status=st,
+                                 n_threads=n_threads, **hyper)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(w, n_threads, target_s: float):
+    """The oracle as it stands, on a bounded sample of the same workload (whole
+    tensors, decoder layers first, the embedding last), timed on this host's cores.
+    One decoder layer is timed first to size a sample of about target_s seconds."""
+    K = len(w.shapes)
+    order = list(range(K))
+    if len(w.shapes[0]) == 2 and w.shapes[0][0] > 100000:
+        order = order[1:] + order[:1]
+    first = order[:min(K, 9)]
+    dt = _oracle_pass(w, first, n_threads)
+    rate = sum(w.numels[k] for k in first) / dt
+    ks, total = [], 0
+    for k in order:
+        if ks and total + w.numels[k] > rate * target_s:
+            break
+        ks.append(k)
+        total += w.numels[k]
+    if ks != first:
+        dt = _oracle_pass(w, ks, n_threads)
+    desc = f"{len(ks)} of {K} tensors ({total} of {w.n_params} params) of {w.name}"
+    return {"value": total / dt, "unit": "params/s", "cores": n_threads, "kind": "oracle",
+            "sample": desc + ": sum of squares + clip + step, one pass", "seconds": round(dt, 3)}
+
+
+def copy_probe(dev, nbytes: int, reps: int):
+    """A plain copy kernel of known size, for scaling the HBM byte counters."""
+    import torch
+    x = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        torch.mul(x, 1.0, out=y)
+    torch.cuda.synchronize()
+    log(f"copy probe: {reps} x torch.mul(out=) over {nbytes} bytes read + {nbytes} written")
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="full")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="approximate CPU seconds for the oracle sample")
+    ap.add_argument("--copy-probe-bytes", type=int, default=0,
+                    help="also run a plain copy of this many bytes (counter scaling)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(see DESIGN.md for how the step would shard)", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2608_11919_amd as lt
+    import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    dev = torch.device("cuda", 0)
+    lt.lib()  # fails loudly when the HIP library is not built
+    n_threads = synth.default_threads()
+    w = getattr(synth, WORKLOADS[args.workload])()
+    K, B = len(w.shapes), w.block_size
+    log(f"workload {w.name}: {K} tensors, {w.n_params} params, block {B}")
+
+    if args.copy_probe_bytes:
+        copy_probe(dev, args.copy_probe_bytes, 5)
+
+    params, grads, mq, ma, vq, va, t_first = build_device_workload(w, dev, n_threads)
+    sq_total = torch.zeros(1, dtype=torch.float64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    coef = torch.zeros(1, dtype=torch.float32, device=dev)
+    norm = torch.zeros(1, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    hyper = dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay)
+    ws_sq = torch.empty(lt.lt_grad_sqnorm_workspace_bytes(w.numels), dtype=torch.uint8, device=dev)
+    ws_step = torch.empty(lt.lt_step_workspace_bytes(K), dtype=torch.uint8, device=dev)
+
+    def one_step(t, ev=None):
+        if ev:
+            ev[0].record(stream)
+        lt.lt_grad_sqnorm(grads, sq_total, status, workspace=ws_sq, stream=stream)
+        lt.lt_clip_coef(sq_total, w.max_norm, coef, total_norm=norm, stream=stream)
+        if ev:
+            ev[1].record(stream)
+        lt.lt_hybrid8bit_adamw_step(params, grads, mq, ma, vq, va, B, step=t, coef=coef,
+                                    status=status, workspace=ws_step, stream=stream, **hyper)
+        if ev:
+            ev[2].record(stream)
+
+    t = t_first
+    for _ in range(args.warmup):
+        one_step(t)
+        t += 1
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        one_step(t, events[i])
+        t += 1
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    st = lt.lt_read_status(status)
+
+    norm_ms = [e[0].elapsed_time(e[1]) for e in events]
+    step_ms = [e[1].elapsed_time(e[2]) for e in events]
+    avg_step_s = sum(step_ms) / len(step_ms) * 1e-3
+    avg_norm_s = sum(norm_ms) / len(norm_ms) * 1e-3
+    gb = grad_bytes(w.grad_dtype)
+    kbytes = step_kernel_bytes(w.numels, B, gb)
+    nbytes = norm_bytes(w.numels, gb)
+    ms_per_step = elapsed / args.steps * 1e3
+    step_total_bytes = kbytes + nbytes
+    achieved = kbytes / avg_step_s / 1e9
+    log(f"status {st}, norm {norm.item():.6g}, coef {coef.item():.6g}; step kernel "
+        f"{avg_step_s * 1e3:.3f} ms ({achieved:.0f} GB/s), norm pass {avg_norm_s * 1e3:.3f} ms "
+        f"({nbytes / avg_norm_s / 1e9:.0f} GB/s)")
+
+    out = {
+        "metric": METRIC,
+        "value": w.n_params / (elapsed / args.steps),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "params": w.n_params, "tensors": K, "block_size": B,
+                   "grad_dtype": "bf16" if w.grad_dtype == synth.BF16 else "f32",
+                   "states": "int8 m / uint8 v, fp32 absmax per block",
+                   "master": "fp32", "norm_accumulation": "f64",
+                   "hyper": {"lr": w.lr, "betas": [w.beta1, w.beta2], "eps": w.eps,
+                             "weight_decay": w.weight_decay, "max_norm": w.max_norm}},
+        "hbm_gbps": round(step_total_bytes / (elapsed / args.steps) / 1e9, 1),
+        "hbm_frac": round(step_total_bytes / (elapsed / args.steps) / 1e9 / PEAK_HBM_GBPS, 4),
+        "bytes_per_param": round(step_total_bytes / w.n_params, 4),
+        "kernels_ms": {"norm_pass": round(avg_norm_s * 1e3, 4),
+                       "adamw8_step": round(avg_step_s * 1e3, 4)},
+        "roofline": {"kernel": "k_adamw8_step", "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+                     "bytes_per_launch": kbytes},
+        "status": st,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(w, n_threads, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

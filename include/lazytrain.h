@@ -1,0 +1,159 @@
+/*
+ * lazytrain.h -- C ABI of the MI355X (gfx950) Hybrid 8-bit optimizer step.
+ *
+ * The operation is the optimizer-side component of LazyTrain's Hybrid 8-bit
+ * operator (paper Sec. 3.5, Hybrid 8-bit operator paragraph): fast gradient
+ * clipping (per-tensor norms, one global norm, one scale) coupled with AdamW
+ * whose first and second moments are stored as block-wise absmax 8-bit codes
+ * over fp32 master weights.  Hyperparameter roles follow the App. C
+ * training-configuration table (beta1, beta2, eps, learning rate, weight
+ * decay, max grad norm; non-finite gradients skip the step).
+ *
+ * Conventions for every entry point:
+ *  - Tensor data, workspace and scalar outputs are DEVICE pointers on the
+ *    current HIP device, owned by the caller.  The library never frees them
+ *    and keeps no reference after the work it enqueued has run.
+ *  - Lists (arrays of pointers and numels) are HOST arrays of length
+ *    n_tensors, read during the call only.
+ *  - All work is enqueued on `stream` (a hipStream_t; NULL is the default
+ *    stream) in call order.  No call synchronizes the host unless its name
+ *    says so (lt_read_status).
+ *  - The return value reports argument and launch problems synchronously.
+ *    Data problems (a non-finite gradient) are reported on the device through
+ *    a status word.  lt_last_error() gives a message for the calling thread.
+ *  - Every tensor is dense and contiguous.  Base pointers of weights,
+ *    gradients and codes must be 16-byte aligned, absmax arrays 4-byte
+ *    aligned, the workspace 256-byte aligned.
+ *  - The workspace holds the tensor-list descriptors the call uploads (and,
+ *    for the norm, its partial sums).  Calls that overlap on the device must
+ *    use different workspaces.
+ *  - Results are bitwise reproducible: they do not depend on the grid size,
+ *    the device occupancy or the stream.
+ */
+#ifndef LAZYTRAIN_H
+#define LAZYTRAIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum lt_err {
+    LT_OK = 0,
+    LT_ERR_INVALID_ARG = 1, /* NULL pointer, size < 1, unsupported block size or dtype, bad hyperparameter */
+    LT_ERR_ALIGNMENT = 2,   /* a base pointer is not aligned as stated above */
+    LT_ERR_WORKSPACE = 3,   /* workspace NULL, misaligned or smaller than the size query returns */
+    LT_ERR_HIP = 4          /* a HIP runtime call failed (device query, copy, launch, sync) */
+} lt_err;
+
+typedef enum lt_status {
+    LT_STATUS_OK = 0,
+    LT_STATUS_NONFINITE = 1 /* the global sum of squares is NaN or infinite */
+} lt_status;
+
+typedef enum lt_dtype {
+    LT_DTYPE_F32 = 0,
+    LT_DTYPE_BF16 = 1
+} lt_dtype;
+
+/* Bytes of device workspace lt_grad_sqnorm needs for this list (descriptors,
+ * one fp64 partial per 8192-element chunk, one fp64 per tensor).  Returns 0 if
+ * n_tensors < 1, numels is NULL or a numel is < 1. */
+size_t lt_grad_sqnorm_workspace_bytes(const int64_t* numels, int n_tensors);
+
+/*
+ * Steps a1-a2: global sum of squares of a list of gradient tensors
+ * (Sec. 3.5: per-tensor norms, then one global aggregate).
+ *   grads[k]       device, numels[k] elements of grad_dtype (LT_DTYPE_F32 or
+ *                  LT_DTYPE_BF16), read only.
+ *   sq_per_tensor  device double[n_tensors] or NULL: S_k, the sum of squares
+ *                  of tensor k.
+ *   sq_total       device double: S = S_0 + S_1 + ... in list order.
+ *   status         device int32: LT_STATUS_NONFINITE if S is NaN or
+ *                  infinite, else LT_STATUS_OK.
+ * Accumulation is fp64 in a fixed order: each tensor is cut into 8192-element
+ * chunks; in a chunk, lane l of 256 adds the squares of elements
+ * 8*(l + 256*r) + e (r = 0..3, e = 0..7) in that order, a 64-lane halving
+ * tree follows, then (W0 + W2) + (W1 + W3) over the four 64-lane groups; a
+ * tensor's chunk sums go round-robin into 256 accumulators in ascending chunk
+ * order, combined by a halving tree.  Results are therefore bitwise fixed.
+ */
+lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_tensors,
+                      int grad_dtype, void* workspace, size_t workspace_bytes,
+                      double* sq_per_tensor, double* sq_total, int32_t* status, void* stream);
+
+/*
+ * Step a3: clip coefficient, device-resident (Sec. 3.5 scale step; App. C max
+ * grad norm).  total_norm = fp32(sqrt(*sq_total)): the fp64 square root, correctly
+ * rounded, then rounded to fp32 (ties to even);
+ * coef = fminf(1, max_norm / (total_norm + 1e-6f)) in fp32.  max_norm must be
+ * > 0; +INFINITY gives coef = 1 exactly.  total_norm may be NULL.
+ */
+lt_err lt_clip_coef(const double* sq_total, float max_norm, float* total_norm, float* coef,
+                    void* stream);
+
+/* Bytes of device workspace lt_hybrid8bit_adamw_step needs for n_tensors
+ * tensors (the uploaded descriptor table).  0 if n_tensors < 1. */
+size_t lt_step_workspace_bytes(int n_tensors);
+
+/*
+ * Steps a4-a10: one fused Hybrid 8-bit AdamW step over a list of tensors
+ * (Sec. 3.5: block-wise 8-bit AdamW states, block-wise scale handling, the
+ * clip scale; App. C: AdamW hyperparameters and the non-finite skip).
+ * For tensor k with n = numels[k] and nb = ceil(n / block_size):
+ *   params[k]   device float[n], read and written (fp32 master weights);
+ *   grads[k]    device grad_dtype[n], read only;
+ *   m_codes[k]  device int8[n]  and m_absmax[k] device float[nb]: first moment,
+ *               value = code * absmax / 127;
+ *   v_codes[k]  device uint8[n] and v_absmax[k] device float[nb]: second
+ *               moment, value = code * absmax / 255.
+ * Blocks are contiguous runs of block_size elements of one tensor (the last
+ * may be partial).  block_size is a power of two in [64, 8192].
+ * Per element, in fp32 with one rounding per operation (fma rounds once,
+ * division and sqrt are correctly rounded):
+ *   m0 = q_m * (A_m / 127), v0 = q_v * (A_v / 255), g = grad * coef,
+ *   m1 = fma(b1, m0, c1 * g), v1 = fma(b2, v0, c2 * (g * g)),
+ *   w1 = fma(-step_size, m1 / fma(sqrt(v1), rbc2, eps), w * decay),
+ * with b1 = fp32(beta1), b2 = fp32(beta2), c1 = fp32(1 - beta1),
+ * c2 = fp32(1 - beta2), decay = fp32(1 - lr * weight_decay),
+ * step_size = fp32(lr / (1 - beta1^step)), rbc2 = fp32(1 / sqrt(1 - beta2^step)),
+ * eps = fp32(eps), each computed on the host in fp64 from the double
+ * arguments.  Per block: A'_m = max |m1|, A'_v = max v1; codes
+ * rint(m1 * (127 / A'_m)) clamped to [-127, 127] and rint(v1 * (255 / A'_v))
+ * clamped to [0, 255] (round half to even); a block whose new absmax or its
+ * reciprocal is not finite stores zero codes and absmax 0.
+ *   step     1-based index t of the step being applied (>= 1).
+ *   lr, weight_decay >= 0; 0 <= beta1, beta2 < 1; eps >= 0; all finite.
+ *   coef     device float or NULL (no clipping, 1.0f).
+ *   status   device int32 or NULL (never skip).  When it holds
+ *            LT_STATUS_NONFINITE the kernel writes nothing: weights, codes and
+ *            absmax stay bitwise unchanged.
+ * The tensors of one call must not overlap.
+ */
+lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int grad_dtype,
+                                int8_t* const* m_codes, float* const* m_absmax,
+                                uint8_t* const* v_codes, float* const* v_absmax,
+                                const int64_t* numels, int n_tensors, int block_size, double lr,
+                                double beta1, double beta2, double eps, double weight_decay,
+                                int64_t step, const float* coef, const int32_t* status,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Copies the device status word to *out and synchronizes `stream` (the only
+ * entry point that blocks the host).  An asynchronous device fault from
+ * earlier work on the stream surfaces here as LT_ERR_HIP. */
+lt_err lt_read_status(const int32_t* status, void* stream, int32_t* out);
+
+/* Caps the number of workgroups of the persistent kernels (0 = size the grid
+ * from the device's compute units and occupancy).  Results do not depend on
+ * it; tests use it to check that.  Process-wide. */
+lt_err lt_set_max_workgroups(int max_workgroups);
+
+/* Message of the last error returned on the calling thread ("" if none). */
+const char* lt_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LAZYTRAIN_H */

@@ -1,0 +1,884 @@
+// lazytrain.hip -- gfx950 kernels and C ABI of the Hybrid 8-bit optimizer step
+// (LazyTrain, Sec. 3.5: fast gradient clipping coupled with block-wise 8-bit
+// AdamW states; App. C: AdamW hyperparameters, max grad norm, non-finite skip).
+//
+// Kernels (all HBM-bound streaming, no MFMA: there is no contraction):
+//   k_sqnorm_chunks  one fp64 sum of squares per 8192-element gradient chunk;
+//                    16-byte loads, wave64 butterfly, 4-wave combine in LDS.
+//   k_sqnorm_finish  per-tensor fixed-order combine of the chunk sums.
+//   k_sqnorm_total   list-order global sum and the non-finite status.
+//   k_clip_coef      fp32(sqrt(S)) (fp64 root, then fp32) and the clip coefficient.
+//   k_adamw8_step    fused dequantize -> AdamW -> block absmax -> requantize.
+// The reduction order and the fp32 operation order are fixed (see
+// include/lazytrain.h); every kernel's result is independent of its grid.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "lazytrain.h"
+
+namespace {
+
+constexpr int kThreads = 256;  // 4 wave64s per workgroup
+constexpr int kChunk = 8192;   // sum-of-squares chunk: 256 lanes x 4 granules x 8 elements
+constexpr int kGranule = 8;    // elements per lane per 16-byte bf16 load
+constexpr int kTile = 2048;    // step elements per workgroup pass when block_size <= 2048
+
+// ------------------------------------------------------------------ errors
+
+thread_local std::string g_last_error;
+
+lt_err fail(lt_err code, const std::string& msg)
+{
+    g_last_error = msg;
+    return code;
+}
+
+#define LT_HIP(call)                                                                    \
+    do {                                                                                \
+        hipError_t e_ = (call);                                                         \
+        if (e_ != hipSuccess)                                                           \
+            return fail(LT_ERR_HIP, std::string(#call) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+// ------------------------------------------------------------- descriptors
+
+// Device-side view of one tensor of the step.
+struct StepTensor {
+    float* w;
+    const void* g;
+    int8_t* mq;
+    float* ma;
+    uint8_t* vq;
+    float* va;
+    int64_t numel;
+    int64_t pad_;
+};
+static_assert(sizeof(StepTensor) == 64, "descriptor is one 64-byte line");
+
+struct StepScalars {
+    float beta1, beta2, eps, c1, c2, decay, step_size, rbc2;
+};
+
+constexpr size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Sum-of-squares workspace: [chunk_prefix K+1][ptr K][numel K] | [partials C][S_k K]
+struct SqLayout {
+    size_t prefix, ptrs, numels, header_bytes, partials, sk, total;
+};
+
+SqLayout sq_layout(int K, int64_t C)
+{
+    SqLayout l;
+    l.prefix = 0;
+    l.ptrs = round_up(sizeof(int64_t) * (K + 1), 64);
+    l.numels = l.ptrs + round_up(sizeof(uint64_t) * K, 64);
+    l.header_bytes = l.numels + round_up(sizeof(int64_t) * K, 64);
+    l.partials = round_up(l.header_bytes, 256);
+    l.sk = l.partials + round_up(sizeof(double) * C, 256);
+    l.total = l.sk + round_up(sizeof(double) * K, 256);
+    return l;
+}
+
+// Step workspace: [tile_prefix K+1][StepTensor K]
+struct StepLayout {
+    size_t prefix, desc, total;
+};
+
+StepLayout step_layout(int K)
+{
+    StepLayout l;
+    l.prefix = 0;
+    l.desc = round_up(sizeof(int64_t) * (K + 1), 64);
+    l.total = round_up(l.desc + sizeof(StepTensor) * K, 256);
+    return l;
+}
+
+// ---------------------------------------------------- descriptor uploads
+//
+// The tensor-list descriptors are packed on the host into a pinned staging
+// slot and copied into the caller's workspace on the caller's stream, so the
+// call never blocks.  A slot is reused only after the event recorded behind
+// its copy has completed.
+
+struct StagingSlot {
+    void* host = nullptr;
+    size_t cap = 0;
+    hipEvent_t done = nullptr;
+    bool pending = false;
+};
+
+constexpr int kSlots = 8;
+constexpr int kMaxDevices = 64;
+
+struct DeviceState {
+    std::mutex mu;
+    StagingSlot slots[kSlots];
+    int next = 0;
+    int cu_count = 0;
+    std::unordered_map<const void*, int> occupancy;  // workgroups per CU, by kernel
+};
+
+DeviceState g_dev[kMaxDevices];
+std::atomic<int> g_max_workgroups{0};
+
+lt_err current_device(int* dev)
+{
+    LT_HIP(hipGetDevice(dev));
+    if (*dev < 0 || *dev >= kMaxDevices)
+        return fail(LT_ERR_HIP, "device index out of range");
+    return LT_OK;
+}
+
+lt_err upload(const void* src, size_t bytes, void* dst, hipStream_t stream)
+{
+    int dev;
+    if (lt_err e = current_device(&dev))
+        return e;
+    DeviceState& ds = g_dev[dev];
+    std::lock_guard<std::mutex> lock(ds.mu);
+    StagingSlot& s = ds.slots[ds.next];
+    ds.next = (ds.next + 1) % kSlots;
+    if (!s.done)
+        LT_HIP(hipEventCreateWithFlags(&s.done, hipEventDisableTiming));
+    if (s.pending) {
+        LT_HIP(hipEventSynchronize(s.done));
+        s.pending = false;
+    }
+    if (s.cap < bytes) {
+        if (s.host)
+            LT_HIP(hipHostFree(s.host));
+        s.host = nullptr;
+        s.cap = 0;
+        size_t cap = round_up(std::max(bytes, size_t(4096)), 4096);
+        LT_HIP(hipHostMalloc(&s.host, cap, hipHostMallocDefault));
+        s.cap = cap;
+    }
+    std::memcpy(s.host, src, bytes);
+    LT_HIP(hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream));
+    LT_HIP(hipEventRecord(s.done, stream));
+    s.pending = true;
+    return LT_OK;
+}
+
+lt_err compute_units(int* cus)
+{
+    int dev;
+    if (lt_err e = current_device(&dev))
+        return e;
+    DeviceState& ds = g_dev[dev];
+    if (ds.cu_count <= 0) {
+        int n = 0;
+        LT_HIP(hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev));
+        ds.cu_count = n > 0 ? n : 1;
+    }
+    *cus = ds.cu_count;
+    return LT_OK;
+}
+
+// Persistent grid: enough workgroups to fill every CU at the kernel's
+// occupancy, never more than there are work units.  The occupancy of each
+// kernel is queried once per device.
+template <typename Kernel>
+lt_err grid_size(Kernel kernel, int64_t units, int* grid)
+{
+    int cus, dev;
+    if (lt_err e = compute_units(&cus))
+        return e;
+    if (lt_err e = current_device(&dev))
+        return e;
+    const void* key = reinterpret_cast<const void*>(kernel);
+    int per_cu = 0;
+    {
+        std::lock_guard<std::mutex> lock(g_dev[dev].mu);
+        auto it = g_dev[dev].occupancy.find(key);
+        if (it != g_dev[dev].occupancy.end())
+            per_cu = it->second;
+    }
+    if (per_cu <= 0) {
+        LT_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0));
+        per_cu = std::max(per_cu, 1);
+        std::lock_guard<std::mutex> lock(g_dev[dev].mu);
+        g_dev[dev].occupancy[key] = per_cu;
+    }
+    int64_t g = int64_t(cus) * std::max(per_cu, 1);
+    int cap = g_max_workgroups.load();
+    if (cap > 0)
+        g = std::min<int64_t>(g, cap);
+    g = std::min<int64_t>(g, units);
+    *grid = int(std::max<int64_t>(g, 1));
+    return LT_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// ============================================================== device code
+
+__device__ inline int64_t i64min(int64_t a, int64_t b) { return a < b ? a : b; }
+__device__ inline int64_t i64max(int64_t a, int64_t b) { return a > b ? a : b; }
+
+__device__ inline float bf16_lo(uint32_t d) { return __uint_as_float(d << 16); }
+__device__ inline float bf16_hi(uint32_t d) { return __uint_as_float(d & 0xFFFF0000u); }
+
+// Eight consecutive gradient values of a full granule, as fp32 (exact).
+__device__ inline void load_granule(const uint16_t* p, float (&x)[8])
+{
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    x[0] = bf16_lo(v.x); x[1] = bf16_hi(v.x);
+    x[2] = bf16_lo(v.y); x[3] = bf16_hi(v.y);
+    x[4] = bf16_lo(v.z); x[5] = bf16_hi(v.z);
+    x[6] = bf16_lo(v.w); x[7] = bf16_hi(v.w);
+}
+
+__device__ inline void load_granule(const float* p, float (&x)[8])
+{
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+__device__ inline float load_one(const uint16_t* p) { return __uint_as_float(uint32_t(*p) << 16); }
+__device__ inline float load_one(const float* p) { return *p; }
+
+// Index of the tensor that holds work unit u: the last k with prefix[k] <= u.
+__device__ inline int find_tensor(const int64_t* __restrict__ prefix, int n_tensors, int64_t u)
+{
+    int lo = 0, hi = n_tensors - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (prefix[mid] <= u)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+// Contiguous, balanced range of work units for this workgroup.
+__device__ inline void unit_range(int64_t units, int64_t* begin, int64_t* end)
+{
+    const int64_t G = gridDim.x, b = blockIdx.x;
+    const int64_t per = units / G, rem = units % G;
+    *begin = b * per + (b < rem ? b : rem);
+    *end = *begin + per + (b < rem ? 1 : 0);
+}
+
+// ------------------------------------------------------- a1: chunk sums
+
+template <typename GT>
+__global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __restrict__ chunk_prefix,
+                                                            const uint64_t* __restrict__ ptrs,
+                                                            const int64_t* __restrict__ numels,
+                                                            int n_tensors, int64_t n_chunks,
+                                                            double* __restrict__ partials)
+{
+    __shared__ double wave_sum[2][4];
+    const int lane = threadIdx.x;
+    const int wave = lane >> 6;
+    int64_t c_begin, c_end;
+    unit_range(n_chunks, &c_begin, &c_end);
+    if (c_begin >= c_end)
+        return;
+    int k = find_tensor(chunk_prefix, n_tensors, c_begin);
+    int buf = 0;
+    for (int64_t c = c_begin; c < c_end; ++c, buf ^= 1) {
+        while (c >= chunk_prefix[k + 1])
+            ++k;
+        const int64_t local = c - chunk_prefix[k];
+        const int64_t n_in = i64min(kChunk, numels[k] - local * kChunk);
+        const GT* base = reinterpret_cast<const GT*>(ptrs[k]) + local * kChunk;
+
+        float x[4][8];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int j0 = kGranule * (lane + kThreads * r);
+            if (j0 + kGranule <= n_in) {
+                load_granule(base + j0, x[r]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    x[r][e] = (j0 + e < n_in) ? load_one(base + j0 + e) : 0.0f;
+            }
+        }
+        // Lane sum in the fixed order.  The square of an fp32 value is exact in
+        // fp64, so fma(x, x, a) is the single rounding of a + x*x.  Positions
+        // past the end hold 0 and leave the non-negative sum unchanged.
+        double a = 0.0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const double xd = double(x[r][e]);
+                a = __builtin_fma(xd, xd, a);
+            }
+        // 64-lane halving tree as a butterfly: lane i adds lane i^o; for i < o
+        // that is a_i + a_(i+o), and addition is commutative.
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1)
+            a = a + __shfl_xor(a, o, 64);
+        if ((lane & 63) == 0)
+            wave_sum[buf][wave] = a;
+        __syncthreads();
+        if (lane == 0)
+            partials[c] = (wave_sum[buf][0] + wave_sum[buf][2]) + (wave_sum[buf][1] + wave_sum[buf][3]);
+        // The other buffer is written next; this one again only after the next
+        // barrier, which lane 0 reaches after its read.
+    }
+}
+
+// ------------------------------------------------- a2: fixed-order finish
+
+__global__ __launch_bounds__(kThreads) void k_sqnorm_finish(const int64_t* __restrict__ chunk_prefix,
+                                                            const double* __restrict__ partials,
+                                                            double* __restrict__ sk)
+{
+    __shared__ double acc[kThreads];
+    const int k = blockIdx.x;
+    const int t = threadIdx.x;
+    const int64_t c0 = chunk_prefix[k];
+    const int64_t nc = chunk_prefix[k + 1] - c0;
+    double b = 0.0;
+    for (int64_t c = t; c < nc; c += kThreads)  // accumulator t takes chunks c = t (mod 256)
+        b = b + partials[c0 + c];
+    acc[t] = b;
+    __syncthreads();
+    if (t < 128) {
+        b = b + acc[t + 128];
+        acc[t] = b;
+    }
+    __syncthreads();
+    if (t < 64) {
+        b = b + acc[t + 64];
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1)
+            b = b + __shfl_xor(b, o, 64);
+        if (t == 0)
+            sk[k] = b;
+    }
+}
+
+__global__ __launch_bounds__(64) void k_sqnorm_total(const double* __restrict__ sk, int n_tensors,
+                                                     double* __restrict__ sk_out,
+                                                     double* __restrict__ sq_total,
+                                                     int32_t* __restrict__ status)
+{
+    if (sk_out)
+        for (int k = threadIdx.x; k < n_tensors; k += 64)
+            sk_out[k] = sk[k];
+    if (threadIdx.x == 0) {
+        double S = 0.0;
+        for (int k = 0; k < n_tensors; ++k)  // list order
+            S = S + sk[k];
+        *sq_total = S;
+        *status = isfinite(S) ? LT_STATUS_OK : LT_STATUS_NONFINITE;
+    }
+}
+
+// ------------------------------------------------------ a3: clip coefficient
+
+// Spacing of fp32 values just above (up) and just below (down) a positive
+// finite fp32 f, as doubles.
+__device__ inline void fp32_spacing(float f, double* up, double* down)
+{
+    const uint32_t u = __float_as_uint(f);
+    const int biased = int(u >> 23);
+    if (biased == 0) {  // subnormal
+        *up = *down = 0x1p-149;
+        return;
+    }
+    *up = ldexp(1.0, biased - 127 - 23);
+    *down = ((u & 0x7FFFFFu) == 0 && biased > 1) ? *up * 0.5 : *up;
+}
+
+// The fp32 value nearest sqrt(S) (ties to even) for any double S >= 0.  An
+// approximate square root is corrected against the exact squares of the two
+// neighbouring fp32 midpoints: a midpoint has at most 25 significant bits, so
+// its square is exact in fp64.
+__device__ float sqrt_fp32_single_rounding(double S)
+{
+    float f = float(sqrt(S));
+    if (!(S > 0.0) || !isfinite(f))
+        return f;  // 0, NaN, +inf, and overflow to +inf (the exact result rounds there too)
+    for (int i = 0; i < 4; ++i) {
+        double up, down;
+        fp32_spacing(f, &up, &down);
+        const double hi = double(f) + 0.5 * up;
+        const double lo = double(f) - 0.5 * down;
+        const bool odd = (__float_as_uint(f) & 1u) != 0;
+        if (S > hi * hi || (S == hi * hi && odd))
+            f = __uint_as_float(__float_as_uint(f) + 1u);
+        else if (__float_as_uint(f) != 0u && (S < lo * lo || (S == lo * lo && odd)))
+            f = __uint_as_float(__float_as_uint(f) - 1u);  // +0 has no smaller neighbour >= 0
+        else
+            break;
+    }
+    return f;
+}
+
+// The norm is defined as fp32(sqrt(S)) with the fp64 square root correctly
+// rounded first: two roundings.  They differ from one rounding only when the
+// fp64 root lands exactly on an fp32 midpoint m; then the conversion ties to
+// even.  The fp64 root is m exactly when m - u/2 < sqrt(S) < m + u/2 (u the fp64
+// ulp of m; sqrt(S) is never itself an fp64 midpoint), i.e. when
+// -m*u < S - m*m <= m*u: m*m is exact (25-bit m), S - m*m is exact (Sterbenz:
+// S is within a factor of two of m*m), m*u is exact, and the u*u/4 terms of the
+// squares lie far below the spacing of S - m*m.
+__device__ float norm_from_sum_of_squares(double S)
+{
+    const float f = sqrt_fp32_single_rounding(S);
+    if (!(S > 0.0) || !isfinite(f))
+        return f;
+    double up, down;
+    fp32_spacing(f, &up, &down);
+    const uint32_t fb = __float_as_uint(f);
+    for (int side = 0; side < 2; ++side) {
+        const double m = side == 0 ? double(f) + 0.5 * up : double(f) - 0.5 * down;
+        if (!(m > 0.0))
+            continue;
+        const int e = int((__double_as_longlong(m) >> 52) & 0x7FF) - 1023;
+        const double u = ldexp(1.0, e - 52);
+        const double d = S - m * m;
+        if (d > -m * u && d <= m * u) {
+            const uint32_t lo = side == 0 ? fb : fb - 1u;  // fp32 neighbours lo, lo + 1 of m
+            return __uint_as_float((lo & 1u) ? lo + 1u : lo);
+        }
+    }
+    return f;
+}
+
+__global__ __launch_bounds__(64) void k_clip_coef(const double* __restrict__ sq_total, float max_norm,
+                                                  float* __restrict__ total_norm,
+                                                  float* __restrict__ coef)
+{
+    if (threadIdx.x != 0)
+        return;
+    const float norm = norm_from_sum_of_squares(*sq_total);
+    const float c = max_norm / (norm + 1e-6f);
+    if (total_norm)
+        *total_norm = norm;
+    *coef = fminf(1.0f, c);
+}
+
+// ------------------------------------------------------ a4-a10: fused step
+
+__device__ inline float wave_max_xor(float x, int width)
+{
+    for (int o = width >> 1; o >= 1; o >>= 1)
+        x = fmaxf(x, __shfl_xor(x, o, 64));
+    return x;
+}
+
+template <typename GT, int B>
+__global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restrict__ tile_prefix,
+                                                          const StepTensor* __restrict__ desc,
+                                                          int n_tensors, int64_t n_tiles,
+                                                          StepScalars s,
+                                                          const float* __restrict__ coef_ptr,
+                                                          const int32_t* __restrict__ status_ptr)
+{
+    constexpr int TILE = B > kTile ? B : kTile;  // elements per workgroup pass
+    constexpr int GR = TILE / kTile;             // granules per lane
+    constexpr int L = (B / kGranule) < kThreads ? (B / kGranule) : kThreads;  // lanes per block
+    constexpr int WAVES_PER_BLOCK = L > 64 ? L / 64 : 1;
+    __shared__ float red[2][2][4];  // [buffer][m, v][wave]
+
+    if (status_ptr && *status_ptr == LT_STATUS_NONFINITE)
+        return;  // skipped step: nothing is written
+    const float coef = coef_ptr ? *coef_ptr : 1.0f;
+    const int lane = threadIdx.x;
+    const int wave = lane >> 6;
+
+    int64_t t_begin, t_end;
+    unit_range(n_tiles, &t_begin, &t_end);
+    if (t_begin >= t_end)
+        return;
+    int k = find_tensor(tile_prefix, n_tensors, t_begin);
+    int buf = 0;
+    for (int64_t t = t_begin; t < t_end; ++t, buf ^= 1) {
+        while (t >= tile_prefix[k + 1])
+            ++k;
+        const StepTensor d = desc[k];
+        const int64_t e0 = (t - tile_prefix[k]) * TILE;
+        const int64_t n_valid = i64min(TILE, d.numel - e0);
+        const GT* __restrict__ gp = static_cast<const GT*>(d.g);
+
+        float m1[GR][8], v1[GR][8];
+        float amax_m = 0.0f, amax_v = 0.0f;
+#pragma unroll
+        for (int j = 0; j < GR; ++j) {
+            const int o = kGranule * (lane + kThreads * j);  // offset in the tile
+            const int nv = int(i64min(i64max(n_valid - o, 0), kGranule));
+            const int64_t ei = e0 + o;  // element index in the tensor
+            float w[8], g[8], qm[8], qv[8];
+            float a_m = 0.0f, a_v = 0.0f;
+            if (nv > 0) {
+                const int64_t blk = ei / B;
+                a_m = d.ma[blk];
+                a_v = d.va[blk];
+            }
+            if (nv == kGranule) {
+                const float4 wa = *reinterpret_cast<const float4*>(d.w + ei);
+                const float4 wb = *reinterpret_cast<const float4*>(d.w + ei + 4);
+                w[0] = wa.x; w[1] = wa.y; w[2] = wa.z; w[3] = wa.w;
+                w[4] = wb.x; w[5] = wb.y; w[6] = wb.z; w[7] = wb.w;
+                load_granule(gp + ei, g);
+                const uint2 cm = *reinterpret_cast<const uint2*>(d.mq + ei);
+                const uint2 cv = *reinterpret_cast<const uint2*>(d.vq + ei);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    qm[e] = float(int8_t(cm.x >> (8 * e)));
+                    qm[e + 4] = float(int8_t(cm.y >> (8 * e)));
+                    qv[e] = float((cv.x >> (8 * e)) & 0xFFu);
+                    qv[e + 4] = float((cv.y >> (8 * e)) & 0xFFu);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const bool ok = e < nv;
+                    w[e] = ok ? d.w[ei + e] : 0.0f;
+                    g[e] = ok ? load_one(gp + ei + e) : 0.0f;
+                    qm[e] = ok ? float(d.mq[ei + e]) : 0.0f;
+                    qv[e] = ok ? float(d.vq[ei + e]) : 0.0f;
+                }
+            }
+            const float step_m = a_m / 127.0f;
+            const float step_v = a_v / 255.0f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float m0 = qm[e] * step_m;
+                const float v0 = qv[e] * step_v;
+                const float gc = g[e] * coef;
+                const float m = __builtin_fmaf(s.beta1, m0, s.c1 * gc);
+                const float v = __builtin_fmaf(s.beta2, v0, s.c2 * (gc * gc));
+                const float den = __builtin_fmaf(sqrtf(v), s.rbc2, s.eps);
+                w[e] = __builtin_fmaf(-s.step_size, m / den, w[e] * s.decay);
+                m1[j][e] = m;
+                v1[j][e] = v;
+                if (e < nv) {
+                    amax_m = fmaxf(amax_m, fabsf(m));
+                    amax_v = fmaxf(amax_v, v);
+                }
+            }
+            if (nv == kGranule) {
+                *reinterpret_cast<float4*>(d.w + ei) = make_float4(w[0], w[1], w[2], w[3]);
+                *reinterpret_cast<float4*>(d.w + ei + 4) = make_float4(w[4], w[5], w[6], w[7]);
+            } else {
+                for (int e = 0; e < nv; ++e)
+                    d.w[ei + e] = w[e];
+            }
+        }
+
+        // Block absmax (max is exact and order-free).
+        amax_m = wave_max_xor(amax_m, L < 64 ? L : 64);
+        amax_v = wave_max_xor(amax_v, L < 64 ? L : 64);
+        if constexpr (L > 64) {
+            if ((lane & 63) == 0) {
+                red[buf][0][wave] = amax_m;
+                red[buf][1][wave] = amax_v;
+            }
+            __syncthreads();
+            const int first = (wave / WAVES_PER_BLOCK) * WAVES_PER_BLOCK;
+            amax_m = red[buf][0][first];
+            amax_v = red[buf][1][first];
+#pragma unroll
+            for (int i = 1; i < WAVES_PER_BLOCK; ++i) {
+                amax_m = fmaxf(amax_m, red[buf][0][first + i]);
+                amax_v = fmaxf(amax_v, red[buf][1][first + i]);
+            }
+        }
+        const float inv_m = 127.0f / amax_m;
+        const float inv_v = 255.0f / amax_v;
+        const bool ok_m = isfinite(amax_m) && isfinite(inv_m);
+        const bool ok_v = isfinite(amax_v) && isfinite(inv_v);
+
+#pragma unroll
+        for (int j = 0; j < GR; ++j) {
+            const int o = kGranule * (lane + kThreads * j);
+            const int nv = int(i64min(i64max(n_valid - o, 0), kGranule));
+            const int64_t ei = e0 + o;
+            uint32_t pm[2] = {0u, 0u}, pv[2] = {0u, 0u};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float qmf = fminf(fmaxf(rintf(m1[j][e] * inv_m), -127.0f), 127.0f);
+                const float qvf = fminf(fmaxf(rintf(v1[j][e] * inv_v), 0.0f), 255.0f);
+                const uint32_t bm = ok_m ? (uint32_t(int32_t(qmf)) & 0xFFu) : 0u;
+                const uint32_t bv = ok_v ? uint32_t(int32_t(qvf)) : 0u;
+                pm[e >> 2] |= bm << (8 * (e & 3));
+                pv[e >> 2] |= bv << (8 * (e & 3));
+            }
+            if (nv == kGranule) {
+                *reinterpret_cast<uint2*>(d.mq + ei) = make_uint2(pm[0], pm[1]);
+                *reinterpret_cast<uint2*>(d.vq + ei) = make_uint2(pv[0], pv[1]);
+            } else {
+                for (int e = 0; e < nv; ++e) {
+                    d.mq[ei + e] = int8_t((pm[e >> 2] >> (8 * (e & 3))) & 0xFFu);
+                    d.vq[ei + e] = uint8_t((pv[e >> 2] >> (8 * (e & 3))) & 0xFFu);
+                }
+            }
+            // The first lane of each block writes its scales.
+            if (j == 0 && nv > 0 && (lane % L) == 0) {
+                const int64_t blk = ei / B;
+                d.ma[blk] = ok_m ? amax_m : 0.0f;
+                d.va[blk] = ok_v ? amax_v : 0.0f;
+            }
+        }
+    }
+}
+
+// ================================================================ host side
+
+template <typename GT, int B>
+lt_err launch_step_b(const int64_t* prefix, const StepTensor* desc, int K, int64_t tiles,
+                     const StepScalars& s, const float* coef, const int32_t* status,
+                     hipStream_t stream)
+{
+    int grid;
+    if (lt_err e = grid_size(k_adamw8_step<GT, B>, tiles, &grid))
+        return e;
+    k_adamw8_step<GT, B><<<grid, kThreads, 0, stream>>>(prefix, desc, K, tiles, s, coef, status);
+    LT_HIP(hipGetLastError());
+    return LT_OK;
+}
+
+template <typename GT>
+lt_err launch_step(int B, const int64_t* prefix, const StepTensor* desc, int K, int64_t tiles,
+                   const StepScalars& s, const float* coef, const int32_t* status,
+                   hipStream_t stream)
+{
+    switch (B) {
+    case 64: return launch_step_b<GT, 64>(prefix, desc, K, tiles, s, coef, status, stream);
+    case 128: return launch_step_b<GT, 128>(prefix, desc, K, tiles, s, coef, status, stream);
+    case 256: return launch_step_b<GT, 256>(prefix, desc, K, tiles, s, coef, status, stream);
+    case 512: return launch_step_b<GT, 512>(prefix, desc, K, tiles, s, coef, status, stream);
+    case 1024: return launch_step_b<GT, 1024>(prefix, desc, K, tiles, s, coef, status, stream);
+    case 2048: return launch_step_b<GT, 2048>(prefix, desc, K, tiles, s, coef, status, stream);
+    case 4096: return launch_step_b<GT, 4096>(prefix, desc, K, tiles, s, coef, status, stream);
+    case 8192: return launch_step_b<GT, 8192>(prefix, desc, K, tiles, s, coef, status, stream);
+    default: return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
+    }
+}
+
+int64_t sq_chunks_of(const int64_t* numels, int K)
+{
+    int64_t C = 0;
+    for (int k = 0; k < K; ++k)
+        C += (numels[k] + kChunk - 1) / kChunk;
+    return C;
+}
+
+bool valid_list(const int64_t* numels, int K)
+{
+    if (K < 1 || !numels)
+        return false;
+    for (int k = 0; k < K; ++k)
+        if (numels[k] < 1)
+            return false;
+    return true;
+}
+
+}  // namespace
+
+// =================================================================== C ABI
+
+extern "C" {
+
+size_t lt_grad_sqnorm_workspace_bytes(const int64_t* numels, int n_tensors)
+{
+    if (!valid_list(numels, n_tensors))
+        return 0;
+    return sq_layout(n_tensors, sq_chunks_of(numels, n_tensors)).total;
+}
+
+lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_tensors,
+                      int grad_dtype, void* workspace, size_t workspace_bytes,
+                      double* sq_per_tensor, double* sq_total, int32_t* status, void* stream)
+{
+    g_last_error.clear();
+    if (!grads || !valid_list(numels, n_tensors))
+        return fail(LT_ERR_INVALID_ARG, "grads/numels must hold n_tensors >= 1 entries with numel >= 1");
+    if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
+        return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
+    if (!sq_total || !status)
+        return fail(LT_ERR_INVALID_ARG, "sq_total and status must not be NULL");
+    if (!aligned(sq_total, 8) || !aligned(status, 4) || (sq_per_tensor && !aligned(sq_per_tensor, 8)))
+        return fail(LT_ERR_ALIGNMENT, "scalar outputs must be naturally aligned");
+    for (int k = 0; k < n_tensors; ++k) {
+        if (!grads[k])
+            return fail(LT_ERR_INVALID_ARG, "grads[" + std::to_string(k) + "] is NULL");
+        if (!aligned(grads[k], 16))
+            return fail(LT_ERR_ALIGNMENT, "grads[" + std::to_string(k) + "] is not 16-byte aligned");
+    }
+    const int K = n_tensors;
+    const int64_t C = sq_chunks_of(numels, K);
+    const SqLayout lay = sq_layout(K, C);
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < lay.total)
+        return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
+                                          std::to_string(lay.total) + " bytes");
+
+    std::vector<uint8_t> header(lay.header_bytes, 0);
+    auto* prefix = reinterpret_cast<int64_t*>(header.data() + lay.prefix);
+    auto* ptrs = reinterpret_cast<uint64_t*>(header.data() + lay.ptrs);
+    auto* ns = reinterpret_cast<int64_t*>(header.data() + lay.numels);
+    prefix[0] = 0;
+    for (int k = 0; k < K; ++k) {
+        prefix[k + 1] = prefix[k] + (numels[k] + kChunk - 1) / kChunk;
+        ptrs[k] = reinterpret_cast<uint64_t>(grads[k]);
+        ns[k] = numels[k];
+    }
+    auto* ws = static_cast<uint8_t*>(workspace);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (lt_err e = upload(header.data(), header.size(), ws, st))
+        return e;
+    const auto* d_prefix = reinterpret_cast<const int64_t*>(ws + lay.prefix);
+    const auto* d_ptrs = reinterpret_cast<const uint64_t*>(ws + lay.ptrs);
+    const auto* d_numels = reinterpret_cast<const int64_t*>(ws + lay.numels);
+    auto* d_partials = reinterpret_cast<double*>(ws + lay.partials);
+    auto* d_sk = reinterpret_cast<double*>(ws + lay.sk);
+
+    int grid;
+    if (grad_dtype == LT_DTYPE_BF16) {
+        if (lt_err e = grid_size(k_sqnorm_chunks<uint16_t>, C, &grid))
+            return e;
+        k_sqnorm_chunks<uint16_t><<<grid, kThreads, 0, st>>>(d_prefix, d_ptrs, d_numels, K, C,
+                                                             d_partials);
+    } else {
+        if (lt_err e = grid_size(k_sqnorm_chunks<float>, C, &grid))
+            return e;
+        k_sqnorm_chunks<float><<<grid, kThreads, 0, st>>>(d_prefix, d_ptrs, d_numels, K, C,
+                                                          d_partials);
+    }
+    LT_HIP(hipGetLastError());
+    k_sqnorm_finish<<<K, kThreads, 0, st>>>(d_prefix, d_partials, d_sk);
+    LT_HIP(hipGetLastError());
+    k_sqnorm_total<<<1, 64, 0, st>>>(d_sk, K, sq_per_tensor, sq_total, status);
+    LT_HIP(hipGetLastError());
+    return LT_OK;
+}
+
+lt_err lt_clip_coef(const double* sq_total, float max_norm, float* total_norm, float* coef,
+                    void* stream)
+{
+    g_last_error.clear();
+    if (!sq_total || !coef)
+        return fail(LT_ERR_INVALID_ARG, "sq_total and coef must not be NULL");
+    if (!(max_norm > 0.0f))
+        return fail(LT_ERR_INVALID_ARG, "max_norm must be > 0 (+inf disables clipping)");
+    if (!aligned(sq_total, 8) || !aligned(coef, 4) || (total_norm && !aligned(total_norm, 4)))
+        return fail(LT_ERR_ALIGNMENT, "scalar arguments must be naturally aligned");
+    k_clip_coef<<<1, 64, 0, static_cast<hipStream_t>(stream)>>>(sq_total, max_norm, total_norm,
+                                                                 coef);
+    LT_HIP(hipGetLastError());
+    return LT_OK;
+}
+
+size_t lt_step_workspace_bytes(int n_tensors)
+{
+    return n_tensors < 1 ? 0 : step_layout(n_tensors).total;
+}
+
+lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int grad_dtype,
+                                int8_t* const* m_codes, float* const* m_absmax,
+                                uint8_t* const* v_codes, float* const* v_absmax,
+                                const int64_t* numels, int n_tensors, int block_size, double lr,
+                                double beta1, double beta2, double eps, double weight_decay,
+                                int64_t step, const float* coef, const int32_t* status,
+                                void* workspace, size_t workspace_bytes, void* stream)
+{
+    g_last_error.clear();
+    if (!params || !grads || !m_codes || !m_absmax || !v_codes || !v_absmax ||
+        !valid_list(numels, n_tensors))
+        return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 1 entries with numel >= 1");
+    if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
+        return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
+    if (block_size < 64 || block_size > 8192 || (block_size & (block_size - 1)))
+        return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
+    if (!(std::isfinite(lr) && lr >= 0.0) || !(std::isfinite(weight_decay) && weight_decay >= 0.0) ||
+        !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) ||
+        !(std::isfinite(eps) && eps >= 0.0) || step < 1)
+        return fail(LT_ERR_INVALID_ARG,
+                    "need finite lr, weight_decay, eps >= 0, 0 <= beta1, beta2 < 1 and step >= 1");
+    if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)))
+        return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned");
+    const int K = n_tensors;
+    for (int k = 0; k < K; ++k) {
+        const std::string at = "[" + std::to_string(k) + "]";
+        if (!params[k] || !grads[k] || !m_codes[k] || !m_absmax[k] || !v_codes[k] || !v_absmax[k])
+            return fail(LT_ERR_INVALID_ARG, "NULL tensor pointer at index " + at);
+        if (!aligned(params[k], 16) || !aligned(grads[k], 16) || !aligned(m_codes[k], 16) ||
+            !aligned(v_codes[k], 16))
+            return fail(LT_ERR_ALIGNMENT, "params/grads/codes" + at + " must be 16-byte aligned");
+        if (!aligned(m_absmax[k], 4) || !aligned(v_absmax[k], 4))
+            return fail(LT_ERR_ALIGNMENT, "absmax" + at + " must be 4-byte aligned");
+    }
+    const StepLayout lay = step_layout(K);
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < lay.total)
+        return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
+                                          std::to_string(lay.total) + " bytes");
+
+    const int64_t tile = std::max<int64_t>(block_size, kTile);
+    std::vector<uint8_t> host(lay.total, 0);
+    auto* prefix = reinterpret_cast<int64_t*>(host.data() + lay.prefix);
+    auto* desc = reinterpret_cast<StepTensor*>(host.data() + lay.desc);
+    prefix[0] = 0;
+    for (int k = 0; k < K; ++k) {
+        prefix[k + 1] = prefix[k] + (numels[k] + tile - 1) / tile;
+        desc[k] = StepTensor{params[k], grads[k], m_codes[k], m_absmax[k], v_codes[k], v_absmax[k],
+                             numels[k], 0};
+    }
+    const int64_t tiles = prefix[K];
+
+    StepScalars s;
+    const double t = double(step);
+    s.beta1 = float(beta1);
+    s.beta2 = float(beta2);
+    s.eps = float(eps);
+    s.c1 = float(1.0 - beta1);
+    s.c2 = float(1.0 - beta2);
+    s.decay = float(1.0 - lr * weight_decay);
+    s.step_size = float(lr / (1.0 - std::pow(beta1, t)));
+    s.rbc2 = float(1.0 / std::sqrt(1.0 - std::pow(beta2, t)));
+
+    auto* ws = static_cast<uint8_t*>(workspace);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (lt_err e = upload(host.data(), host.size(), ws, st))
+        return e;
+    const auto* d_prefix = reinterpret_cast<const int64_t*>(ws + lay.prefix);
+    const auto* d_desc = reinterpret_cast<const StepTensor*>(ws + lay.desc);
+    if (grad_dtype == LT_DTYPE_BF16)
+        return launch_step<uint16_t>(block_size, d_prefix, d_desc, K, tiles, s, coef, status, st);
+    return launch_step<float>(block_size, d_prefix, d_desc, K, tiles, s, coef, status, st);
+}
+
+lt_err lt_read_status(const int32_t* status, void* stream, int32_t* out)
+{
+    g_last_error.clear();
+    if (!status || !out)
+        return fail(LT_ERR_INVALID_ARG, "status and out must not be NULL");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    LT_HIP(hipMemcpyAsync(out, status, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+    LT_HIP(hipStreamSynchronize(st));
+    return LT_OK;
+}
+
+lt_err lt_set_max_workgroups(int max_workgroups)
+{
+    g_last_error.clear();
+    if (max_workgroups < 0)
+        return fail(LT_ERR_INVALID_ARG, "max_workgroups must be >= 0");
+    g_max_workgroups.store(max_workgroups);
+    return LT_OK;
+}
+
+const char* lt_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

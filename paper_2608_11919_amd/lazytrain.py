@@ -1,0 +1,276 @@
+"""Python binding of liblazytrain.so (include/lazytrain.h), argument marshalling only.
+
+Every function has the name of the C entry point it calls.  Tensors are
+torch tensors on one HIP device; the binding checks devices, dtypes, sizes and
+contiguity, passes ``data_ptr()``s and the stream handle, and raises on any
+error code.  bf16 gradients may be torch.bfloat16 tensors (or raw bf16 bits in
+int16/uint16 tensors).  All arithmetic runs in the HIP kernels; if the library
+is not built this module raises instead of falling back to anything.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblazytrain.so")
+
+LT_OK, LT_ERR_INVALID_ARG, LT_ERR_ALIGNMENT, LT_ERR_WORKSPACE, LT_ERR_HIP = range(5)
+LT_STATUS_OK, LT_STATUS_NONFINITE = 0, 1
+LT_DTYPE_F32, LT_DTYPE_BF16 = 0, 1
+ERROR_NAMES = {1: "LT_ERR_INVALID_ARG", 2: "LT_ERR_ALIGNMENT", 3: "LT_ERR_WORKSPACE",
+               4: "LT_ERR_HIP"}
+
+_lib = None
+
+
+class LazyTrainError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERROR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+def lib() -> ctypes.CDLL:
+    """Loads liblazytrain.so, raising if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                          "(there is no fallback path)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64p = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)
+    vpp = ctypes.POINTER(ctypes.c_void_p)
+    L.lt_grad_sqnorm_workspace_bytes.argtypes = [i64p, ctypes.c_int]
+    L.lt_grad_sqnorm_workspace_bytes.restype = ctypes.c_size_t
+    L.lt_grad_sqnorm.argtypes = [vpp, i64p, ctypes.c_int, ctypes.c_int, vp, ctypes.c_size_t,
+                                 vp, vp, vp, vp]
+    L.lt_clip_coef.argtypes = [vp, ctypes.c_float, vp, vp, vp]
+    L.lt_step_workspace_bytes.argtypes = [ctypes.c_int]
+    L.lt_step_workspace_bytes.restype = ctypes.c_size_t
+    L.lt_hybrid8bit_adamw_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, i64p,
+                                           ctypes.c_int, ctypes.c_int] + [ctypes.c_double] * 5 + [
+                                               ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp]
+    L.lt_read_status.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32)]
+    L.lt_set_max_workgroups.argtypes = [ctypes.c_int]
+    L.lt_last_error.argtypes = []
+    L.lt_last_error.restype = ctypes.c_char_p
+    for name in ("lt_grad_sqnorm", "lt_clip_coef", "lt_hybrid8bit_adamw_step", "lt_read_status",
+                 "lt_set_max_workgroups"):
+        getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(rc: int) -> None:
+    if rc != LT_OK:
+        raise LazyTrainError(rc, lib().lt_last_error().decode())
+
+
+def _stream_handle(stream, device) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ptr_array(tensors) -> ctypes.Array:
+    return (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+
+
+def _numel_array(tensors) -> ctypes.Array:
+    return (ctypes.c_int64 * len(tensors))(*[t.numel() for t in tensors])
+
+
+def _grad_dtype(grads) -> int:
+    dt = grads[0].dtype
+    if any(g.dtype != dt for g in grads):
+        raise TypeError("all gradients must share one dtype")
+    if dt == torch.float32:
+        return LT_DTYPE_F32
+    if dt in (torch.bfloat16, torch.int16, torch.uint16):
+        return LT_DTYPE_BF16
+    raise TypeError(f"gradient dtype must be float32 or bfloat16, got {dt}")
+
+
+def _check_tensors(tensors, device, dtype=None, what="tensor"):
+    for i, t in enumerate(tensors):
+        if t.device != device:
+            raise ValueError(f"{what}[{i}] is on {t.device}, expected {device}")
+        if not t.is_contiguous():
+            raise ValueError(f"{what}[{i}] must be contiguous")
+        if dtype is not None and t.dtype != dtype:
+            raise TypeError(f"{what}[{i}] has dtype {t.dtype}, expected {dtype}")
+
+
+def _scalar(t: Optional[torch.Tensor], device, dtype, what) -> int:
+    if t is None:
+        return 0
+    if t.device != device or t.dtype != dtype or t.numel() < 1:
+        raise ValueError(f"{what} must be a {dtype} tensor on {device}")
+    return t.data_ptr()
+
+
+_workspaces = {}
+
+
+def _workspace(device, nbytes: int, workspace: Optional[torch.Tensor], stream) -> torch.Tensor:
+    if workspace is not None:
+        if workspace.device != device or workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError(f"workspace must hold {nbytes} bytes on {device}")
+        return workspace
+    key = (device, _stream_handle(stream, device))
+    ws = _workspaces.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(nbytes, 4096), dtype=torch.uint8, device=device)
+        _workspaces[key] = ws
+    return ws
+
+
+# ------------------------------------------------------------------ entry points
+
+def lt_grad_sqnorm_workspace_bytes(numels: Sequence[int]) -> int:
+    arr = (ctypes.c_int64 * len(numels))(*numels)
+    return int(lib().lt_grad_sqnorm_workspace_bytes(arr, len(numels)))
+
+
+def lt_step_workspace_bytes(n_tensors: int) -> int:
+    return int(lib().lt_step_workspace_bytes(n_tensors))
+
+
+def lt_grad_sqnorm(grads: Sequence[torch.Tensor], sq_total: torch.Tensor, status: torch.Tensor,
+                   sq_per_tensor: Optional[torch.Tensor] = None,
+                   workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Steps a1-a2: S_k, S and the non-finite status into device tensors (float64,
+    float64[1], int32[1])."""
+    if not grads:
+        raise ValueError("empty gradient list")
+    device = grads[0].device
+    _check_tensors(grads, device, what="grads")
+    gdt = _grad_dtype(grads)
+    if sq_per_tensor is not None and sq_per_tensor.numel() < len(grads):
+        raise ValueError("sq_per_tensor needs one float64 per tensor")
+    nbytes = lt_grad_sqnorm_workspace_bytes([g.numel() for g in grads])
+    ws = _workspace(device, nbytes, workspace, stream)
+    _check(lib().lt_grad_sqnorm(
+        _ptr_array(grads), _numel_array(grads), len(grads), gdt, ws.data_ptr(),
+        ws.numel() * ws.element_size(), _scalar(sq_per_tensor, device, torch.float64, "sq_per_tensor"),
+        _scalar(sq_total, device, torch.float64, "sq_total"),
+        _scalar(status, device, torch.int32, "status"), _stream_handle(stream, device)))
+
+
+def lt_clip_coef(sq_total: torch.Tensor, max_norm: float, coef: torch.Tensor,
+                 total_norm: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Step a3: norm and clip coefficient into device float32 tensors."""
+    device = sq_total.device
+    _check(lib().lt_clip_coef(_scalar(sq_total, device, torch.float64, "sq_total"),
+                              float(max_norm),
+                              _scalar(total_norm, device, torch.float32, "total_norm"),
+                              _scalar(coef, device, torch.float32, "coef"),
+                              _stream_handle(stream, device)))
+
+
+def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Tensor],
+                             m_codes: Sequence[torch.Tensor], m_absmax: Sequence[torch.Tensor],
+                             v_codes: Sequence[torch.Tensor], v_absmax: Sequence[torch.Tensor],
+                             block_size: int, lr: float, beta1: float, beta2: float, eps: float,
+                             weight_decay: float, step: int,
+                             coef: Optional[torch.Tensor] = None,
+                             status: Optional[torch.Tensor] = None,
+                             workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Steps a4-a10 in place on params, codes and absmax (see include/lazytrain.h)."""
+    k = len(params)
+    if k == 0 or not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) ==
+                      len(v_absmax) == k):
+        raise ValueError("tensor lists must be non-empty and of equal length")
+    device = params[0].device
+    _check_tensors(params, device, torch.float32, "params")
+    _check_tensors(grads, device, what="grads")
+    _check_tensors(m_codes, device, torch.int8, "m_codes")
+    _check_tensors(v_codes, device, torch.uint8, "v_codes")
+    _check_tensors(m_absmax, device, torch.float32, "m_absmax")
+    _check_tensors(v_absmax, device, torch.float32, "v_absmax")
+    gdt = _grad_dtype(grads)
+    for i in range(k):
+        n = params[i].numel()
+        nb = -(-n // block_size)
+        if grads[i].numel() != n or m_codes[i].numel() != n or v_codes[i].numel() != n:
+            raise ValueError(f"tensor {i}: params, grads and codes must have {n} elements")
+        if m_absmax[i].numel() < nb or v_absmax[i].numel() < nb:
+            raise ValueError(f"tensor {i}: absmax arrays need ceil({n}/{block_size}) = {nb} entries")
+    ws = _workspace(device, lt_step_workspace_bytes(k), workspace, stream)
+    _check(lib().lt_hybrid8bit_adamw_step(
+        _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
+        _ptr_array(v_codes), _ptr_array(v_absmax), _numel_array(params), k, int(block_size),
+        float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
+        _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
+        ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
+
+
+def lt_read_status(status: torch.Tensor, stream=None) -> int:
+    """Reads the device status word (synchronizes the stream)."""
+    out = ctypes.c_int32()
+    device = status.device
+    _check(lib().lt_read_status(_scalar(status, device, torch.int32, "status"),
+                                _stream_handle(stream, device), ctypes.byref(out)))
+    return out.value
+
+
+def lt_set_max_workgroups(max_workgroups: int) -> None:
+    _check(lib().lt_set_max_workgroups(int(max_workgroups)))
+
+
+# ------------------------------------------------------------- optimizer object
+
+class Hybrid8bitAdamW:
+    """Holds the 8-bit states of a list of fp32 master tensors and runs one clipped
+    step per call: lt_grad_sqnorm -> lt_clip_coef -> lt_hybrid8bit_adamw_step, all
+    enqueued on one stream without a host synchronization.  The caller owns the
+    skip/abort policy: ``last_status()`` reads the status word of the last step."""
+
+    def __init__(self, params: Sequence[torch.Tensor], lr: float = 1e-5,
+                 betas=(0.9, 0.999), eps: float = 1e-8, weight_decay: float = 0.01,
+                 max_norm: float = 1.0, block_size: int = 4096):
+        self.params = list(params)
+        if not self.params:
+            raise ValueError("no parameters")
+        dev = self.params[0].device
+        self.lr, self.betas, self.eps, self.weight_decay = lr, betas, eps, weight_decay
+        self.max_norm, self.block_size = max_norm, block_size
+        self.m_codes = [torch.zeros(p.numel(), dtype=torch.int8, device=dev) for p in self.params]
+        self.v_codes = [torch.zeros(p.numel(), dtype=torch.uint8, device=dev) for p in self.params]
+        nb = [-(-p.numel() // block_size) for p in self.params]
+        self.m_absmax = [torch.zeros(n, dtype=torch.float32, device=dev) for n in nb]
+        self.v_absmax = [torch.zeros(n, dtype=torch.float32, device=dev) for n in nb]
+        self.sq_total = torch.zeros(1, dtype=torch.float64, device=dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.coef = torch.ones(1, dtype=torch.float32, device=dev)
+        self.total_norm = torch.zeros(1, dtype=torch.float32, device=dev)
+        self.step_count = 0  # steps applied (skipped steps do not count)
+        self._unchecked = False
+
+    def step(self, grads: Sequence[torch.Tensor], stream=None) -> None:
+        if self._unchecked:
+            self.last_status(stream)  # the bias correction needs the true step count
+        t = self.step_count + 1
+        lt_grad_sqnorm(grads, self.sq_total, self.status, stream=stream)
+        clip = self.max_norm if self.max_norm is not None else math.inf
+        lt_clip_coef(self.sq_total, clip, self.coef, self.total_norm, stream=stream)
+        lt_hybrid8bit_adamw_step(self.params, grads, self.m_codes, self.m_absmax, self.v_codes,
+                                 self.v_absmax, self.block_size, self.lr, self.betas[0],
+                                 self.betas[1], self.eps, self.weight_decay, t, coef=self.coef,
+                                 status=self.status, stream=stream)
+        self.step_count = t
+        self._unchecked = True
+
+    def last_status(self, stream=None) -> int:
+        """Reads the status of the last step (synchronizes the stream); a skipped step
+        is taken off the step count once."""
+        st = lt_read_status(self.status, stream)
+        if self._unchecked and st == LT_STATUS_NONFINITE:
+            self.step_count -= 1
+        self._unchecked = False
+        return st
