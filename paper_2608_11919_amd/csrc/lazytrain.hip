@@ -229,26 +229,70 @@ __device__ inline int64_t i64max(int64_t a, int64_t b) { return a > b ? a : b; }
 __device__ inline float bf16_lo(uint32_t d) { return __uint_as_float(d << 16); }
 __device__ inline float bf16_hi(uint32_t d) { return __uint_as_float(d & 0xFFFF0000u); }
 
-// Eight consecutive gradient values of a full granule, as fp32 (exact).
-__device__ inline void load_granule(const uint16_t* p, float (&x)[8])
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load that asks the memory system not to keep the line (streaming).
+__device__ inline uint4 load16_stream(const void* p)
 {
-    const uint4 v = *reinterpret_cast<const uint4*>(p);
-    x[0] = bf16_lo(v.x); x[1] = bf16_hi(v.x);
-    x[2] = bf16_lo(v.y); x[3] = bf16_hi(v.y);
-    x[4] = bf16_lo(v.z); x[5] = bf16_hi(v.z);
-    x[6] = bf16_lo(v.w); x[7] = bf16_hi(v.w);
+    const u32x4 v = __builtin_nontemporal_load(static_cast<const u32x4*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-__device__ inline void load_granule(const float* p, float (&x)[8])
+__device__ inline uint4 load16(const void* p) { return *static_cast<const uint4*>(p); }
+
+// Raw bits of one gradient element (bf16: 16 bits, fp32: 32 bits).
+__device__ inline uint32_t grad_bits(const uint16_t* p) { return *p; }
+__device__ inline uint32_t grad_bits(const float* p) { return __float_as_uint(*p); }
+
+// Packed 16-byte words holding the 8 gradients of one granule: bf16 needs one
+// word, fp32 two.  Unpacking is exact (bf16 is the top half of an fp32).
+template <typename GT>
+struct GradWords {
+    static constexpr int N = sizeof(GT) / 2;
+    uint4 q[N];
+};
+
+template <typename GT>
+__device__ inline void unpack8(const GradWords<GT>& r, float (&x)[8])
 {
-    const float4 a = *reinterpret_cast<const float4*>(p);
-    const float4 b = *reinterpret_cast<const float4*>(p + 4);
-    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+    if constexpr (sizeof(GT) == 2) {
+        const uint4 v = r.q[0];
+        x[0] = bf16_lo(v.x); x[1] = bf16_hi(v.x);
+        x[2] = bf16_lo(v.y); x[3] = bf16_hi(v.y);
+        x[4] = bf16_lo(v.z); x[5] = bf16_hi(v.z);
+        x[6] = bf16_lo(v.w); x[7] = bf16_hi(v.w);
+    } else {
+        x[0] = __uint_as_float(r.q[0].x); x[1] = __uint_as_float(r.q[0].y);
+        x[2] = __uint_as_float(r.q[0].z); x[3] = __uint_as_float(r.q[0].w);
+        x[4] = __uint_as_float(r.q[1].x); x[5] = __uint_as_float(r.q[1].y);
+        x[6] = __uint_as_float(r.q[1].z); x[7] = __uint_as_float(r.q[1].w);
+    }
 }
 
-__device__ inline float load_one(const uint16_t* p) { return __uint_as_float(uint32_t(*p) << 16); }
-__device__ inline float load_one(const float* p) { return *p; }
+// Loads the granule of 8 gradients at p of which the first nv exist; the
+// others read as +0.  STREAM selects non-temporal loads for full granules.
+template <bool STREAM, typename GT>
+__device__ inline void load_grads(const GT* p, int nv, GradWords<GT>& r)
+{
+    if (nv >= kGranule) {
+#pragma unroll
+        for (int q = 0; q < GradWords<GT>::N; ++q)
+            r.q[q] = STREAM ? load16_stream(reinterpret_cast<const uint4*>(p) + q)
+                            : load16(reinterpret_cast<const uint4*>(p) + q);
+        return;
+    }
+    uint32_t b[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        b[e] = e < nv ? grad_bits(p + e) : 0u;
+    if constexpr (sizeof(GT) == 2) {
+        r.q[0] = make_uint4(b[0] | (b[1] << 16), b[2] | (b[3] << 16), b[4] | (b[5] << 16),
+                            b[6] | (b[7] << 16));
+    } else {
+        r.q[0] = make_uint4(b[0], b[1], b[2], b[3]);
+        r.q[1] = make_uint4(b[4], b[5], b[6], b[7]);
+    }
+}
 
 // Index of the tensor that holds work unit u: the last k with prefix[k] <= u.
 __device__ inline int find_tensor(const int64_t* __restrict__ prefix, int n_tensors, int64_t u)
@@ -275,6 +319,26 @@ __device__ inline void unit_range(int64_t units, int64_t* begin, int64_t* end)
 
 // ------------------------------------------------------- a1: chunk sums
 
+// One lane's share of a chunk: granules lane + 256*r, r = 0..3.
+template <typename GT>
+struct ChunkLane {
+    GradWords<GT> r[4];
+};
+
+template <typename GT>
+__device__ inline void load_chunk_lane(const uint64_t* __restrict__ ptrs,
+                                       const int64_t* __restrict__ numels, int k, int64_t local,
+                                       int lane, ChunkLane<GT>& out)
+{
+    const int64_t n_in = i64min(kChunk, numels[k] - local * kChunk);
+    const GT* base = reinterpret_cast<const GT*>(ptrs[k]) + local * kChunk;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int j0 = kGranule * (lane + kThreads * r);
+        load_grads<true>(base + j0, int(i64min(i64max(n_in - j0, 0), kGranule)), out.r[r]);
+    }
+}
+
 template <typename GT>
 __global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __restrict__ chunk_prefix,
                                                             const uint64_t* __restrict__ ptrs,
@@ -290,37 +354,30 @@ __global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __res
     if (c_begin >= c_end)
         return;
     int k = find_tensor(chunk_prefix, n_tensors, c_begin);
+    ChunkLane<GT> cur, nxt;
+    load_chunk_lane(ptrs, numels, k, c_begin - chunk_prefix[k], lane, cur);
     int buf = 0;
     for (int64_t c = c_begin; c < c_end; ++c, buf ^= 1) {
-        while (c >= chunk_prefix[k + 1])
-            ++k;
-        const int64_t local = c - chunk_prefix[k];
-        const int64_t n_in = i64min(kChunk, numels[k] - local * kChunk);
-        const GT* base = reinterpret_cast<const GT*>(ptrs[k]) + local * kChunk;
-
-        float x[4][8];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int j0 = kGranule * (lane + kThreads * r);
-            if (j0 + kGranule <= n_in) {
-                load_granule(base + j0, x[r]);
-            } else {
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    x[r][e] = (j0 + e < n_in) ? load_one(base + j0 + e) : 0.0f;
-            }
+        // Prefetch the next chunk before reducing this one.
+        if (c + 1 < c_end) {
+            while (c + 1 >= chunk_prefix[k + 1])
+                ++k;
+            load_chunk_lane(ptrs, numels, k, c + 1 - chunk_prefix[k], lane, nxt);
         }
         // Lane sum in the fixed order.  The square of an fp32 value is exact in
         // fp64, so fma(x, x, a) is the single rounding of a + x*x.  Positions
-        // past the end hold 0 and leave the non-negative sum unchanged.
+        // past the end read as 0 and leave the non-negative sum unchanged.
         double a = 0.0;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int r = 0; r < 4; ++r) {
+            float x[8];
+            unpack8(cur.r[r], x);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const double xd = double(x[r][e]);
+                const double xd = double(x[e]);
                 a = __builtin_fma(xd, xd, a);
             }
+        }
         // 64-lane halving tree as a butterfly: lane i adds lane i^o; for i < o
         // that is a_i + a_(i+o), and addition is commutative.
 #pragma unroll
@@ -333,6 +390,8 @@ __global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __res
             partials[c] = (wave_sum[buf][0] + wave_sum[buf][2]) + (wave_sum[buf][1] + wave_sum[buf][3]);
         // The other buffer is written next; this one again only after the next
         // barrier, which lane 0 reaches after its read.
+        if (c + 1 < c_end)
+            cur = nxt;
     }
 }
 
@@ -343,12 +402,23 @@ __global__ __launch_bounds__(kThreads) void k_sqnorm_finish(const int64_t* __res
                                                             double* __restrict__ sk)
 {
     __shared__ double acc[kThreads];
+    constexpr int U = 8;  // loads in flight per accumulator; the additions stay in order
     const int k = blockIdx.x;
     const int t = threadIdx.x;
     const int64_t c0 = chunk_prefix[k];
     const int64_t nc = chunk_prefix[k + 1] - c0;
-    double b = 0.0;
-    for (int64_t c = t; c < nc; c += kThreads)  // accumulator t takes chunks c = t (mod 256)
+    double b = 0.0;  // accumulator t takes chunks c = t (mod 256), ascending
+    int64_t c = t;
+    for (; c + (U - 1) * kThreads < nc; c += U * kThreads) {
+        double p[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            p[u] = partials[c0 + c + u * kThreads];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            b = b + p[u];
+    }
+    for (; c < nc; c += kThreads)
         b = b + partials[c0 + c];
     acc[t] = b;
     __syncthreads();
@@ -367,18 +437,28 @@ __global__ __launch_bounds__(kThreads) void k_sqnorm_finish(const int64_t* __res
     }
 }
 
-__global__ __launch_bounds__(64) void k_sqnorm_total(const double* __restrict__ sk, int n_tensors,
-                                                     double* __restrict__ sk_out,
-                                                     double* __restrict__ sq_total,
-                                                     int32_t* __restrict__ status)
+__global__ __launch_bounds__(256) void k_sqnorm_total(const double* __restrict__ sk, int n_tensors,
+                                                      double* __restrict__ sk_out,
+                                                      double* __restrict__ sq_total,
+                                                      int32_t* __restrict__ status)
 {
-    if (sk_out)
-        for (int k = threadIdx.x; k < n_tensors; k += 64)
-            sk_out[k] = sk[k];
+    __shared__ double batch[1024];
+    double S = 0.0;  // kept by thread 0: the list-order sum
+    for (int k0 = 0; k0 < n_tensors; k0 += 1024) {
+        const int n = min(1024, n_tensors - k0);
+        for (int i = threadIdx.x; i < n; i += 256) {
+            const double v = sk[k0 + i];
+            batch[i] = v;
+            if (sk_out)
+                sk_out[k0 + i] = v;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0)
+            for (int i = 0; i < n; ++i)
+                S = S + batch[i];
+        __syncthreads();
+    }
     if (threadIdx.x == 0) {
-        double S = 0.0;
-        for (int k = 0; k < n_tensors; ++k)  // list order
-            S = S + sk[k];
         *sq_total = S;
         *status = isfinite(S) ? LT_STATUS_OK : LT_STATUS_NONFINITE;
     }
@@ -478,6 +558,81 @@ __device__ inline float wave_max_xor(float x, int width)
     return x;
 }
 
+// The inputs of one granule (8 consecutive elements of a tensor), as loaded:
+// fp32 weights, gradients, both code bytes and the scales of its block.
+template <typename GT>
+struct StepIn {
+    uint4 w[2];
+    GradWords<GT> g;
+    uint2 m, v;
+    float am, av;
+};
+
+template <typename GT, int B>
+__device__ inline void load_step_granule(const StepTensor& d, int64_t ei, int nv, StepIn<GT>& in)
+{
+    in.am = 0.0f;
+    in.av = 0.0f;
+    if (nv > 0) {
+        const int64_t blk = ei / B;
+        in.am = d.ma[blk];
+        in.av = d.va[blk];
+    }
+    load_grads<false>(static_cast<const GT*>(d.g) + ei, nv, in.g);
+    if (nv >= kGranule) {
+        in.w[0] = load16(d.w + ei);
+        in.w[1] = load16(d.w + ei + 4);
+        in.m = *reinterpret_cast<const uint2*>(d.mq + ei);
+        in.v = *reinterpret_cast<const uint2*>(d.vq + ei);
+        return;
+    }
+    uint32_t wb[8], mb[8], vb[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const bool ok = e < nv;
+        wb[e] = ok ? __float_as_uint(d.w[ei + e]) : 0u;
+        mb[e] = ok ? uint32_t(uint8_t(d.mq[ei + e])) : 0u;
+        vb[e] = ok ? uint32_t(d.vq[ei + e]) : 0u;
+    }
+    in.w[0] = make_uint4(wb[0], wb[1], wb[2], wb[3]);
+    in.w[1] = make_uint4(wb[4], wb[5], wb[6], wb[7]);
+    in.m = make_uint2(mb[0] | (mb[1] << 8) | (mb[2] << 16) | (mb[3] << 24),
+                      mb[4] | (mb[5] << 8) | (mb[6] << 16) | (mb[7] << 24));
+    in.v = make_uint2(vb[0] | (vb[1] << 8) | (vb[2] << 16) | (vb[3] << 24),
+                      vb[4] | (vb[5] << 8) | (vb[6] << 16) | (vb[7] << 24));
+}
+
+// Where a tile lives: its tensor, first element and number of valid elements.
+struct TilePos {
+    int k;
+    int64_t e0, n_valid;
+};
+
+template <int TILE>
+__device__ inline TilePos tile_pos(const int64_t* __restrict__ tile_prefix,
+                                   const StepTensor* __restrict__ desc, int k, int64_t t)
+{
+    while (t >= tile_prefix[k + 1])
+        ++k;
+    TilePos p;
+    p.k = k;
+    p.e0 = (t - tile_prefix[k]) * TILE;
+    p.n_valid = i64min(TILE, desc[k].numel - p.e0);
+    return p;
+}
+
+template <typename GT, int B, int TILE, int GR>
+__device__ inline void load_step_tile(const StepTensor& d, const TilePos& p, int lane,
+                                      StepIn<GT> (&in)[GR])
+{
+#pragma unroll
+    for (int j = 0; j < GR; ++j) {
+        const int o = kGranule * (lane + kThreads * j);
+        load_step_granule<GT, B>(d, p.e0 + o, int(i64min(i64max(p.n_valid - o, 0), kGranule)),
+                                 in[j]);
+    }
+}
+
 template <typename GT, int B>
 __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restrict__ tile_prefix,
                                                           const StepTensor* __restrict__ desc,
@@ -502,61 +657,36 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
     unit_range(n_tiles, &t_begin, &t_end);
     if (t_begin >= t_end)
         return;
-    int k = find_tensor(tile_prefix, n_tensors, t_begin);
+    TilePos pos = tile_pos<TILE>(tile_prefix, desc, find_tensor(tile_prefix, n_tensors, t_begin),
+                                 t_begin);
+    StepIn<GT> cur[GR], nxt[GR];
+    load_step_tile<GT, B, TILE, GR>(desc[pos.k], pos, lane, cur);
     int buf = 0;
     for (int64_t t = t_begin; t < t_end; ++t, buf ^= 1) {
-        while (t >= tile_prefix[k + 1])
-            ++k;
-        const StepTensor d = desc[k];
-        const int64_t e0 = (t - tile_prefix[k]) * TILE;
-        const int64_t n_valid = i64min(TILE, d.numel - e0);
-        const GT* __restrict__ gp = static_cast<const GT*>(d.g);
-
+        const StepTensor d = desc[pos.k];
         float m1[GR][8], v1[GR][8];
         float amax_m = 0.0f, amax_v = 0.0f;
 #pragma unroll
         for (int j = 0; j < GR; ++j) {
-            const int o = kGranule * (lane + kThreads * j);  // offset in the tile
-            const int nv = int(i64min(i64max(n_valid - o, 0), kGranule));
-            const int64_t ei = e0 + o;  // element index in the tensor
-            float w[8], g[8], qm[8], qv[8];
-            float a_m = 0.0f, a_v = 0.0f;
-            if (nv > 0) {
-                const int64_t blk = ei / B;
-                a_m = d.ma[blk];
-                a_v = d.va[blk];
-            }
-            if (nv == kGranule) {
-                const float4 wa = *reinterpret_cast<const float4*>(d.w + ei);
-                const float4 wb = *reinterpret_cast<const float4*>(d.w + ei + 4);
-                w[0] = wa.x; w[1] = wa.y; w[2] = wa.z; w[3] = wa.w;
-                w[4] = wb.x; w[5] = wb.y; w[6] = wb.z; w[7] = wb.w;
-                load_granule(gp + ei, g);
-                const uint2 cm = *reinterpret_cast<const uint2*>(d.mq + ei);
-                const uint2 cv = *reinterpret_cast<const uint2*>(d.vq + ei);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    qm[e] = float(int8_t(cm.x >> (8 * e)));
-                    qm[e + 4] = float(int8_t(cm.y >> (8 * e)));
-                    qv[e] = float((cv.x >> (8 * e)) & 0xFFu);
-                    qv[e + 4] = float((cv.y >> (8 * e)) & 0xFFu);
-                }
-            } else {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const bool ok = e < nv;
-                    w[e] = ok ? d.w[ei + e] : 0.0f;
-                    g[e] = ok ? load_one(gp + ei + e) : 0.0f;
-                    qm[e] = ok ? float(d.mq[ei + e]) : 0.0f;
-                    qv[e] = ok ? float(d.vq[ei + e]) : 0.0f;
-                }
-            }
-            const float step_m = a_m / 127.0f;
-            const float step_v = a_v / 255.0f;
+            const int o = kGranule * (lane + kThreads * j);
+            const int nv = int(i64min(i64max(pos.n_valid - o, 0), kGranule));
+            const int64_t ei = pos.e0 + o;
+            float g[8], w[8];
+            unpack8(cur[j].g, g);
+            w[0] = __uint_as_float(cur[j].w[0].x); w[1] = __uint_as_float(cur[j].w[0].y);
+            w[2] = __uint_as_float(cur[j].w[0].z); w[3] = __uint_as_float(cur[j].w[0].w);
+            w[4] = __uint_as_float(cur[j].w[1].x); w[5] = __uint_as_float(cur[j].w[1].y);
+            w[6] = __uint_as_float(cur[j].w[1].z); w[7] = __uint_as_float(cur[j].w[1].w);
+            const float step_m = cur[j].am / 127.0f;
+            const float step_v = cur[j].av / 255.0f;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const float m0 = qm[e] * step_m;
-                const float v0 = qv[e] * step_v;
+                const uint32_t mw = e < 4 ? cur[j].m.x : cur[j].m.y;
+                const uint32_t vw = e < 4 ? cur[j].v.x : cur[j].v.y;
+                const float qm = float(int8_t(mw >> (8 * (e & 3))));
+                const float qv = float((vw >> (8 * (e & 3))) & 0xFFu);
+                const float m0 = qm * step_m;
+                const float v0 = qv * step_v;
                 const float gc = g[e] * coef;
                 const float m = __builtin_fmaf(s.beta1, m0, s.c1 * gc);
                 const float v = __builtin_fmaf(s.beta2, v0, s.c2 * (gc * gc));
@@ -569,6 +699,7 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                     amax_v = fmaxf(amax_v, v);
                 }
             }
+            // The new weights do not depend on the block scales: store them now.
             if (nv == kGranule) {
                 *reinterpret_cast<float4*>(d.w + ei) = make_float4(w[0], w[1], w[2], w[3]);
                 *reinterpret_cast<float4*>(d.w + ei + 4) = make_float4(w[4], w[5], w[6], w[7]);
@@ -576,6 +707,13 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                 for (int e = 0; e < nv; ++e)
                     d.w[ei + e] = w[e];
             }
+        }
+
+        // Prefetch the next tile while the block maxima are combined.
+        const TilePos here = pos;
+        if (t + 1 < t_end) {
+            pos = tile_pos<TILE>(tile_prefix, desc, pos.k, t + 1);
+            load_step_tile<GT, B, TILE, GR>(desc[pos.k], pos, lane, nxt);
         }
 
         // Block absmax (max is exact and order-free).
@@ -604,8 +742,8 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
 #pragma unroll
         for (int j = 0; j < GR; ++j) {
             const int o = kGranule * (lane + kThreads * j);
-            const int nv = int(i64min(i64max(n_valid - o, 0), kGranule));
-            const int64_t ei = e0 + o;
+            const int nv = int(i64min(i64max(here.n_valid - o, 0), kGranule));
+            const int64_t ei = here.e0 + o;
             uint32_t pm[2] = {0u, 0u}, pv[2] = {0u, 0u};
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
@@ -631,6 +769,11 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                 d.ma[blk] = ok_m ? amax_m : 0.0f;
                 d.va[blk] = ok_v ? amax_v : 0.0f;
             }
+        }
+        if (t + 1 < t_end) {
+#pragma unroll
+            for (int j = 0; j < GR; ++j)
+                cur[j] = nxt[j];
         }
     }
 }
@@ -760,7 +903,7 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
     LT_HIP(hipGetLastError());
     k_sqnorm_finish<<<K, kThreads, 0, st>>>(d_prefix, d_partials, d_sk);
     LT_HIP(hipGetLastError());
-    k_sqnorm_total<<<1, 64, 0, st>>>(d_sk, K, sq_per_tensor, sq_total, status);
+    k_sqnorm_total<<<1, 256, 0, st>>>(d_sk, K, sq_per_tensor, sq_total, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
 }
