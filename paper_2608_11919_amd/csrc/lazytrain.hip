@@ -31,7 +31,6 @@ namespace {
 constexpr int kThreads = 256;  // 4 wave64s per workgroup
 constexpr int kChunk = 8192;   // sum-of-squares chunk: 256 lanes x 4 granules x 8 elements
 constexpr int kGranule = 8;    // elements per lane per 16-byte bf16 load
-constexpr int kTile = 2048;    // step elements per workgroup pass when block_size <= 2048
 
 // ------------------------------------------------------------------ errors
 
@@ -550,6 +549,29 @@ __global__ __launch_bounds__(64) void k_clip_coef(const double* __restrict__ sq_
 }
 
 // ------------------------------------------------------ a4-a10: fused step
+//
+// Geometry.  A lane owns E consecutive-granule slots (granule j of lane l is
+// elements 8*(l + 64*j) .. +7 of its wave's span), so each load instruction of
+// a wave covers one contiguous 1-2 KB run.  E = 32 for B >= 2048, B/64 for
+// B = 512, 1024 and 8 below.  For B <= 2048 a wave owns whole blocks and the
+// block absmax is a wave reduction; for B = 4096 and 8192, B/2048 waves of a
+// workgroup share a block and combine their maxima in LDS.
+
+// 32 elements per lane keeps 16 KB of long contiguous runs in flight per wave
+// (about 220 VGPRs, two waves per SIMD); measured on the 3B-class step it beats
+// 16 and 8 per lane, and forcing more waves per SIMD is slower still.
+constexpr int kStepElemsPerLane = 32;
+
+template <int B>
+struct StepGeom {
+    static constexpr int E_MAX = kStepElemsPerLane;
+    static constexpr int E = B >= 64 * E_MAX ? E_MAX : (B >= 512 ? B / 64 : 8);  // elements per lane
+    static constexpr int G = E / kGranule;                             // granules per lane
+    static constexpr int WAVE_SPAN = 64 * E;                           // elements per wave pass
+    static constexpr int W = B > WAVE_SPAN ? B / WAVE_SPAN : 1;        // waves per block
+    static constexpr int L = B >= 512 ? 64 : B / kGranule;             // lanes per block in a wave
+    static constexpr int UNIT = W > 1 ? 4 * WAVE_SPAN : WAVE_SPAN;      // elements per work unit
+};
 
 __device__ inline float wave_max_xor(float x, int width)
 {
@@ -558,34 +580,58 @@ __device__ inline float wave_max_xor(float x, int width)
     return x;
 }
 
-// The inputs of one granule (8 consecutive elements of a tensor), as loaded:
-// fp32 weights, gradients, both code bytes and the scales of its block.
+// a / 127 and a / 255, correctly rounded, for every fp32 a: the product with
+// the rounded reciprocal, corrected once by its fma residual; zero, infinite
+// and NaN inputs take the plain product.  A CPU test checks all 2^32 inputs.
+template <int D>
+__device__ inline float div_by_const(float a)
+{
+    constexpr float c = D == 127 ? 0x1.020408p-7f : 0x1.010102p-8f;  // RN(1/D)
+    const float q = a * c;
+    const float r = __builtin_fmaf(-q, float(D), a);
+    const float q1 = __builtin_fmaf(r, c, q);
+    return __builtin_amdgcn_classf(a, 0x267) ? q : q1;  // 0x267: +-0, +-inf, NaN
+}
+
+// Correctly rounded sqrt of an fp32 v that is 0, >= 2^-96, infinite or NaN:
+// the hardware estimate corrected by the signs of the fma residuals of its two
+// neighbours.  This is the sequence the compiler emits for sqrtf once the
+// scaling it applies to inputs below 2^-96 is not needed.
+__device__ inline float sqrt_rn_unscaled(float v)
+{
+    const float s = __builtin_amdgcn_sqrtf(v);
+    const float dn = __uint_as_float(__float_as_uint(s) - 1u);
+    const float up = __uint_as_float(__float_as_uint(s) + 1u);
+    const float r_dn = __builtin_fmaf(-dn, s, v);
+    const float r_up = __builtin_fmaf(-up, s, v);
+    float t = r_dn <= 0.0f ? dn : s;
+    t = r_up > 0.0f ? up : t;
+    return t;
+}
+
+// The inputs of one granule (8 consecutive elements of a tensor), as loaded.
 template <typename GT>
 struct StepIn {
     uint4 w[2];
     GradWords<GT> g;
     uint2 m, v;
-    float am, av;
 };
 
-template <typename GT, int B>
-__device__ inline void load_step_granule(const StepTensor& d, int64_t ei, int nv, StepIn<GT>& in)
+template <typename GT>
+__device__ inline void load_step_full(const StepTensor& d, int64_t ei, StepIn<GT>& in)
 {
-    in.am = 0.0f;
-    in.av = 0.0f;
-    if (nv > 0) {
-        const int64_t blk = ei / B;
-        in.am = d.ma[blk];
-        in.av = d.va[blk];
-    }
+    load_grads<false>(static_cast<const GT*>(d.g) + ei, kGranule, in.g);
+    in.w[0] = load16(d.w + ei);
+    in.w[1] = load16(d.w + ei + 4);
+    in.m = *reinterpret_cast<const uint2*>(d.mq + ei);
+    in.v = *reinterpret_cast<const uint2*>(d.vq + ei);
+}
+
+// Ragged granule: the first nv (0..8) elements exist, the others read as 0.
+template <typename GT>
+__device__ inline void load_step_ragged(const StepTensor& d, int64_t ei, int nv, StepIn<GT>& in)
+{
     load_grads<false>(static_cast<const GT*>(d.g) + ei, nv, in.g);
-    if (nv >= kGranule) {
-        in.w[0] = load16(d.w + ei);
-        in.w[1] = load16(d.w + ei + 4);
-        in.m = *reinterpret_cast<const uint2*>(d.mq + ei);
-        in.v = *reinterpret_cast<const uint2*>(d.vq + ei);
-        return;
-    }
     uint32_t wb[8], mb[8], vb[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -602,134 +648,149 @@ __device__ inline void load_step_granule(const StepTensor& d, int64_t ei, int nv
                       vb[4] | (vb[5] << 8) | (vb[6] << 16) | (vb[7] << 24));
 }
 
-// Where a tile lives: its tensor, first element and number of valid elements.
-struct TilePos {
-    int k;
-    int64_t e0, n_valid;
-};
-
-template <int TILE>
-__device__ inline TilePos tile_pos(const int64_t* __restrict__ tile_prefix,
-                                   const StepTensor* __restrict__ desc, int k, int64_t t)
+// Packs four codes held as exact small integers (as floats) into one word.
+// q must lie in [0, 255] (m codes arrive offset by +128).
+__device__ inline uint32_t pack4(float q0, float q1, float q2, float q3)
 {
-    while (t >= tile_prefix[k + 1])
-        ++k;
-    TilePos p;
-    p.k = k;
-    p.e0 = (t - tile_prefix[k]) * TILE;
-    p.n_valid = i64min(TILE, desc[k].numel - p.e0);
-    return p;
-}
-
-template <typename GT, int B, int TILE, int GR>
-__device__ inline void load_step_tile(const StepTensor& d, const TilePos& p, int lane,
-                                      StepIn<GT> (&in)[GR])
-{
-#pragma unroll
-    for (int j = 0; j < GR; ++j) {
-        const int o = kGranule * (lane + kThreads * j);
-        load_step_granule<GT, B>(d, p.e0 + o, int(i64min(i64max(p.n_valid - o, 0), kGranule)),
-                                 in[j]);
-    }
+    uint32_t w = __builtin_amdgcn_cvt_pk_u8_f32(q0, 0, 0u);
+    w = __builtin_amdgcn_cvt_pk_u8_f32(q1, 1, w);
+    w = __builtin_amdgcn_cvt_pk_u8_f32(q2, 2, w);
+    return __builtin_amdgcn_cvt_pk_u8_f32(q3, 3, w);
 }
 
 template <typename GT, int B>
-__global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restrict__ tile_prefix,
+__global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restrict__ unit_prefix,
                                                           const StepTensor* __restrict__ desc,
-                                                          int n_tensors, int64_t n_tiles,
+                                                          int n_tensors, int64_t n_units,
                                                           StepScalars s,
                                                           const float* __restrict__ coef_ptr,
                                                           const int32_t* __restrict__ status_ptr)
 {
-    constexpr int TILE = B > kTile ? B : kTile;  // elements per workgroup pass
-    constexpr int GR = TILE / kTile;             // granules per lane
-    constexpr int L = (B / kGranule) < kThreads ? (B / kGranule) : kThreads;  // lanes per block
-    constexpr int WAVES_PER_BLOCK = L > 64 ? L / 64 : 1;
-    __shared__ float red[2][2][4];  // [buffer][m, v][wave]
+    using Geo = StepGeom<B>;
+    constexpr int E = Geo::E, G = Geo::G, W = Geo::W, L = Geo::L, UNIT = Geo::UNIT;
+    __shared__ float red[2][2][4];  // [buffer][m, v][wave], used when W > 1
 
     if (status_ptr && *status_ptr == LT_STATUS_NONFINITE)
         return;  // skipped step: nothing is written
     const float coef = coef_ptr ? *coef_ptr : 1.0f;
-    const int lane = threadIdx.x;
-    const int wave = lane >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
 
-    int64_t t_begin, t_end;
-    unit_range(n_tiles, &t_begin, &t_end);
-    if (t_begin >= t_end)
-        return;
-    TilePos pos = tile_pos<TILE>(tile_prefix, desc, find_tensor(tile_prefix, n_tensors, t_begin),
-                                 t_begin);
-    StepIn<GT> cur[GR], nxt[GR];
-    load_step_tile<GT, B, TILE, GR>(desc[pos.k], pos, lane, cur);
+    // Work units: wave spans (W == 1, each wave on its own) or workgroup spans.
+    int64_t u_begin, u_end;
+    {
+        const int64_t workers = W > 1 ? int64_t(gridDim.x) : int64_t(gridDim.x) * 4;
+        const int64_t me = W > 1 ? int64_t(blockIdx.x) : int64_t(blockIdx.x) * 4 + wave;
+        const int64_t per = n_units / workers, rem = n_units % workers;
+        u_begin = me * per + (me < rem ? me : rem);
+        u_end = u_begin + per + (me < rem ? 1 : 0);
+    }
+    // Offset of this wave's span inside a unit.
+    const int64_t span0 = W > 1 ? int64_t(wave) * Geo::WAVE_SPAN : 0;
+    int k = u_begin < u_end ? find_tensor(unit_prefix, n_tensors, u_begin) : 0;
     int buf = 0;
-    for (int64_t t = t_begin; t < t_end; ++t, buf ^= 1) {
-        const StepTensor d = desc[pos.k];
-        float m1[GR][8], v1[GR][8];
-        float amax_m = 0.0f, amax_v = 0.0f;
+    for (int64_t u = u_begin; u < u_end; ++u, buf ^= 1) {
+        while (u >= unit_prefix[k + 1])
+            ++k;
+        const StepTensor d = desc[k];
+        const int64_t e_unit = (u - unit_prefix[k]) * UNIT;
+        const int64_t e0 = e_unit + span0;          // first element of this wave's span
+        const int64_t n_span = d.numel - e0;        // elements left from e0 (may be <= 0)
+        const bool full = n_span >= Geo::WAVE_SPAN;  // wave-uniform
+
+        StepIn<GT> in[G];
+        if (full) {
 #pragma unroll
-        for (int j = 0; j < GR; ++j) {
-            const int o = kGranule * (lane + kThreads * j);
-            const int nv = int(i64min(i64max(pos.n_valid - o, 0), kGranule));
-            const int64_t ei = pos.e0 + o;
-            float g[8], w[8];
-            unpack8(cur[j].g, g);
-            w[0] = __uint_as_float(cur[j].w[0].x); w[1] = __uint_as_float(cur[j].w[0].y);
-            w[2] = __uint_as_float(cur[j].w[0].z); w[3] = __uint_as_float(cur[j].w[0].w);
-            w[4] = __uint_as_float(cur[j].w[1].x); w[5] = __uint_as_float(cur[j].w[1].y);
-            w[6] = __uint_as_float(cur[j].w[1].z); w[7] = __uint_as_float(cur[j].w[1].w);
-            const float step_m = cur[j].am / 127.0f;
-            const float step_v = cur[j].av / 255.0f;
+            for (int j = 0; j < G; ++j)
+                load_step_full(d, e0 + kGranule * (lane + 64 * j), in[j]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < G; ++j) {
+                const int64_t o = kGranule * (lane + 64 * j);
+                load_step_ragged(d, e0 + o, int(i64min(i64max(n_span - o, 0), kGranule)), in[j]);
+            }
+        }
+        // Stored scales of this lane's block (one block per lane for B >= 512).
+        float a_m, a_v;
+        {
+            const int64_t blk = (e0 + (B >= 512 ? 0 : kGranule * lane)) / B;
+            const bool exists = n_span > (B >= 512 ? 0 : kGranule * lane);
+            a_m = exists ? d.ma[blk] : 0.0f;
+            a_v = exists ? d.va[blk] : 0.0f;
+        }
+        const float step_m = div_by_const<127>(a_m);
+        const float step_v = div_by_const<255>(a_v);
+
+        // Moments.  Elements past the end read as zero gradient and zero codes,
+        // so they produce m1 = v1 = 0 (or NaN from a non-finite stored scale)
+        // and leave the block maxima unchanged.
+        float m1[E], v1[E];
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            float g[8];
+            unpack8(in[j].g, g);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const uint32_t mw = e < 4 ? cur[j].m.x : cur[j].m.y;
-                const uint32_t vw = e < 4 ? cur[j].v.x : cur[j].v.y;
+                const uint32_t mw = e < 4 ? in[j].m.x : in[j].m.y;
+                const uint32_t vw = e < 4 ? in[j].v.x : in[j].v.y;
                 const float qm = float(int8_t(mw >> (8 * (e & 3))));
                 const float qv = float((vw >> (8 * (e & 3))) & 0xFFu);
-                const float m0 = qm * step_m;
-                const float v0 = qv * step_v;
                 const float gc = g[e] * coef;
-                const float m = __builtin_fmaf(s.beta1, m0, s.c1 * gc);
-                const float v = __builtin_fmaf(s.beta2, v0, s.c2 * (gc * gc));
-                const float den = __builtin_fmaf(sqrtf(v), s.rbc2, s.eps);
-                w[e] = __builtin_fmaf(-s.step_size, m / den, w[e] * s.decay);
-                m1[j][e] = m;
-                v1[j][e] = v;
-                if (e < nv) {
-                    amax_m = fmaxf(amax_m, fabsf(m));
-                    amax_v = fmaxf(amax_v, v);
-                }
+                m1[8 * j + e] = __builtin_fmaf(s.beta1, qm * step_m, s.c1 * gc);
+                v1[8 * j + e] = __builtin_fmaf(s.beta2, qv * step_v, s.c2 * (gc * gc));
             }
-            // The new weights do not depend on the block scales: store them now.
-            if (nv == kGranule) {
+        }
+        // sqrt: the short correction sequence is exact unless some v1 of the
+        // wave lies in (0, 2^-96); then every lane takes the full sqrtf.
+        uint32_t vmin = 0xFFFFFFFFu;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            vmin = min(vmin, __float_as_uint(v1[e]) - 1u);  // 0 wraps to the top
+        const bool tiny = vmin < 0x0F800000u - 1u;          // 0 < v1 < 2^-96
+        const bool scaled = __builtin_amdgcn_ballot_w64(tiny) != 0;
+
+        float amax_m = 0.0f, amax_v = 0.0f;
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            float w[8];
+            w[0] = __uint_as_float(in[j].w[0].x); w[1] = __uint_as_float(in[j].w[0].y);
+            w[2] = __uint_as_float(in[j].w[0].z); w[3] = __uint_as_float(in[j].w[0].w);
+            w[4] = __uint_as_float(in[j].w[1].x); w[5] = __uint_as_float(in[j].w[1].y);
+            w[6] = __uint_as_float(in[j].w[1].z); w[7] = __uint_as_float(in[j].w[1].w);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float m = m1[8 * j + e], v = v1[8 * j + e];
+                const float root = scaled ? sqrtf(v) : sqrt_rn_unscaled(v);
+                const float den = __builtin_fmaf(root, s.rbc2, s.eps);
+                w[e] = __builtin_fmaf(-s.step_size, m / den, w[e] * s.decay);
+                amax_m = fmaxf(amax_m, fabsf(m));
+                amax_v = fmaxf(amax_v, v);
+            }
+            const int64_t ei = e0 + kGranule * (lane + 64 * j);
+            if (full) {
                 *reinterpret_cast<float4*>(d.w + ei) = make_float4(w[0], w[1], w[2], w[3]);
                 *reinterpret_cast<float4*>(d.w + ei + 4) = make_float4(w[4], w[5], w[6], w[7]);
             } else {
+                const int nv = int(i64min(i64max(n_span - kGranule * (lane + 64 * j), 0), kGranule));
                 for (int e = 0; e < nv; ++e)
                     d.w[ei + e] = w[e];
             }
         }
 
-        // Prefetch the next tile while the block maxima are combined.
-        const TilePos here = pos;
-        if (t + 1 < t_end) {
-            pos = tile_pos<TILE>(tile_prefix, desc, pos.k, t + 1);
-            load_step_tile<GT, B, TILE, GR>(desc[pos.k], pos, lane, nxt);
-        }
-
         // Block absmax (max is exact and order-free).
-        amax_m = wave_max_xor(amax_m, L < 64 ? L : 64);
-        amax_v = wave_max_xor(amax_v, L < 64 ? L : 64);
-        if constexpr (L > 64) {
-            if ((lane & 63) == 0) {
+        amax_m = wave_max_xor(amax_m, L);
+        amax_v = wave_max_xor(amax_v, L);
+        if constexpr (W > 1) {
+            if (lane == 0) {
                 red[buf][0][wave] = amax_m;
                 red[buf][1][wave] = amax_v;
             }
             __syncthreads();
-            const int first = (wave / WAVES_PER_BLOCK) * WAVES_PER_BLOCK;
+            const int first = (wave / W) * W;
             amax_m = red[buf][0][first];
             amax_v = red[buf][1][first];
 #pragma unroll
-            for (int i = 1; i < WAVES_PER_BLOCK; ++i) {
+            for (int i = 1; i < W; ++i) {
                 amax_m = fmaxf(amax_m, red[buf][0][first + i]);
                 amax_v = fmaxf(amax_v, red[buf][1][first + i]);
             }
@@ -740,40 +801,42 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
         const bool ok_v = isfinite(amax_v) && isfinite(inv_v);
 
 #pragma unroll
-        for (int j = 0; j < GR; ++j) {
-            const int o = kGranule * (lane + kThreads * j);
-            const int nv = int(i64min(i64max(here.n_valid - o, 0), kGranule));
-            const int64_t ei = here.e0 + o;
-            uint32_t pm[2] = {0u, 0u}, pv[2] = {0u, 0u};
+        for (int j = 0; j < G; ++j) {
+            float qm[8], qv[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const float qmf = fminf(fmaxf(rintf(m1[j][e] * inv_m), -127.0f), 127.0f);
-                const float qvf = fminf(fmaxf(rintf(v1[j][e] * inv_v), 0.0f), 255.0f);
-                const uint32_t bm = ok_m ? (uint32_t(int32_t(qmf)) & 0xFFu) : 0u;
-                const uint32_t bv = ok_v ? uint32_t(int32_t(qvf)) : 0u;
-                pm[e >> 2] |= bm << (8 * (e & 3));
-                pv[e >> 2] |= bv << (8 * (e & 3));
+                // clamp, then shift m codes by +128 (exact) so both pack as unsigned bytes
+                qm[e] = fminf(fmaxf(rintf(m1[8 * j + e] * inv_m), -127.0f), 127.0f) + 128.0f;
+                qv[e] = fminf(fmaxf(rintf(v1[8 * j + e] * inv_v), 0.0f), 255.0f);
             }
-            if (nv == kGranule) {
-                *reinterpret_cast<uint2*>(d.mq + ei) = make_uint2(pm[0], pm[1]);
-                *reinterpret_cast<uint2*>(d.vq + ei) = make_uint2(pv[0], pv[1]);
+            // m: undo the offset on all four bytes at once (two's complement int8)
+            const uint32_t pm0 = ok_m ? pack4(qm[0], qm[1], qm[2], qm[3]) ^ 0x80808080u : 0u;
+            const uint32_t pm1 = ok_m ? pack4(qm[4], qm[5], qm[6], qm[7]) ^ 0x80808080u : 0u;
+            const uint32_t pv0 = ok_v ? pack4(qv[0], qv[1], qv[2], qv[3]) : 0u;
+            const uint32_t pv1 = ok_v ? pack4(qv[4], qv[5], qv[6], qv[7]) : 0u;
+            const int64_t ei = e0 + kGranule * (lane + 64 * j);
+            if (full) {
+                *reinterpret_cast<uint2*>(d.mq + ei) = make_uint2(pm0, pm1);
+                *reinterpret_cast<uint2*>(d.vq + ei) = make_uint2(pv0, pv1);
             } else {
+                const int nv = int(i64min(i64max(n_span - kGranule * (lane + 64 * j), 0), kGranule));
                 for (int e = 0; e < nv; ++e) {
-                    d.mq[ei + e] = int8_t((pm[e >> 2] >> (8 * (e & 3))) & 0xFFu);
-                    d.vq[ei + e] = uint8_t((pv[e >> 2] >> (8 * (e & 3))) & 0xFFu);
+                    const uint32_t wm = e < 4 ? pm0 : pm1, wv = e < 4 ? pv0 : pv1;
+                    d.mq[ei + e] = int8_t((wm >> (8 * (e & 3))) & 0xFFu);
+                    d.vq[ei + e] = uint8_t((wv >> (8 * (e & 3))) & 0xFFu);
                 }
             }
-            // The first lane of each block writes its scales.
-            if (j == 0 && nv > 0 && (lane % L) == 0) {
-                const int64_t blk = ei / B;
+        }
+        // The first lane of each block writes its scales.
+        {
+            const int64_t o = B >= 512 ? 0 : kGranule * lane;
+            const bool first_lane = B >= 512 ? lane == 0 : (lane % L) == 0;
+            const bool first_wave = W > 1 ? (wave % W) == 0 : true;
+            if (first_lane && first_wave && n_span > o) {
+                const int64_t blk = (e0 + o) / B;
                 d.ma[blk] = ok_m ? amax_m : 0.0f;
                 d.va[blk] = ok_v ? amax_v : 0.0f;
             }
-        }
-        if (t + 1 < t_end) {
-#pragma unroll
-            for (int j = 0; j < GR; ++j)
-                cur[j] = nxt[j];
         }
     }
 }
@@ -781,14 +844,16 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
 // ================================================================ host side
 
 template <typename GT, int B>
-lt_err launch_step_b(const int64_t* prefix, const StepTensor* desc, int K, int64_t tiles,
+lt_err launch_step_b(const int64_t* prefix, const StepTensor* desc, int K, int64_t units,
                      const StepScalars& s, const float* coef, const int32_t* status,
                      hipStream_t stream)
 {
+    // One workgroup takes four units at a time when each wave works alone.
+    const int64_t wg_units = StepGeom<B>::W > 1 ? units : (units + 3) / 4;
     int grid;
-    if (lt_err e = grid_size(k_adamw8_step<GT, B>, tiles, &grid))
+    if (lt_err e = grid_size(k_adamw8_step<GT, B>, wg_units, &grid))
         return e;
-    k_adamw8_step<GT, B><<<grid, kThreads, 0, stream>>>(prefix, desc, K, tiles, s, coef, status);
+    k_adamw8_step<GT, B><<<grid, kThreads, 0, stream>>>(prefix, desc, K, units, s, coef, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
 }
@@ -809,6 +874,13 @@ lt_err launch_step(int B, const int64_t* prefix, const StepTensor* desc, int K, 
     case 8192: return launch_step_b<GT, 8192>(prefix, desc, K, tiles, s, coef, status, stream);
     default: return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
     }
+}
+
+// Elements per work unit of the step kernel (StepGeom<B>::UNIT).
+int64_t step_unit_elems(int B)
+{
+    const int64_t E = B >= 64 * kStepElemsPerLane ? kStepElemsPerLane : (B >= 512 ? B / 64 : 8);
+    return B > 64 * E ? 4 * 64 * E : 64 * E;
 }
 
 int64_t sq_chunks_of(const int64_t* numels, int K)
@@ -968,7 +1040,7 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
         return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
                                           std::to_string(lay.total) + " bytes");
 
-    const int64_t tile = std::max<int64_t>(block_size, kTile);
+    const int64_t tile = step_unit_elems(block_size);
     std::vector<uint8_t> host(lay.total, 0);
     auto* prefix = reinterpret_cast<int64_t*>(host.data() + lay.prefix);
     auto* desc = reinterpret_cast<StepTensor*>(host.data() + lay.desc);
