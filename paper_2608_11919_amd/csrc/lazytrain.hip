@@ -338,6 +338,32 @@ __device__ inline void load_chunk_lane(const uint64_t* __restrict__ ptrs,
     }
 }
 
+// Lane sum of one chunk in the fixed order.  The square of an fp32 value is
+// exact in fp64, so fma(x, x, a) is the single rounding of a + x*x; positions
+// past the end read as 0 and leave the non-negative sum unchanged.
+template <typename GT>
+__device__ inline double lane_sum(const ChunkLane<GT>& c)
+{
+    double a = 0.0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        float x[8];
+        unpack8(c.r[r], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const double xd = double(x[e]);
+            a = __builtin_fma(xd, xd, a);
+        }
+    }
+    return a;
+}
+
+// Chunks per iteration: their loads are all issued first, then the wave sums,
+// one barrier and the partials.  Two measured best among 1-8 with and without a
+// next-iteration prefetch and with grid-strided iterations (all within ~5%).
+constexpr int kSqChunksPerIter = 2;
+
+// Each iteration takes U consecutive chunks of the workgroup's contiguous range.
 template <typename GT>
 __global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __restrict__ chunk_prefix,
                                                             const uint64_t* __restrict__ ptrs,
@@ -345,52 +371,48 @@ __global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __res
                                                             int n_tensors, int64_t n_chunks,
                                                             double* __restrict__ partials)
 {
-    __shared__ double wave_sum[2][4];
+    constexpr int U = kSqChunksPerIter;
+    __shared__ double wave_sum[2][U][4];
     const int lane = threadIdx.x;
     const int wave = lane >> 6;
-    int64_t c_begin, c_end;
-    unit_range(n_chunks, &c_begin, &c_end);
-    if (c_begin >= c_end)
+    const int64_t n_iter = (n_chunks + U - 1) / U;
+    int64_t i_begin, i_end;
+    unit_range(n_iter, &i_begin, &i_end);
+    if (i_begin >= i_end)
         return;
-    int k = find_tensor(chunk_prefix, n_tensors, c_begin);
-    ChunkLane<GT> cur, nxt;
-    load_chunk_lane(ptrs, numels, k, c_begin - chunk_prefix[k], lane, cur);
+    int k = find_tensor(chunk_prefix, n_tensors, i_begin * U);
     int buf = 0;
-    for (int64_t c = c_begin; c < c_end; ++c, buf ^= 1) {
-        // Prefetch the next chunk before reducing this one.
-        if (c + 1 < c_end) {
-            while (c + 1 >= chunk_prefix[k + 1])
-                ++k;
-            load_chunk_lane(ptrs, numels, k, c + 1 - chunk_prefix[k], lane, nxt);
-        }
-        // Lane sum in the fixed order.  The square of an fp32 value is exact in
-        // fp64, so fma(x, x, a) is the single rounding of a + x*x.  Positions
-        // past the end read as 0 and leave the non-negative sum unchanged.
-        double a = 0.0;
+    for (int64_t it = i_begin; it < i_end; ++it, buf ^= 1) {
+        ChunkLane<GT> cur[U];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float x[8];
-            unpack8(cur.r[r], x);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const double xd = double(x[e]);
-                a = __builtin_fma(xd, xd, a);
+        for (int u = 0; u < U; ++u) {
+            const int64_t c = it * U + u;
+            if (c < n_chunks) {
+                while (c >= chunk_prefix[k + 1])
+                    ++k;
+                load_chunk_lane(ptrs, numels, k, c - chunk_prefix[k], lane, cur[u]);
             }
         }
-        // 64-lane halving tree as a butterfly: lane i adds lane i^o; for i < o
-        // that is a_i + a_(i+o), and addition is commutative.
 #pragma unroll
-        for (int o = 32; o >= 1; o >>= 1)
-            a = a + __shfl_xor(a, o, 64);
-        if ((lane & 63) == 0)
-            wave_sum[buf][wave] = a;
+        for (int u = 0; u < U; ++u) {
+            double a = lane_sum(cur[u]);
+            // 64-lane halving tree as a butterfly: lane i adds lane i^o; for
+            // i < o that is a_i + a_(i+o), and addition is commutative.
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1)
+                a = a + __shfl_xor(a, o, 64);
+            if ((lane & 63) == 0)
+                wave_sum[buf][u][wave] = a;
+        }
         __syncthreads();
-        if (lane == 0)
-            partials[c] = (wave_sum[buf][0] + wave_sum[buf][2]) + (wave_sum[buf][1] + wave_sum[buf][3]);
+        if (lane < U) {
+            const int64_t c = it * U + lane;
+            if (c < n_chunks)
+                partials[c] = (wave_sum[buf][lane][0] + wave_sum[buf][lane][2]) +
+                              (wave_sum[buf][lane][1] + wave_sum[buf][lane][3]);
+        }
         // The other buffer is written next; this one again only after the next
-        // barrier, which lane 0 reaches after its read.
-        if (c + 1 < c_end)
-            cur = nxt;
+        // barrier, which the reading lanes reach after their reads.
     }
 }
 
@@ -961,13 +983,14 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
     auto* d_sk = reinterpret_cast<double*>(ws + lay.sk);
 
     int grid;
+    const int64_t sq_iters = (C + kSqChunksPerIter - 1) / kSqChunksPerIter;
     if (grad_dtype == LT_DTYPE_BF16) {
-        if (lt_err e = grid_size(k_sqnorm_chunks<uint16_t>, C, &grid))
+        if (lt_err e = grid_size(k_sqnorm_chunks<uint16_t>, sq_iters, &grid))
             return e;
         k_sqnorm_chunks<uint16_t><<<grid, kThreads, 0, st>>>(d_prefix, d_ptrs, d_numels, K, C,
                                                              d_partials);
     } else {
-        if (lt_err e = grid_size(k_sqnorm_chunks<float>, C, &grid))
+        if (lt_err e = grid_size(k_sqnorm_chunks<float>, sq_iters, &grid))
             return e;
         k_sqnorm_chunks<float><<<grid, kThreads, 0, st>>>(d_prefix, d_ptrs, d_numels, K, C,
                                                           d_partials);

@@ -1,0 +1,242 @@
+"""GPU parity at full size, in the launch configuration bench.py times.
+
+3B-class full model (325 tensors, 3.09e9 parameters): the sum of squares, norm and
+clip coefficient over all gradients are compared bitwise with the oracle; the step
+is compared bitwise on sampled blocks (the first and last block of every tensor and
+random blocks), which the oracle recomputes one by one from the generator; every
+block of every tensor is checked for the properties the quantizer guarantees at any
+size.  The clip-stress variant runs three steps from zero state with fresh
+gradients, all-zero blocks and +-1e4 outliers, in lockstep (the oracle starts each
+step from the GPU's state of the sampled blocks) and free-running (the oracle's own
+three-step state)."""
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_11919_amd as lt
+import synth
+from gpu_helpers import DEV, to_host
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def _say(msg):
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
+
+
+def _hyper(w):
+    return dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay)
+
+
+class Device:
+    """The workload's tensors in HBM, filled from the generator one tensor at a time."""
+
+    def __init__(self, w, n_threads):
+        self.w, self.B = w, w.block_size
+        big = max(w.numels)
+        gdt = torch.bfloat16 if w.grad_dtype == synth.BF16 else torch.float32
+        self.stage_w = torch.empty(big, dtype=torch.float32, pin_memory=True)
+        self.stage_g = torch.empty(big, dtype=gdt, pin_memory=True)
+        self.n_threads = n_threads
+        self.params, self.grads, self.mq, self.vq, self.ma, self.va = [], [], [], [], [], []
+        for k, n in enumerate(w.numels):
+            synth.fill_ptr(self.stage_w.data_ptr(), synth.F32, 0, n, w.seed,
+                           synth.STREAM_WEIGHTS, k, w.weight_recipe, n_threads)
+            self.params.append(self.stage_w[:n].to(DEV))
+            self.grads.append(torch.empty(n, dtype=gdt, device=DEV))
+            nb = -(-n // self.B)
+            self.mq.append(torch.zeros(n, dtype=torch.int8, device=DEV))
+            self.vq.append(torch.zeros(n, dtype=torch.uint8, device=DEV))
+            self.ma.append(torch.zeros(nb, dtype=torch.float32, device=DEV))
+            self.va.append(torch.zeros(nb, dtype=torch.float32, device=DEV))
+        self.S = torch.zeros(1, dtype=torch.float64, device=DEV)
+        self.sk = torch.zeros(len(w.numels), dtype=torch.float64, device=DEV)
+        self.status = torch.zeros(1, dtype=torch.int32, device=DEV)
+        self.coef = torch.zeros(1, dtype=torch.float32, device=DEV)
+        self.norm = torch.zeros(1, dtype=torch.float32, device=DEV)
+
+    def load_grads(self, stream):
+        w = self.w
+        for k, n in enumerate(w.numels):
+            synth.fill_ptr(self.stage_g.data_ptr(), w.grad_dtype, 0, n, w.seed, stream, k,
+                           w.grad_recipe, self.n_threads)
+            self.grads[k].copy_(self.stage_g[:n])
+        torch.cuda.synchronize()
+
+    def step(self, t, clip=True, **over):
+        h = dict(_hyper(self.w), **over)
+        if clip:
+            lt.lt_grad_sqnorm(self.grads, self.S, self.status, sq_per_tensor=self.sk)
+            lt.lt_clip_coef(self.S, self.w.max_norm, self.coef, total_norm=self.norm)
+            lt.lt_hybrid8bit_adamw_step(self.params, self.grads, self.mq, self.ma, self.vq,
+                                        self.va, self.B, step=t, coef=self.coef,
+                                        status=self.status, **h)
+        else:
+            lt.lt_hybrid8bit_adamw_step(self.params, self.grads, self.mq, self.ma, self.vq,
+                                        self.va, self.B, step=t, **h)
+        torch.cuda.synchronize()
+
+    def read_blocks(self, blocks):
+        """Host copies of (w, m codes, m absmax, v codes, v absmax) of blocks (k, b)."""
+        out = []
+        for k, b in blocks:
+            lo = b * self.B
+            hi = min(self.w.numels[k], lo + self.B)
+            out.append((to_host(self.params[k][lo:hi]), to_host(self.mq[k][lo:hi]),
+                        to_host(self.ma[k][b:b + 1]), to_host(self.vq[k][lo:hi]),
+                        to_host(self.va[k][b:b + 1])))
+        return out
+
+
+def _sample_blocks(w, n_random, seed):
+    B = w.block_size
+    blocks = set()
+    for k, n in enumerate(w.numels):
+        nb = -(-n // B)
+        blocks.add((k, 0))
+        blocks.add((k, nb - 1))
+    rng = np.random.default_rng(seed)
+    p = np.array(w.numels, dtype=np.float64)
+    ks = rng.choice(len(w.numels), size=n_random, p=p / p.sum())
+    for k in ks:
+        blocks.add((int(k), int(rng.integers(0, -(-w.numels[k] // w.block_size)))))
+    return sorted(blocks)
+
+
+def _host_slices(w, blocks, stream):
+    B = w.block_size
+    gs = []
+    for k, b in blocks:
+        lo = b * B
+        n = min(w.numels[k], lo + B) - lo
+        gs.append(w.grads(k, stream, offset=lo, n=n, n_threads=1))
+    return gs
+
+
+def _full_grads(w, stream, n_threads):
+    return [w.grads(k, stream, n_threads=n_threads) for k in range(len(w.numels))]
+
+
+def _compare_blocks(got, want, what):
+    for i, (g, r) in enumerate(zip(got, want)):
+        for name, a, b in zip(("w", "m codes", "m absmax", "v codes", "v absmax"), g, r):
+            if a.tobytes() != b.tobytes():
+                bad = np.flatnonzero(a != b)
+                raise AssertionError(f"{what}: block #{i} {name} differs at {bad.size} "
+                                     f"positions (first {bad[:3]})")
+
+
+def _check_code_properties(dev):
+    """At any size: a block with a positive stored absmax holds a code of magnitude
+    127 (m) or 255 (v), since its largest element maps to full scale; a block with
+    absmax 0 holds only zero codes; every m code lies in [-127, 127]."""
+    B = dev.B
+    for k, n in enumerate(dev.w.numels):
+        nb_full = n // B
+        for codes, absmax, top in ((dev.mq[k], dev.ma[k], 127), (dev.vq[k], dev.va[k], 255)):
+            c = codes.to(torch.int16).abs()
+            assert int(c.max()) <= top
+            if nb_full:
+                blk_max = c[:nb_full * B].view(nb_full, B).amax(dim=1)
+                a = absmax[:nb_full]
+                assert bool(torch.all(torch.where(a > 0, blk_max == top, blk_max == 0)))
+                assert bool(torch.all(torch.isfinite(a)))
+
+
+def test_full_3b_model_step_parity():
+    w = synth.full_3b()
+    n_threads = synth.default_threads()
+    B, K = w.block_size, len(w.shapes)
+    _say(f"{w.name}: generating {w.n_params} params on the host and in HBM")
+    dev = Device(w, n_threads)
+    dev.load_grads(synth.STREAM_PRIOR_GRAD)
+    dev.step(1, clip=False, lr=0.0)  # 8-bit states from one prior step (weights unchanged)
+    dev.load_grads(synth.grad_stream(w.step))
+    _say("GPU step at t = 2 (sum of squares, clip, fused step)")
+    dev.step(w.step)
+    assert lt.lt_read_status(dev.status) == lt.LT_STATUS_OK
+
+    _say("oracle sum of squares over all gradients")
+    host_g = _full_grads(w, synth.grad_stream(w.step), n_threads)
+    rsk, rS, rst = oracle.grad_sqnorm(host_g, n_threads=n_threads)
+    del host_g
+    rnorm, rcoef = oracle.clip_coef(rS, w.max_norm)
+    assert to_host(dev.S)[0].hex() == rS.hex()
+    assert to_host(dev.sk).tobytes() == rsk.tobytes()
+    assert to_host(dev.norm)[0] == rnorm and to_host(dev.coef)[0] == rcoef
+    _say(f"S = {rS!r}, norm = {float(rnorm):.6g}, coef = {float(rcoef):.6g}: bitwise equal")
+
+    blocks = _sample_blocks(w, 3000, seed=11)
+    _say(f"oracle on {len(blocks)} sampled blocks")
+    ws, g0s, gs = [], _host_slices(w, blocks, synth.STREAM_PRIOR_GRAD), \
+        _host_slices(w, blocks, synth.grad_stream(w.step))
+    for k, b in blocks:
+        lo = b * B
+        ws.append(w.weights(k, offset=lo, n=min(w.numels[k], lo + B) - lo, n_threads=1))
+    mq = [np.zeros(x.size, np.int8) for x in ws]
+    vq = [np.zeros(x.size, np.uint8) for x in ws]
+    ma = [np.zeros(1, np.float32) for _ in ws]
+    va = [np.zeros(1, np.float32) for _ in ws]
+    h = _hyper(w)
+    oracle.hybrid8bit_adamw_step(ws, g0s, mq, ma, vq, va, B, step=1, n_threads=n_threads,
+                                 **dict(h, lr=0.0))
+    oracle.hybrid8bit_adamw_step(ws, gs, mq, ma, vq, va, B, step=w.step, coef=float(rcoef),
+                                 status=rst, n_threads=n_threads, **h)
+    _compare_blocks(dev.read_blocks(blocks), list(zip(ws, mq, ma, vq, va)), w.name)
+    _say("sampled blocks bitwise equal; checking code properties of every block")
+    _check_code_properties(dev)
+
+
+def test_clip_stress_three_steps():
+    w = synth.clip_stress()
+    n_threads = synth.default_threads()
+    B = w.block_size
+    _say(f"{w.name}: generating {w.n_params} params")
+    dev = Device(w, n_threads)
+    blocks = _sample_blocks(w, 2000, seed=12)
+    # add sampled all-zero blocks
+    zero_blocks = [(k, b) for (k, b) in _sample_blocks(w, 20000, seed=13)
+                   if synth.block_is_zero(w.seed, k, b, w.grad_recipe.zero_mod)][:200]
+    blocks = sorted(set(blocks) | set(zero_blocks))
+    h = _hyper(w)
+    free = None  # the oracle's own state of the sampled blocks (free-running)
+    for t in (1, 2, 3):
+        stream = synth.grad_stream(t)
+        before = dev.read_blocks(blocks)
+        if free is None:
+            free = [tuple(a.copy() for a in blk) for blk in before]
+        dev.load_grads(stream)
+        _say(f"step t = {t}: GPU")
+        dev.step(t)
+        assert lt.lt_read_status(dev.status) == lt.LT_STATUS_OK
+        host_g = _full_grads(w, stream, n_threads)
+        rsk, rS, rst = oracle.grad_sqnorm(host_g, n_threads=n_threads)
+        del host_g
+        rnorm, rcoef = oracle.clip_coef(rS, w.max_norm)
+        assert to_host(dev.S)[0].hex() == rS.hex()
+        assert to_host(dev.coef)[0] == rcoef
+        _say(f"  S bitwise equal; norm {float(rnorm):.6g}, coef {float(rcoef):.6g}")
+        gs = _host_slices(w, blocks, stream)
+        # lockstep: the oracle starts from the GPU's state of each sampled block
+        lock = [tuple(a.copy() for a in blk) for blk in before]
+        oracle.hybrid8bit_adamw_step([x[0] for x in lock], gs, [x[1] for x in lock],
+                                     [x[2] for x in lock], [x[3] for x in lock],
+                                     [x[4] for x in lock], B, step=t, coef=float(rcoef),
+                                     status=rst, n_threads=n_threads, **h)
+        after = dev.read_blocks(blocks)
+        _compare_blocks(after, lock, f"lockstep t = {t}")
+        oracle.hybrid8bit_adamw_step([x[0] for x in free], gs, [x[1] for x in free],
+                                     [x[2] for x in free], [x[3] for x in free],
+                                     [x[4] for x in free], B, step=t, coef=float(rcoef),
+                                     status=rst, n_threads=n_threads, **h)
+        _compare_blocks(after, free, f"free-running t = {t}")
+        for (k, b), blk in zip(blocks, after):
+            if (k, b) in zero_blocks:
+                assert not blk[1].any() and not blk[3].any() and blk[2][0] == 0 and blk[4][0] == 0
+        _say(f"  {len(blocks)} sampled blocks bitwise equal (lockstep and free-running)")
+    _check_code_properties(dev)
+    # the reading of this workload: norm ~ 1.76e7 from the +-9984 outliers
+    assert 1.5e7 < float(rnorm) < 2.0e7
