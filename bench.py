@@ -147,6 +147,27 @@ def cpu_baseline(w, n_threads, target_s: float):
             "sample": desc + ": sum of squares + clip + step, one pass", "seconds": round(dt, 3)}
 
 
+COUNTERS = os.path.join(ROOT, "profiles", "adamw8_step_3b_full_counters.json")
+
+
+def counter_traffic(workload_name: str):
+    """HBM bytes per launch of the fused step kernel from the committed rocprofv3
+    counter summary (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy of known
+    size).  None unless the summary covers this workload and the kernel source is the
+    one the counters were taken on."""
+    import hashlib
+    try:
+        with open(COUNTERS) as f:
+            c = json.load(f)
+        with open(os.path.join(ROOT, c["source"]), "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, KeyError, ValueError):
+        return None
+    if sha != c.get("source_sha256") or workload_name != c.get("workload"):
+        return None
+    return c["kernels"]["k_adamw8_step"]["traffic_bytes"]
+
+
 def copy_probe(dev, nbytes: int, reps: int):
     """A plain copy kernel of known size, for scaling the HBM byte counters."""
     import torch
@@ -271,7 +292,8 @@ def main() -> int:
                        "adamw8_step": round(avg_step_s * 1e3, 4)},
         "roofline": {"kernel": "k_adamw8_step", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                     "traffic": counter_traffic(w.name),
                      "bytes_per_launch": kbytes},
         "status": st,
     }
