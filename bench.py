@@ -27,7 +27,8 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E peak
 METRIC = "optimizer step params/s + achieved HBM GB/s (% of MI355X peak)"
-WORKLOADS = {"full": "full_3b", "layer": "layer_3b", "tiny": "tiny", "stress": "clip_stress"}
+WORKLOADS = {"full": "full_3b", "layer": "layer_3b", "tiny": "tiny", "stress": "clip_stress",
+             "streamed": "streamed_27b"}
 
 
 def log(msg: str) -> None:
@@ -168,6 +169,141 @@ def counter_traffic(workload_name: str):
     return c["kernels"]["k_adamw8_step"]["traffic_bytes"]
 
 
+def pcie_rates(dev, nbytes: int):
+    """Pinned host <-> HBM copy rates on this machine: H2D alone, D2H alone and both at
+    once on two streams (GB/s)."""
+    import torch
+    h_in = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    h_out = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    d_a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    d_b = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    s1, s2 = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        fn()
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    def h2d():
+        with torch.cuda.stream(s1):
+            d_a.copy_(h_in, non_blocking=True)
+
+    def d2h():
+        with torch.cuda.stream(s2):
+            h_out.copy_(d_b, non_blocking=True)
+
+    def both():
+        h2d()
+        d2h()
+
+    t_h2d, t_d2h, t_both = timed(h2d), timed(d2h), timed(both)
+    return {"h2d_gbps": round(nbytes / t_h2d / 1e9, 2), "d2h_gbps": round(nbytes / t_d2h / 1e9, 2),
+            "concurrent_gbps_each": round(nbytes / t_both / 1e9, 2), "probe_bytes": nbytes}
+
+
+def run_streamed(args, w, dev, n_threads) -> int:
+    """a11: the layer-streamed step.  Weights, gradients and 8-bit states live in pinned
+    host memory; each step streams the gradients through HBM for the norm (pass 1),
+    then every layer in, through the fused step and out (pass 2).  Host memory holds
+    args.host_layers distinct layers that the model's layers cycle through (logical
+    layer l uses host layer l mod host_layers), which bounds pinned memory while
+    moving exactly the bytes of the full model."""
+    import torch
+
+    import paper_2608_11919_amd as lt
+    import synth
+
+    per_layer = 9
+    L = len(w.shapes) // per_layer
+    R = min(args.host_layers, L)
+    B = w.block_size
+    hyper = dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay)
+    log(f"{w.name}: {L} layers, {w.n_params} params; {R} distinct pinned host layers")
+    rates = pcie_rates(dev, 1 << 31)
+    log(f"pinned copies: {rates}")
+    t0 = time.time()
+    host = {name: [] for name in ("w", "g", "mq", "ma", "vq", "va")}
+    for r in range(R):
+        for j in range(per_layer):
+            k = r * per_layer + j
+            n = w.numels[k]
+            nb = -(-n // B)
+            wt = torch.empty(n, dtype=torch.float32, pin_memory=True)
+            synth.fill_ptr(wt.data_ptr(), synth.F32, 0, n, w.seed, synth.STREAM_WEIGHTS, k,
+                           w.weight_recipe, n_threads)
+            gt = torch.empty(n, dtype=torch.bfloat16, pin_memory=True)
+            synth.fill_ptr(gt.data_ptr(), synth.BF16, 0, n, w.seed, synth.grad_stream(w.step), k,
+                           w.grad_recipe, n_threads)
+            host["w"].append(wt)
+            host["g"].append(gt)
+            host["mq"].append(torch.zeros(n, dtype=torch.int8, pin_memory=True))
+            host["vq"].append(torch.zeros(n, dtype=torch.uint8, pin_memory=True))
+            host["ma"].append(torch.zeros(nb, dtype=torch.float32, pin_memory=True))
+            host["va"].append(torch.zeros(nb, dtype=torch.float32, pin_memory=True))
+        log(f"host layer {r + 1}/{R} ready ({time.time() - t0:.1f} s)")
+    lists = {name: [v[(l % R) * per_layer + j] for l in range(L) for j in range(per_layer)]
+             for name, v in host.items()}
+    first = list(range(0, L * per_layer + 1, per_layer))
+    S = torch.zeros(1, dtype=torch.float64, device=dev)
+    coef = torch.zeros(1, dtype=torch.float32, device=dev)
+    norm = torch.zeros(1, dtype=torch.float32, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    cs, hs, ds = torch.cuda.Stream(dev), torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+    slots = args.ring_slots
+    nbytes = lt.lt_streamed_workspace_bytes(w.numels, first, lt.LT_DTYPE_BF16, B, slots)
+    workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def step(t):
+        lt.lt_streamed_hybrid8bit_adamw_step(
+            lists["w"], lists["g"], lists["mq"], lists["ma"], lists["vq"], lists["va"], first, B,
+            step=t, max_norm=w.max_norm, ring_slots=slots, sq_total=S, coef=coef, status=status,
+            total_norm=norm, workspace=workspace, compute_stream=cs, h2d_stream=hs,
+            d2h_stream=ds, **hyper)
+
+    t = 1
+    for _ in range(args.warmup):
+        step(t)
+        t += 1
+        cs.synchronize()
+        log(f"warmup step done")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(t)
+        t += 1
+        cs.synchronize()
+        log(f"timed step done ({time.perf_counter() - t0:.2f} s)")
+    elapsed = time.perf_counter() - t0
+    st = lt.lt_read_status(status, cs)
+    per = elapsed / args.steps
+    n = w.n_params
+    nb = sum(-(-x // B) for x in w.numels)
+    h2d = n * 2 + n * 8 + nb * 8  # pass 1 gradients; pass 2 weights, gradients, codes, scales
+    d2h = n * 6 + nb * 8          # weights, codes, scales back
+    bound = max(h2d / (rates["h2d_gbps"] * 1e9), d2h / (rates["d2h_gbps"] * 1e9))
+    out = {
+        "metric": METRIC, "value": n / per, "unit": "params/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(per * 1e3, 2),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "params": n, "tensors": len(w.shapes), "layers": L,
+                   "block_size": B, "grad_dtype": "bf16", "ring_slots": slots,
+                   "host_layers": R, "host_state": "pinned, cycled over host_layers"},
+        "pcie": {"h2d_bytes_per_step": h2d, "d2h_bytes_per_step": d2h, **rates,
+                 "link_bound_ms": round(bound * 1e3, 1),
+                 "h2d_gbps_achieved": round(h2d / per / 1e9, 2),
+                 "d2h_gbps_achieved": round(d2h / per / 1e9, 2),
+                 "frac_of_link_bound": round(bound / per, 4)},
+        "status": st, "norm": float(norm.item()), "coef": float(coef.item()),
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def copy_probe(dev, nbytes: int, reps: int):
     """A plain copy kernel of known size, for scaling the HBM byte counters."""
     import torch
@@ -188,6 +324,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU seconds for the oracle sample")
+    ap.add_argument("--host-layers", type=int, default=8,
+                    help="streamed workload: distinct pinned host layers the model cycles over")
+    ap.add_argument("--ring-slots", type=int, default=3, help="streamed workload: device slots")
     ap.add_argument("--copy-probe-bytes", type=int, default=0,
                     help="also run a plain copy of this many bytes (counter scaling)")
     args = ap.parse_args()
@@ -214,6 +353,8 @@ def main() -> int:
 
     if args.copy_probe_bytes:
         copy_probe(dev, args.copy_probe_bytes, 5)
+    if args.workload == "streamed":
+        return run_streamed(args, w, dev, n_threads)
 
     params, grads, mq, ma, vq, va, t_first = build_device_workload(w, dev, n_threads)
     sq_total = torch.zeros(1, dtype=torch.float64, device=dev)

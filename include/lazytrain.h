@@ -140,6 +140,59 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
                                 int64_t step, const float* coef, const int32_t* status,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of device workspace lt_streamed_hybrid8bit_adamw_step needs: the
+ * descriptors of every layer, one fp64 partial per 8192-element chunk of the
+ * whole model, and ring_slots slots each large enough for the largest layer's
+ * weights, gradients, codes and scales.  0 if an argument is invalid. */
+size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const int* layer_first,
+                                   int n_layers, int grad_dtype, int block_size, int ring_slots);
+
+/*
+ * Step a11: one clipped Hybrid 8-bit AdamW step over a model whose fp32
+ * weights, gradients and 8-bit states stay in HOST memory and pass through HBM
+ * layer by layer (Sec. 3.5: parameters and optimizer states are kept in CPU
+ * memory while the GPU is a transient compute cache; Sec. 3.4: the CPU-GPU
+ * link is the shared transfer resource).  Same per-element arithmetic, block
+ * layout and skip rule as lt_hybrid8bit_adamw_step, and the same fixed-order
+ * sum of squares over the whole model, so every result is bitwise that of the
+ * resident path on the same data.
+ *   params .. v_absmax  HOST pointers, one entry per tensor, layouts as in
+ *                       lt_hybrid8bit_adamw_step.  Pinned memory (hipHostMalloc)
+ *                       lets copies overlap compute; pageable memory works but
+ *                       serializes the copies.  Read and written asynchronously:
+ *                       the caller must not touch them until compute_stream has
+ *                       completed the call's work.
+ *   layer_first         host int[n_layers + 1]: layer i is tensors
+ *                       [layer_first[i], layer_first[i + 1]); 0 = first, n_tensors
+ *                       = last, strictly rising.  Layers are streamed in order.
+ *   max_norm            > 0; +INFINITY disables clipping (coef = 1).
+ *   ring_slots          device slots in the ring, 2..16 (3 lets one layer copy in
+ *                       while one computes and one copies out).
+ *   sq_total, total_norm (may be NULL), coef, status: device outputs as in
+ *                       lt_grad_sqnorm and lt_clip_coef.  A NONFINITE status
+ *                       skips the update: weights, codes and scales are copied
+ *                       back unchanged.
+ *   compute_stream, h2d_stream, d2h_stream: the copies in, the kernels and the
+ *                       copies out are ordered by events; the call's work ends on
+ *                       compute_stream (synchronize it before reading results).
+ *                       The three may be the same stream.  Streamed calls on one
+ *                       device are serialized by the library.
+ * Pass 1 copies each layer's gradients in (2 or 4 B/param) and sums them; pass 2
+ * copies weights, gradients, codes and scales in (8 or 10 B/param + 8 B/block)
+ * and weights, codes and scales out (6 B/param + 8 B/block).
+ */
+lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const* grads,
+                                         int grad_dtype, int8_t* const* m_codes,
+                                         float* const* m_absmax, uint8_t* const* v_codes,
+                                         float* const* v_absmax, const int64_t* numels,
+                                         int n_tensors, const int* layer_first, int n_layers,
+                                         int block_size, double lr, double beta1, double beta2,
+                                         double eps, double weight_decay, int64_t step,
+                                         float max_norm, int ring_slots, void* workspace,
+                                         size_t workspace_bytes, double* sq_total,
+                                         float* total_norm, float* coef, int32_t* status,
+                                         void* compute_stream, void* h2d_stream, void* d2h_stream);
+
 /* Copies the device status word to *out and synchronizes `stream` (the only
  * entry point that blocks the host).  An asynchronous device fault from
  * earlier work on the stream surfaces here as LT_ERR_HIP. */

@@ -923,6 +923,146 @@ bool valid_list(const int64_t* numels, int K)
     return true;
 }
 
+bool valid_hyper(double lr, double beta1, double beta2, double eps, double weight_decay,
+                 int64_t step)
+{
+    return std::isfinite(lr) && lr >= 0.0 && std::isfinite(weight_decay) && weight_decay >= 0.0 &&
+           beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0 && std::isfinite(eps) &&
+           eps >= 0.0 && step >= 1;
+}
+
+bool valid_block_size(int B) { return B >= 64 && B <= 8192 && (B & (B - 1)) == 0; }
+
+// The fp32 scalars of one step, each computed in fp64 and rounded once.
+StepScalars make_scalars(double lr, double beta1, double beta2, double eps, double weight_decay,
+                         int64_t step)
+{
+    StepScalars s;
+    const double t = double(step);
+    s.beta1 = float(beta1);
+    s.beta2 = float(beta2);
+    s.eps = float(eps);
+    s.c1 = float(1.0 - beta1);
+    s.c2 = float(1.0 - beta2);
+    s.decay = float(1.0 - lr * weight_decay);
+    s.step_size = float(lr / (1.0 - std::pow(beta1, t)));
+    s.rbc2 = float(1.0 / std::sqrt(1.0 - std::pow(beta2, t)));
+    return s;
+}
+
+lt_err launch_sq_chunks(int gdt, const int64_t* prefix, const uint64_t* ptrs, const int64_t* numels,
+                        int K, int64_t C, double* partials, hipStream_t st)
+{
+    const int64_t iters = (C + kSqChunksPerIter - 1) / kSqChunksPerIter;
+    int grid;
+    if (gdt == LT_DTYPE_BF16) {
+        if (lt_err e = grid_size(k_sqnorm_chunks<uint16_t>, iters, &grid))
+            return e;
+        k_sqnorm_chunks<uint16_t><<<grid, kThreads, 0, st>>>(prefix, ptrs, numels, K, C, partials);
+    } else {
+        if (lt_err e = grid_size(k_sqnorm_chunks<float>, iters, &grid))
+            return e;
+        k_sqnorm_chunks<float><<<grid, kThreads, 0, st>>>(prefix, ptrs, numels, K, C, partials);
+    }
+    LT_HIP(hipGetLastError());
+    return LT_OK;
+}
+
+// ---------------------------------------------------- a11: layer streaming
+//
+// Weights, gradients and 8-bit states stay in (pinned) host memory; layers pass
+// through a ring of device slots.  Pass 1 copies each layer's gradients in and
+// writes its chunk sums at their global indices, so S is bitwise the resident
+// sum; the finish, total and clip run once.  Pass 2 copies each layer in, runs
+// the fused step on it and copies weights, codes and scales back.  Copies in,
+// kernels and copies out run on three streams ordered by per-slot events.
+
+constexpr int kMaxSlots = 16;
+
+struct StreamEvents {
+    hipEvent_t in[kMaxSlots], computed[kMaxSlots], freed[kMaxSlots], done;
+    bool ready = false;
+};
+
+StreamEvents g_stream_events[kMaxDevices];
+std::mutex g_stream_mu[kMaxDevices];
+
+size_t align256(size_t x) { return round_up(x, 256); }
+
+// Bytes of one tensor's arrays inside a slot: w, g, m codes, v codes, m and v absmax.
+struct SlotTensor {
+    size_t w, g, mq, vq, ma, va, end;
+};
+
+SlotTensor slot_tensor(size_t at, int64_t n, int gbytes, int B)
+{
+    const int64_t nb = (n + B - 1) / B;
+    SlotTensor t;
+    t.w = at;
+    t.g = t.w + align256(size_t(n) * 4);
+    t.mq = t.g + align256(size_t(n) * gbytes);
+    t.vq = t.mq + align256(size_t(n));
+    t.ma = t.vq + align256(size_t(n));
+    t.va = t.ma + align256(size_t(nb) * 4);
+    t.end = t.va + align256(size_t(nb) * 4);
+    return t;
+}
+
+struct StreamLayout {
+    size_t header = 0;                  // uploaded descriptors
+    size_t gprefix = 0;                 // global chunk prefix, K + 1
+    std::vector<size_t> sq_prefix, sq_ptrs, sq_numels, st_prefix, st_desc;  // per layer
+    size_t partials = 0, sk = 0, slots = 0, slot_bytes = 0, total = 0;
+    int64_t C = 0;
+};
+
+StreamLayout stream_layout(const int64_t* numels, int K, const int* first, int L, int gbytes, int B,
+                           int S)
+{
+    StreamLayout l;
+    size_t at = 0;
+    l.gprefix = at;
+    at = round_up(at + sizeof(int64_t) * (K + 1), 64);
+    for (int i = 0; i < L; ++i) {
+        const int Ki = first[i + 1] - first[i];
+        l.sq_prefix.push_back(at);
+        at = round_up(at + sizeof(int64_t) * (Ki + 1), 64);
+        l.sq_ptrs.push_back(at);
+        at = round_up(at + sizeof(uint64_t) * Ki, 64);
+        l.sq_numels.push_back(at);
+        at = round_up(at + sizeof(int64_t) * Ki, 64);
+        l.st_prefix.push_back(at);
+        at = round_up(at + sizeof(int64_t) * (Ki + 1), 64);
+        l.st_desc.push_back(at);
+        at = round_up(at + sizeof(StepTensor) * Ki, 64);
+    }
+    l.header = round_up(at, 256);
+    l.C = sq_chunks_of(numels, K);
+    l.partials = l.header;
+    l.sk = l.partials + align256(sizeof(double) * l.C);
+    l.slots = l.sk + align256(sizeof(double) * K);
+    size_t biggest = 0;
+    for (int i = 0; i < L; ++i) {
+        size_t b = 0;
+        for (int k = first[i]; k < first[i + 1]; ++k)
+            b = slot_tensor(b, numels[k], gbytes, B).end;
+        biggest = std::max(biggest, b);
+    }
+    l.slot_bytes = biggest;
+    l.total = l.slots + l.slot_bytes * size_t(S);
+    return l;
+}
+
+bool valid_layers(const int* first, int L, int K)
+{
+    if (!first || L < 1 || first[0] != 0 || first[L] != K)
+        return false;
+    for (int i = 0; i < L; ++i)
+        if (first[i + 1] <= first[i])
+            return false;
+    return true;
+}
+
 }  // namespace
 
 // =================================================================== C ABI
@@ -982,20 +1122,8 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
     auto* d_partials = reinterpret_cast<double*>(ws + lay.partials);
     auto* d_sk = reinterpret_cast<double*>(ws + lay.sk);
 
-    int grid;
-    const int64_t sq_iters = (C + kSqChunksPerIter - 1) / kSqChunksPerIter;
-    if (grad_dtype == LT_DTYPE_BF16) {
-        if (lt_err e = grid_size(k_sqnorm_chunks<uint16_t>, sq_iters, &grid))
-            return e;
-        k_sqnorm_chunks<uint16_t><<<grid, kThreads, 0, st>>>(d_prefix, d_ptrs, d_numels, K, C,
-                                                             d_partials);
-    } else {
-        if (lt_err e = grid_size(k_sqnorm_chunks<float>, sq_iters, &grid))
-            return e;
-        k_sqnorm_chunks<float><<<grid, kThreads, 0, st>>>(d_prefix, d_ptrs, d_numels, K, C,
-                                                          d_partials);
-    }
-    LT_HIP(hipGetLastError());
+    if (lt_err e = launch_sq_chunks(grad_dtype, d_prefix, d_ptrs, d_numels, K, C, d_partials, st))
+        return e;
     k_sqnorm_finish<<<K, kThreads, 0, st>>>(d_prefix, d_partials, d_sk);
     LT_HIP(hipGetLastError());
     k_sqnorm_total<<<1, 256, 0, st>>>(d_sk, K, sq_per_tensor, sq_total, status);
@@ -1038,11 +1166,9 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
         return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 1 entries with numel >= 1");
     if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
-    if (block_size < 64 || block_size > 8192 || (block_size & (block_size - 1)))
+    if (!valid_block_size(block_size))
         return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
-    if (!(std::isfinite(lr) && lr >= 0.0) || !(std::isfinite(weight_decay) && weight_decay >= 0.0) ||
-        !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) ||
-        !(std::isfinite(eps) && eps >= 0.0) || step < 1)
+    if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step))
         return fail(LT_ERR_INVALID_ARG,
                     "need finite lr, weight_decay, eps >= 0, 0 <= beta1, beta2 < 1 and step >= 1");
     if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)))
@@ -1075,16 +1201,7 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
     }
     const int64_t tiles = prefix[K];
 
-    StepScalars s;
-    const double t = double(step);
-    s.beta1 = float(beta1);
-    s.beta2 = float(beta2);
-    s.eps = float(eps);
-    s.c1 = float(1.0 - beta1);
-    s.c2 = float(1.0 - beta2);
-    s.decay = float(1.0 - lr * weight_decay);
-    s.step_size = float(lr / (1.0 - std::pow(beta1, t)));
-    s.rbc2 = float(1.0 / std::sqrt(1.0 - std::pow(beta2, t)));
+    const StepScalars s = make_scalars(lr, beta1, beta2, eps, weight_decay, step);
 
     auto* ws = static_cast<uint8_t*>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -1095,6 +1212,203 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
     if (grad_dtype == LT_DTYPE_BF16)
         return launch_step<uint16_t>(block_size, d_prefix, d_desc, K, tiles, s, coef, status, st);
     return launch_step<float>(block_size, d_prefix, d_desc, K, tiles, s, coef, status, st);
+}
+
+size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const int* layer_first,
+                                   int n_layers, int grad_dtype, int block_size, int ring_slots)
+{
+    if (!valid_list(numels, n_tensors) || !valid_layers(layer_first, n_layers, n_tensors) ||
+        (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16) ||
+        !valid_block_size(block_size) || ring_slots < 2 || ring_slots > kMaxSlots)
+        return 0;
+    return stream_layout(numels, n_tensors, layer_first, n_layers,
+                         grad_dtype == LT_DTYPE_BF16 ? 2 : 4, block_size, ring_slots)
+        .total;
+}
+
+lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const* grads,
+                                         int grad_dtype, int8_t* const* m_codes,
+                                         float* const* m_absmax, uint8_t* const* v_codes,
+                                         float* const* v_absmax, const int64_t* numels,
+                                         int n_tensors, const int* layer_first, int n_layers,
+                                         int block_size, double lr, double beta1, double beta2,
+                                         double eps, double weight_decay, int64_t step,
+                                         float max_norm, int ring_slots, void* workspace,
+                                         size_t workspace_bytes, double* sq_total,
+                                         float* total_norm, float* coef, int32_t* status,
+                                         void* compute_stream, void* h2d_stream, void* d2h_stream)
+{
+    g_last_error.clear();
+    const int K = n_tensors, L = n_layers, S = ring_slots, B = block_size;
+    if (!params || !grads || !m_codes || !m_absmax || !v_codes || !v_absmax ||
+        !valid_list(numels, K))
+        return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 1 entries with numel >= 1");
+    if (!valid_layers(layer_first, L, K))
+        return fail(LT_ERR_INVALID_ARG,
+                    "layer_first must rise strictly from 0 to n_tensors over n_layers + 1 entries");
+    if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
+        return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
+    if (!valid_block_size(B))
+        return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
+    if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step) || !(max_norm > 0.0f))
+        return fail(LT_ERR_INVALID_ARG, "need finite lr, weight_decay, eps >= 0, 0 <= beta1, "
+                                        "beta2 < 1, step >= 1 and max_norm > 0");
+    if (S < 2 || S > kMaxSlots)
+        return fail(LT_ERR_INVALID_ARG, "ring_slots must be in [2, 16]");
+    if (!sq_total || !coef || !status)
+        return fail(LT_ERR_INVALID_ARG, "sq_total, coef and status must not be NULL");
+    if (!aligned(sq_total, 8) || !aligned(coef, 4) || !aligned(status, 4) ||
+        (total_norm && !aligned(total_norm, 4)))
+        return fail(LT_ERR_ALIGNMENT, "scalar outputs must be naturally aligned");
+    for (int k = 0; k < K; ++k)
+        if (!params[k] || !grads[k] || !m_codes[k] || !m_absmax[k] || !v_codes[k] || !v_absmax[k])
+            return fail(LT_ERR_INVALID_ARG, "NULL host pointer at index " + std::to_string(k));
+    const int gbytes = grad_dtype == LT_DTYPE_BF16 ? 2 : 4;
+    const StreamLayout lay = stream_layout(numels, K, layer_first, L, gbytes, B, S);
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < lay.total)
+        return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
+                                          std::to_string(lay.total) + " bytes");
+
+    auto* ws = static_cast<uint8_t*>(workspace);
+    auto slot_base = [&](int layer) { return ws + lay.slots + lay.slot_bytes * size_t(layer % S); };
+    const int64_t unit = step_unit_elems(B);
+
+    // Descriptors of every layer, each pointing into the slot the layer will use.
+    std::vector<uint8_t> header(lay.header, 0);
+    auto* gprefix = reinterpret_cast<int64_t*>(header.data() + lay.gprefix);
+    gprefix[0] = 0;
+    for (int k = 0; k < K; ++k)
+        gprefix[k + 1] = gprefix[k] + (numels[k] + kChunk - 1) / kChunk;
+    std::vector<std::vector<SlotTensor>> places(L);
+    for (int i = 0; i < L; ++i) {
+        auto* sp = reinterpret_cast<int64_t*>(header.data() + lay.sq_prefix[i]);
+        auto* pp = reinterpret_cast<uint64_t*>(header.data() + lay.sq_ptrs[i]);
+        auto* np = reinterpret_cast<int64_t*>(header.data() + lay.sq_numels[i]);
+        auto* up = reinterpret_cast<int64_t*>(header.data() + lay.st_prefix[i]);
+        auto* dp = reinterpret_cast<StepTensor*>(header.data() + lay.st_desc[i]);
+        uint8_t* base = slot_base(i);
+        size_t at = 0;
+        sp[0] = 0;
+        up[0] = 0;
+        for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
+            const SlotTensor t = slot_tensor(at, numels[k], gbytes, B);
+            places[i].push_back(t);
+            at = t.end;
+            sp[j + 1] = sp[j] + (numels[k] + kChunk - 1) / kChunk;
+            pp[j] = reinterpret_cast<uint64_t>(base + t.g);
+            np[j] = numels[k];
+            up[j + 1] = up[j] + (numels[k] + unit - 1) / unit;
+            dp[j] = StepTensor{reinterpret_cast<float*>(base + t.w), base + t.g,
+                               reinterpret_cast<int8_t*>(base + t.mq),
+                               reinterpret_cast<float*>(base + t.ma),
+                               reinterpret_cast<uint8_t*>(base + t.vq),
+                               reinterpret_cast<float*>(base + t.va), numels[k], 0};
+        }
+    }
+
+    int dev;
+    if (lt_err e = current_device(&dev))
+        return e;
+    std::lock_guard<std::mutex> lock(g_stream_mu[dev]);  // one streamed call per device at a time
+    StreamEvents& ev = g_stream_events[dev];
+    if (!ev.ready) {
+        for (int i = 0; i < kMaxSlots; ++i) {
+            LT_HIP(hipEventCreateWithFlags(&ev.in[i], hipEventDisableTiming));
+            LT_HIP(hipEventCreateWithFlags(&ev.computed[i], hipEventDisableTiming));
+            LT_HIP(hipEventCreateWithFlags(&ev.freed[i], hipEventDisableTiming));
+        }
+        LT_HIP(hipEventCreateWithFlags(&ev.done, hipEventDisableTiming));
+        ev.ready = true;
+    }
+    hipStream_t cs = static_cast<hipStream_t>(compute_stream);
+    hipStream_t hs = static_cast<hipStream_t>(h2d_stream);
+    hipStream_t ds = static_cast<hipStream_t>(d2h_stream);
+    if (lt_err e = upload(header.data(), header.size(), ws, cs))
+        return e;
+    // Copies into a slot may start once the work that last used it is done.
+    bool used[kMaxSlots] = {};
+    LT_HIP(hipEventRecord(ev.done, cs));  // the descriptors are in place
+    LT_HIP(hipStreamWaitEvent(hs, ev.done, 0));
+    auto* d_partials = reinterpret_cast<double*>(ws + lay.partials);
+    auto* d_sk = reinterpret_cast<double*>(ws + lay.sk);
+    const auto H2D = hipMemcpyHostToDevice, D2H = hipMemcpyDeviceToHost;
+
+    // Pass 1: gradients in, chunk sums at their global indices.
+    for (int i = 0; i < L; ++i) {
+        const int sl = i % S;
+        if (used[sl])
+            LT_HIP(hipStreamWaitEvent(hs, ev.freed[sl], 0));
+        uint8_t* base = slot_base(i);
+        for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j)
+            LT_HIP(hipMemcpyAsync(base + places[i][j].g, grads[k], size_t(numels[k]) * gbytes, H2D,
+                                  hs));
+        LT_HIP(hipEventRecord(ev.in[sl], hs));
+        LT_HIP(hipStreamWaitEvent(cs, ev.in[sl], 0));
+        const int Ki = layer_first[i + 1] - layer_first[i];
+        const int64_t Ci = reinterpret_cast<int64_t*>(header.data() + lay.sq_prefix[i])[Ki];
+        if (lt_err e = launch_sq_chunks(
+                grad_dtype, reinterpret_cast<const int64_t*>(ws + lay.sq_prefix[i]),
+                reinterpret_cast<const uint64_t*>(ws + lay.sq_ptrs[i]),
+                reinterpret_cast<const int64_t*>(ws + lay.sq_numels[i]), Ki, Ci,
+                d_partials + gprefix[layer_first[i]], cs))
+            return e;
+        LT_HIP(hipEventRecord(ev.freed[sl], cs));
+        used[sl] = true;
+    }
+    const auto* d_gprefix = reinterpret_cast<const int64_t*>(ws + lay.gprefix);
+    k_sqnorm_finish<<<K, kThreads, 0, cs>>>(d_gprefix, d_partials, d_sk);
+    LT_HIP(hipGetLastError());
+    k_sqnorm_total<<<1, 256, 0, cs>>>(d_sk, K, nullptr, sq_total, status);
+    LT_HIP(hipGetLastError());
+    k_clip_coef<<<1, 64, 0, cs>>>(sq_total, max_norm, total_norm, coef);
+    LT_HIP(hipGetLastError());
+
+    // Pass 2: layer in, fused step, layer out.
+    const StepScalars sc = make_scalars(lr, beta1, beta2, eps, weight_decay, step);
+    for (int i = 0; i < L; ++i) {
+        const int sl = i % S;
+        if (used[sl])
+            LT_HIP(hipStreamWaitEvent(hs, ev.freed[sl], 0));
+        uint8_t* base = slot_base(i);
+        for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
+            const SlotTensor& t = places[i][j];
+            const size_t n = size_t(numels[k]), nb = size_t((numels[k] + B - 1) / B);
+            LT_HIP(hipMemcpyAsync(base + t.w, params[k], n * 4, H2D, hs));
+            LT_HIP(hipMemcpyAsync(base + t.g, grads[k], n * gbytes, H2D, hs));
+            LT_HIP(hipMemcpyAsync(base + t.mq, m_codes[k], n, H2D, hs));
+            LT_HIP(hipMemcpyAsync(base + t.vq, v_codes[k], n, H2D, hs));
+            LT_HIP(hipMemcpyAsync(base + t.ma, m_absmax[k], nb * 4, H2D, hs));
+            LT_HIP(hipMemcpyAsync(base + t.va, v_absmax[k], nb * 4, H2D, hs));
+        }
+        LT_HIP(hipEventRecord(ev.in[sl], hs));
+        LT_HIP(hipStreamWaitEvent(cs, ev.in[sl], 0));
+        const int Ki = layer_first[i + 1] - layer_first[i];
+        const auto* up = reinterpret_cast<const int64_t*>(ws + lay.st_prefix[i]);
+        const auto* dp = reinterpret_cast<const StepTensor*>(ws + lay.st_desc[i]);
+        const int64_t units = reinterpret_cast<int64_t*>(header.data() + lay.st_prefix[i])[Ki];
+        lt_err e = grad_dtype == LT_DTYPE_BF16
+                       ? launch_step<uint16_t>(B, up, dp, Ki, units, sc, coef, status, cs)
+                       : launch_step<float>(B, up, dp, Ki, units, sc, coef, status, cs);
+        if (e)
+            return e;
+        LT_HIP(hipEventRecord(ev.computed[sl], cs));
+        LT_HIP(hipStreamWaitEvent(ds, ev.computed[sl], 0));
+        for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
+            const SlotTensor& t = places[i][j];
+            const size_t n = size_t(numels[k]), nb = size_t((numels[k] + B - 1) / B);
+            LT_HIP(hipMemcpyAsync(params[k], base + t.w, n * 4, D2H, ds));
+            LT_HIP(hipMemcpyAsync(m_codes[k], base + t.mq, n, D2H, ds));
+            LT_HIP(hipMemcpyAsync(v_codes[k], base + t.vq, n, D2H, ds));
+            LT_HIP(hipMemcpyAsync(m_absmax[k], base + t.ma, nb * 4, D2H, ds));
+            LT_HIP(hipMemcpyAsync(v_absmax[k], base + t.va, nb * 4, D2H, ds));
+        }
+        LT_HIP(hipEventRecord(ev.freed[sl], ds));
+        used[sl] = true;
+    }
+    // The call's work ends on the compute stream once the last copy out is done.
+    LT_HIP(hipEventRecord(ev.done, ds));
+    LT_HIP(hipStreamWaitEvent(cs, ev.done, 0));
+    return LT_OK;
 }
 
 lt_err lt_read_status(const int32_t* status, void* stream, int32_t* out)

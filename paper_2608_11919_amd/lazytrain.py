@@ -55,12 +55,20 @@ def lib() -> ctypes.CDLL:
     L.lt_hybrid8bit_adamw_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, i64p,
                                            ctypes.c_int, ctypes.c_int] + [ctypes.c_double] * 5 + [
                                                ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp]
+    ip = ctypes.POINTER(ctypes.c_int)
+    L.lt_streamed_workspace_bytes.argtypes = [i64p, ctypes.c_int, ip, ctypes.c_int, ctypes.c_int,
+                                              ctypes.c_int, ctypes.c_int]
+    L.lt_streamed_workspace_bytes.restype = ctypes.c_size_t
+    L.lt_streamed_hybrid8bit_adamw_step.argtypes = [
+        vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, i64p, ctypes.c_int, ip, ctypes.c_int,
+        ctypes.c_int] + [ctypes.c_double] * 5 + [ctypes.c_int64, ctypes.c_float, ctypes.c_int, vp,
+                                                 ctypes.c_size_t, vp, vp, vp, vp, vp, vp, vp]
     L.lt_read_status.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32)]
     L.lt_set_max_workgroups.argtypes = [ctypes.c_int]
     L.lt_last_error.argtypes = []
     L.lt_last_error.restype = ctypes.c_char_p
     for name in ("lt_grad_sqnorm", "lt_clip_coef", "lt_hybrid8bit_adamw_step", "lt_read_status",
-                 "lt_set_max_workgroups"):
+                 "lt_set_max_workgroups", "lt_streamed_hybrid8bit_adamw_step"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -208,6 +216,69 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
         float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
         _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
         ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
+
+
+def lt_streamed_workspace_bytes(numels: Sequence[int], layer_first: Sequence[int],
+                                grad_dtype: int, block_size: int, ring_slots: int) -> int:
+    n = (ctypes.c_int64 * len(numels))(*numels)
+    f = (ctypes.c_int * len(layer_first))(*layer_first)
+    return int(lib().lt_streamed_workspace_bytes(n, len(numels), f, len(layer_first) - 1,
+                                                 grad_dtype, block_size, ring_slots))
+
+
+def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes, v_absmax,
+                                      layer_first: Sequence[int], block_size: int, lr: float,
+                                      beta1: float, beta2: float, eps: float,
+                                      weight_decay: float, step: int, max_norm: float,
+                                      ring_slots: int, sq_total: torch.Tensor,
+                                      coef: torch.Tensor, status: torch.Tensor,
+                                      total_norm: Optional[torch.Tensor] = None,
+                                      workspace: Optional[torch.Tensor] = None,
+                                      compute_stream=None, h2d_stream=None,
+                                      d2h_stream=None) -> None:
+    """Step a11: host-resident tensors (CPU, ideally pinned) streamed layer by layer
+    through HBM; scalar outputs are device tensors (see include/lazytrain.h)."""
+    k = len(params)
+    if k == 0 or not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) ==
+                      len(v_absmax) == k):
+        raise ValueError("tensor lists must be non-empty and of equal length")
+    cpu = torch.device("cpu")
+    _check_tensors(params, cpu, torch.float32, "params")
+    _check_tensors(grads, cpu, what="grads")
+    _check_tensors(m_codes, cpu, torch.int8, "m_codes")
+    _check_tensors(v_codes, cpu, torch.uint8, "v_codes")
+    _check_tensors(m_absmax, cpu, torch.float32, "m_absmax")
+    _check_tensors(v_absmax, cpu, torch.float32, "v_absmax")
+    gdt = _grad_dtype(grads)
+    for i in range(k):
+        n = params[i].numel()
+        nb = -(-n // block_size)
+        if grads[i].numel() != n or m_codes[i].numel() != n or v_codes[i].numel() != n:
+            raise ValueError(f"tensor {i}: params, grads and codes must have {n} elements")
+        if m_absmax[i].numel() < nb or v_absmax[i].numel() < nb:
+            raise ValueError(f"tensor {i}: absmax arrays need {nb} entries")
+    device = sq_total.device
+    numels = [p.numel() for p in params]
+    nbytes = lt_streamed_workspace_bytes(numels, layer_first, gdt, block_size, ring_slots)
+    if nbytes == 0:
+        raise ValueError("invalid layer_first, block_size or ring_slots")
+    cs = _stream_handle(compute_stream, device)
+    workspace = _workspace(device, nbytes, workspace, compute_stream)
+    if compute_stream is not None and hasattr(compute_stream, "cuda_stream"):
+        workspace.record_stream(compute_stream)  # in use on that stream until the step is done
+    first = (ctypes.c_int * len(layer_first))(*layer_first)
+    hs = _stream_handle(h2d_stream, device) if h2d_stream is not None else cs
+    ds = _stream_handle(d2h_stream, device) if d2h_stream is not None else cs
+    _check(lib().lt_streamed_hybrid8bit_adamw_step(
+        _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
+        _ptr_array(v_codes), _ptr_array(v_absmax), _numel_array(params), k, first,
+        len(layer_first) - 1, int(block_size), float(lr), float(beta1), float(beta2), float(eps),
+        float(weight_decay), int(step), float(max_norm), int(ring_slots), workspace.data_ptr(),
+        workspace.numel() * workspace.element_size(),
+        _scalar(sq_total, device, torch.float64, "sq_total"),
+        _scalar(total_norm, device, torch.float32, "total_norm"),
+        _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
+        cs, hs, ds))
 
 
 def lt_read_status(status: torch.Tensor, stream=None) -> int:
