@@ -124,17 +124,31 @@ def _oracle_pass(w, ks, n_threads):
     return time.perf_counter() - t0
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, n_threads, target_s: float):
     """The oracle as it stands, on a bounded sample of the same workload (whole
     tensors, decoder layers first, the embedding last), timed on this host's cores.
-    One decoder layer is timed first to size a sample of about target_s seconds."""
+    One decoder layer is timed first to size a sample of about target_s seconds;
+    the same layer is also timed on one thread."""
     K = len(w.shapes)
     order = list(range(K))
     if len(w.shapes[0]) == 2 and w.shapes[0][0] > 100000:
         order = order[1:] + order[:1]
     first = order[:min(K, 9)]
+    n_first = sum(w.numels[k] for k in first)
     dt = _oracle_pass(w, first, n_threads)
-    rate = sum(w.numels[k] for k in first) / dt
+    rate = n_first / dt
+    dt1 = _oracle_pass(w, first, 1)
     ks, total = [], 0
     for k in order:
         if ks and total + w.numels[k] > rate * target_s:
@@ -145,7 +159,12 @@ def cpu_baseline(w, n_threads, target_s: float):
         dt = _oracle_pass(w, ks, n_threads)
     desc = f"{len(ks)} of {K} tensors ({total} of {w.n_params} params) of {w.name}"
     return {"value": total / dt, "unit": "params/s", "cores": n_threads, "kind": "oracle",
-            "sample": desc + ": sum of squares + clip + step, one pass", "seconds": round(dt, 3)}
+            "sample": desc + ": sum of squares + clip + step, one pass", "seconds": round(dt, 3),
+            "single_thread": {"value": n_first / dt1, "unit": "params/s",
+                              "sample": f"{len(first)} tensors ({n_first} params), one thread",
+                              "seconds": round(dt1, 3)},
+            "cpu_model": cpu_model(),
+            "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
 COUNTERS = os.path.join(ROOT, "profiles", "adamw8_step_3b_full_counters.json")
@@ -324,6 +343,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU seconds for the oracle sample")
+    ap.add_argument("--slice-fraction", type=float, default=None,
+                    help="hybrid operator: only this fraction of parameters keeps 8-bit states, "
+                         "the rest fp32 states (the paper's run uses 0.02)")
     ap.add_argument("--host-layers", type=int, default=8,
                     help="streamed workload: distinct pinned host layers the model cycles over")
     ap.add_argument("--ring-slots", type=int, default=3, help="streamed workload: device slots")
@@ -357,6 +379,18 @@ def main() -> int:
         return run_streamed(args, w, dev, n_threads)
 
     params, grads, mq, ma, vq, va, t_first = build_device_workload(w, dev, n_threads)
+    idx8, idx32 = list(range(K)), []
+    if args.slice_fraction is not None:
+        mask, _ = lt.lt_select_8bit_slice(w.numels, args.slice_fraction)
+        idx8 = [k for k in range(K) if mask[k]]
+        idx32 = [k for k in range(K) if not mask[k]]
+        for k in idx32:  # the fp32-state tensors need no 8-bit states
+            mq[k] = vq[k] = ma[k] = va[k] = None
+        torch.cuda.empty_cache()
+        exp_avg = [torch.zeros_like(params[k]) for k in idx32]
+        exp_avg_sq = [torch.zeros_like(params[k]) for k in idx32]
+        log(f"hybrid: {len(idx8)} tensors ({sum(w.numels[k] for k in idx8)} params) with 8-bit "
+            f"states, {len(idx32)} with fp32 states")
     sq_total = torch.zeros(1, dtype=torch.float64, device=dev)
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     coef = torch.zeros(1, dtype=torch.float32, device=dev)
@@ -365,6 +399,11 @@ def main() -> int:
     hyper = dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay)
     ws_sq = torch.empty(lt.lt_grad_sqnorm_workspace_bytes(w.numels), dtype=torch.uint8, device=dev)
     ws_step = torch.empty(lt.lt_step_workspace_bytes(K), dtype=torch.uint8, device=dev)
+    ws_32 = torch.empty(max(1, lt.lt_adamw_fp32_workspace_bytes(len(idx32))), dtype=torch.uint8,
+                        device=dev)
+    p8, g8 = [params[k] for k in idx8], [grads[k] for k in idx8]
+    s8 = [[x[k] for k in idx8] for x in (mq, ma, vq, va)]
+    p32, g32 = [params[k] for k in idx32], [grads[k] for k in idx32]
 
     def one_step(t, ev=None):
         if ev:
@@ -373,8 +412,12 @@ def main() -> int:
         lt.lt_clip_coef(sq_total, w.max_norm, coef, total_norm=norm, stream=stream)
         if ev:
             ev[1].record(stream)
-        lt.lt_hybrid8bit_adamw_step(params, grads, mq, ma, vq, va, B, step=t, coef=coef,
-                                    status=status, workspace=ws_step, stream=stream, **hyper)
+        if p8:
+            lt.lt_hybrid8bit_adamw_step(p8, g8, *s8, B, step=t, coef=coef, status=status,
+                                        workspace=ws_step, stream=stream, **hyper)
+        if p32:
+            lt.lt_adamw_fp32_step(p32, g32, exp_avg, exp_avg_sq, step=t, coef=coef,
+                                  status=status, workspace=ws_32, stream=stream, **hyper)
         if ev:
             ev[2].record(stream)
 
@@ -395,10 +438,16 @@ def main() -> int:
 
     norm_ms = [e[0].elapsed_time(e[1]) for e in events]
     step_ms = [e[1].elapsed_time(e[2]) for e in events]
+    whole_ms = sorted(e[0].elapsed_time(e[2]) for e in events)
+
+    def pct(q):  # nearest-rank percentile of the per-step times
+        return round(whole_ms[min(len(whole_ms) - 1, max(0, math.ceil(q * len(whole_ms)) - 1))], 4)
+
     avg_step_s = sum(step_ms) / len(step_ms) * 1e-3
     avg_norm_s = sum(norm_ms) / len(norm_ms) * 1e-3
     gb = grad_bytes(w.grad_dtype)
-    kbytes = step_kernel_bytes(w.numels, B, gb)
+    kbytes = step_kernel_bytes([w.numels[k] for k in idx8], B, gb) + \
+        sum(w.numels[k] for k in idx32) * (gb + 24)  # fp32 states: w, m, v read and written
     nbytes = norm_bytes(w.numels, gb)
     ms_per_step = elapsed / args.steps * 1e3
     step_total_bytes = kbytes + nbytes
@@ -420,7 +469,11 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "params": w.n_params, "tensors": K, "block_size": B,
+        "step_ms_events": {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9)},
+        "config": {"workload": w.name + ("" if not idx32 else
+                                         f"-hybrid-{args.slice_fraction:g}-8bit"),
+                   "params": w.n_params, "tensors": K, "block_size": B,
+                   "params_8bit": sum(w.numels[k] for k in idx8),
                    "grad_dtype": "bf16" if w.grad_dtype == synth.BF16 else "f32",
                    "states": "int8 m / uint8 v, fp32 absmax per block",
                    "master": "fp32", "norm_accumulation": "f64",
@@ -431,10 +484,11 @@ def main() -> int:
         "bytes_per_param": round(step_total_bytes / w.n_params, 4),
         "kernels_ms": {"norm_pass": round(avg_norm_s * 1e3, 4),
                        "adamw8_step": round(avg_step_s * 1e3, 4)},
-        "roofline": {"kernel": "k_adamw8_step", "bound": "hbm", "achieved": round(achieved, 1),
+        "roofline": {"kernel": "k_adamw8_step" if not idx32 else "k_adamw8_step + k_adamw32_step",
+                     "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                     "traffic": counter_traffic(w.name),
+                     "traffic": counter_traffic(w.name) if not idx32 else None,
                      "bytes_per_launch": kbytes},
         "status": st,
     }

@@ -193,6 +193,37 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                          float* total_norm, float* coef, int32_t* status,
                                          void* compute_stream, void* h2d_stream, void* d2h_stream);
 
+/* Bytes of device workspace lt_adamw_fp32_step needs for n_tensors tensors. */
+size_t lt_adamw_fp32_workspace_bytes(int n_tensors);
+
+/*
+ * fp32-state AdamW over a list of tensors: the part of the Hybrid 8-bit
+ * operator that keeps full-precision optimizer states (Sec. 3.5: DeepSpeed
+ * CPUAdam handles most parameters, a 2% slice uses 8-bit states; App. C
+ * variant table).  exp_avg[k], exp_avg_sq[k] are device float[numels[k]], read
+ * and written.  Per element, the same fp32 operations as
+ * lt_hybrid8bit_adamw_step with m0, v0 taken from and m1, v1 stored to these
+ * arrays.  coef and status as there (NULL: no clipping / never skip).
+ * Pointers 16-byte aligned; workspace 256-byte aligned.
+ */
+lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int grad_dtype,
+                          float* const* exp_avg, float* const* exp_avg_sq, const int64_t* numels,
+                          int n_tensors, double lr, double beta1, double beta2, double eps,
+                          double weight_decay, int64_t step, const float* coef,
+                          const int32_t* status, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+/*
+ * Chooses the tensors that take 8-bit states when only a fraction of the
+ * parameters should (Sec. 3.5: a 2% parameter slice; the paper does not say
+ * which).  Greedy by decreasing size, ties in list order: a tensor is taken
+ * when the running total stays <= fraction * total parameters.  Host only.
+ *   is_8bit       host uint8[n_tensors]: 1 for a chosen tensor, else 0.
+ *   n_8bit_params host int64 or NULL: parameters chosen.
+ */
+lt_err lt_select_8bit_slice(const int64_t* numels, int n_tensors, double fraction,
+                            uint8_t* is_8bit, int64_t* n_8bit_params);
+
 /* Copies the device status word to *out and synchronizes `stream` (the only
  * entry point that blocks the host).  An asynchronous device fault from
  * earlier work on the stream surfaces here as LT_ERR_HIP. */

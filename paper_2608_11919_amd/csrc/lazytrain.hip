@@ -579,10 +579,14 @@ __global__ __launch_bounds__(64) void k_clip_coef(const double* __restrict__ sq_
 // block absmax is a wave reduction; for B = 4096 and 8192, B/2048 waves of a
 // workgroup share a block and combine their maxima in LDS.
 
-// 32 elements per lane keeps 16 KB of long contiguous runs in flight per wave
-// (about 220 VGPRs, two waves per SIMD); measured on the 3B-class step it beats
-// 16 and 8 per lane, and forcing more waves per SIMD is slower still.
+// 32 elements per lane amortizes the per-block work (scales, maxima, the sqrt
+// ballot) over long contiguous runs; measured on the 3B-class step it beats 16
+// and 8 per lane.  The lane's granules are loaded and updated in kStepPhases
+// phases (when its granule count divides evenly), which bounds the registers the
+// loads occupy: about 150 VGPRs, three waves per SIMD.  One, two and four phases
+// time within 0.5% of each other; four is the fastest of them.
 constexpr int kStepElemsPerLane = 32;
+constexpr int kStepPhases = 4;
 
 template <int B>
 struct StepGeom {
@@ -593,6 +597,8 @@ struct StepGeom {
     static constexpr int W = B > WAVE_SPAN ? B / WAVE_SPAN : 1;        // waves per block
     static constexpr int L = B >= 512 ? 64 : B / kGranule;             // lanes per block in a wave
     static constexpr int UNIT = W > 1 ? 4 * WAVE_SPAN : WAVE_SPAN;      // elements per work unit
+    static constexpr int PH = G % kStepPhases == 0 ? kStepPhases : 1;   // load phases
+    static_assert(W <= 4, "a block spans at most the four waves of one workgroup");
 };
 
 __device__ inline float wave_max_xor(float x, int width)
@@ -689,7 +695,7 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                                                           const int32_t* __restrict__ status_ptr)
 {
     using Geo = StepGeom<B>;
-    constexpr int E = Geo::E, G = Geo::G, W = Geo::W, L = Geo::L, UNIT = Geo::UNIT;
+    constexpr int E = Geo::E, G = Geo::G, W = Geo::W, L = Geo::L, UNIT = Geo::UNIT, PH = Geo::PH;
     __shared__ float red[2][2][4];  // [buffer][m, v][wave], used when W > 1
 
     if (status_ptr && *status_ptr == LT_STATUS_NONFINITE)
@@ -720,18 +726,6 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
         const int64_t n_span = d.numel - e0;        // elements left from e0 (may be <= 0)
         const bool full = n_span >= Geo::WAVE_SPAN;  // wave-uniform
 
-        StepIn<GT> in[G];
-        if (full) {
-#pragma unroll
-            for (int j = 0; j < G; ++j)
-                load_step_full(d, e0 + kGranule * (lane + 64 * j), in[j]);
-        } else {
-#pragma unroll
-            for (int j = 0; j < G; ++j) {
-                const int64_t o = kGranule * (lane + 64 * j);
-                load_step_ragged(d, e0 + o, int(i64min(i64max(n_span - o, 0), kGranule)), in[j]);
-            }
-        }
         // Stored scales of this lane's block (one block per lane for B >= 512).
         float a_m, a_v;
         {
@@ -743,59 +737,81 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
         const float step_m = div_by_const<127>(a_m);
         const float step_v = div_by_const<255>(a_v);
 
-        // Moments.  Elements past the end read as zero gradient and zero codes,
-        // so they produce m1 = v1 = 0 (or NaN from a non-finite stored scale)
-        // and leave the block maxima unchanged.
+        // The lane's granules go through load -> moments -> sqrt/divide -> weight
+        // store in PH phases, which bounds the registers the loads occupy.  m1 and
+        // v1 of every granule stay for the block's requantization.  Elements past
+        // the end read as zero gradient and zero codes, so they produce
+        // m1 = v1 = 0 (or NaN from a non-finite stored scale) and leave the block
+        // maxima unchanged.
         float m1[E], v1[E];
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            float g[8];
-            unpack8(in[j].g, g);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const uint32_t mw = e < 4 ? in[j].m.x : in[j].m.y;
-                const uint32_t vw = e < 4 ? in[j].v.x : in[j].v.y;
-                const float qm = float(int8_t(mw >> (8 * (e & 3))));
-                const float qv = float((vw >> (8 * (e & 3))) & 0xFFu);
-                const float gc = g[e] * coef;
-                m1[8 * j + e] = __builtin_fmaf(s.beta1, qm * step_m, s.c1 * gc);
-                v1[8 * j + e] = __builtin_fmaf(s.beta2, qv * step_v, s.c2 * (gc * gc));
-            }
-        }
-        // sqrt: the short correction sequence is exact unless some v1 of the
-        // wave lies in (0, 2^-96); then every lane takes the full sqrtf.
-        uint32_t vmin = 0xFFFFFFFFu;
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-            vmin = min(vmin, __float_as_uint(v1[e]) - 1u);  // 0 wraps to the top
-        const bool tiny = vmin < 0x0F800000u - 1u;          // 0 < v1 < 2^-96
-        const bool scaled = __builtin_amdgcn_ballot_w64(tiny) != 0;
-
         float amax_m = 0.0f, amax_v = 0.0f;
 #pragma unroll
-        for (int j = 0; j < G; ++j) {
-            float w[8];
-            w[0] = __uint_as_float(in[j].w[0].x); w[1] = __uint_as_float(in[j].w[0].y);
-            w[2] = __uint_as_float(in[j].w[0].z); w[3] = __uint_as_float(in[j].w[0].w);
-            w[4] = __uint_as_float(in[j].w[1].x); w[5] = __uint_as_float(in[j].w[1].y);
-            w[6] = __uint_as_float(in[j].w[1].z); w[7] = __uint_as_float(in[j].w[1].w);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float m = m1[8 * j + e], v = v1[8 * j + e];
-                const float root = scaled ? sqrtf(v) : sqrt_rn_unscaled(v);
-                const float den = __builtin_fmaf(root, s.rbc2, s.eps);
-                w[e] = __builtin_fmaf(-s.step_size, m / den, w[e] * s.decay);
-                amax_m = fmaxf(amax_m, fabsf(m));
-                amax_v = fmaxf(amax_v, v);
-            }
-            const int64_t ei = e0 + kGranule * (lane + 64 * j);
+        for (int ph = 0; ph < PH; ++ph) {
+            constexpr int GP = G / PH;
+            StepIn<GT> in[GP];
             if (full) {
-                *reinterpret_cast<float4*>(d.w + ei) = make_float4(w[0], w[1], w[2], w[3]);
-                *reinterpret_cast<float4*>(d.w + ei + 4) = make_float4(w[4], w[5], w[6], w[7]);
+#pragma unroll
+                for (int jj = 0; jj < GP; ++jj)
+                    load_step_full(d, e0 + kGranule * (lane + 64 * (ph * GP + jj)), in[jj]);
             } else {
-                const int nv = int(i64min(i64max(n_span - kGranule * (lane + 64 * j), 0), kGranule));
-                for (int e = 0; e < nv; ++e)
-                    d.w[ei + e] = w[e];
+#pragma unroll
+                for (int jj = 0; jj < GP; ++jj) {
+                    const int64_t o = kGranule * (lane + 64 * (ph * GP + jj));
+                    load_step_ragged(d, e0 + o, int(i64min(i64max(n_span - o, 0), kGranule)),
+                                     in[jj]);
+                }
+            }
+#pragma unroll
+            for (int jj = 0; jj < GP; ++jj) {
+                const int j = ph * GP + jj;
+                float g[8];
+                unpack8(in[jj].g, g);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t mw = e < 4 ? in[jj].m.x : in[jj].m.y;
+                    const uint32_t vw = e < 4 ? in[jj].v.x : in[jj].v.y;
+                    const float qm = float(int8_t(mw >> (8 * (e & 3))));
+                    const float qv = float((vw >> (8 * (e & 3))) & 0xFFu);
+                    const float gc = g[e] * coef;
+                    m1[8 * j + e] = __builtin_fmaf(s.beta1, qm * step_m, s.c1 * gc);
+                    v1[8 * j + e] = __builtin_fmaf(s.beta2, qv * step_v, s.c2 * (gc * gc));
+                }
+            }
+            // sqrt: the short correction sequence is exact unless some v1 of the
+            // wave (in this phase) lies in (0, 2^-96); then every lane takes the
+            // full sqrtf.
+            uint32_t vmin = 0xFFFFFFFFu;
+#pragma unroll
+            for (int e = ph * 8 * GP; e < (ph + 1) * 8 * GP; ++e)
+                vmin = min(vmin, __float_as_uint(v1[e]) - 1u);  // 0 wraps to the top
+            const bool scaled = __builtin_amdgcn_ballot_w64(vmin < 0x0F800000u - 1u) != 0;
+#pragma unroll
+            for (int jj = 0; jj < GP; ++jj) {
+                const int j = ph * GP + jj;
+                float w[8];
+                w[0] = __uint_as_float(in[jj].w[0].x); w[1] = __uint_as_float(in[jj].w[0].y);
+                w[2] = __uint_as_float(in[jj].w[0].z); w[3] = __uint_as_float(in[jj].w[0].w);
+                w[4] = __uint_as_float(in[jj].w[1].x); w[5] = __uint_as_float(in[jj].w[1].y);
+                w[6] = __uint_as_float(in[jj].w[1].z); w[7] = __uint_as_float(in[jj].w[1].w);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float m = m1[8 * j + e], v = v1[8 * j + e];
+                    const float root = scaled ? sqrtf(v) : sqrt_rn_unscaled(v);
+                    const float den = __builtin_fmaf(root, s.rbc2, s.eps);
+                    w[e] = __builtin_fmaf(-s.step_size, m / den, w[e] * s.decay);
+                    amax_m = fmaxf(amax_m, fabsf(m));
+                    amax_v = fmaxf(amax_v, v);
+                }
+                const int64_t ei = e0 + kGranule * (lane + 64 * j);
+                if (full) {
+                    *reinterpret_cast<float4*>(d.w + ei) = make_float4(w[0], w[1], w[2], w[3]);
+                    *reinterpret_cast<float4*>(d.w + ei + 4) = make_float4(w[4], w[5], w[6], w[7]);
+                } else {
+                    const int nv =
+                        int(i64min(i64max(n_span - kGranule * (lane + 64 * j), 0), kGranule));
+                    for (int e = 0; e < nv; ++e)
+                        d.w[ei + e] = w[e];
+                }
             }
         }
 
@@ -859,6 +875,134 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                 d.ma[blk] = ok_m ? amax_m : 0.0f;
                 d.va[blk] = ok_v ? amax_v : 0.0f;
             }
+        }
+    }
+}
+
+// ------------------------------------------ f1: fp32-state fused AdamW
+//
+// The part of the hybrid operator that keeps fp32 moments (the role DeepSpeed
+// CPUAdam plays for most parameters in the paper's run): the same per-element
+// arithmetic as the 8-bit step with m0, v0 read from and m1, v1 written to fp32
+// arrays, 26 B/param with bf16 gradients.  A wave owns spans of 64 x 16
+// elements; there is no cross-lane work.
+
+struct Fp32Tensor {
+    float* w;
+    const void* g;
+    float* m;
+    float* v;
+    int64_t numel;
+    int64_t pad_[3];
+};
+static_assert(sizeof(Fp32Tensor) == 64, "descriptor is one 64-byte line");
+
+constexpr int kFp32ElemsPerLane = 16;
+
+__device__ inline void load8f(const float* p, int nv, float (&x)[8])
+{
+    if (nv >= kGranule) {
+        const uint4 a = load16(p), b = load16(p + 4);
+        x[0] = __uint_as_float(a.x); x[1] = __uint_as_float(a.y);
+        x[2] = __uint_as_float(a.z); x[3] = __uint_as_float(a.w);
+        x[4] = __uint_as_float(b.x); x[5] = __uint_as_float(b.y);
+        x[6] = __uint_as_float(b.z); x[7] = __uint_as_float(b.w);
+        return;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        x[e] = e < nv ? p[e] : 0.0f;
+}
+
+__device__ inline void store8f(float* p, int nv, const float (&x)[8])
+{
+    if (nv >= kGranule) {
+        *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+        *reinterpret_cast<float4*>(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
+        return;
+    }
+    for (int e = 0; e < nv; ++e)
+        p[e] = x[e];
+}
+
+template <typename GT>
+__global__ __launch_bounds__(kThreads) void k_adamw32_step(const int64_t* __restrict__ unit_prefix,
+                                                           const Fp32Tensor* __restrict__ desc,
+                                                           int n_tensors, int64_t n_units,
+                                                           StepScalars s,
+                                                           const float* __restrict__ coef_ptr,
+                                                           const int32_t* __restrict__ status_ptr)
+{
+    constexpr int E = kFp32ElemsPerLane, G = E / kGranule, SPAN = 64 * E;
+    if (status_ptr && *status_ptr == LT_STATUS_NONFINITE)
+        return;  // skipped step: nothing is written
+    const float coef = coef_ptr ? *coef_ptr : 1.0f;
+    const int lane = threadIdx.x & 63;
+    int64_t u_begin, u_end;
+    {
+        const int64_t workers = int64_t(gridDim.x) * 4;
+        const int64_t me = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+        const int64_t per = n_units / workers, rem = n_units % workers;
+        u_begin = me * per + (me < rem ? me : rem);
+        u_end = u_begin + per + (me < rem ? 1 : 0);
+    }
+    int k = u_begin < u_end ? find_tensor(unit_prefix, n_tensors, u_begin) : 0;
+    for (int64_t u = u_begin; u < u_end; ++u) {
+        while (u >= unit_prefix[k + 1])
+            ++k;
+        const Fp32Tensor d = desc[k];
+        const int64_t e0 = (u - unit_prefix[k]) * SPAN;
+        const int64_t n_span = d.numel - e0;
+        float w[E], g[E], m[E], v[E];
+        int nv[G];
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int64_t o = kGranule * (lane + 64 * j);
+            nv[j] = int(i64min(i64max(n_span - o, 0), kGranule));
+            const int64_t ei = e0 + o;
+            GradWords<GT> gw;
+            load_grads<false>(static_cast<const GT*>(d.g) + ei, nv[j], gw);
+            float gg[8], ww[8], mm[8], vv[8];
+            unpack8(gw, gg);
+            load8f(d.w + ei, nv[j], ww);
+            load8f(d.m + ei, nv[j], mm);
+            load8f(d.v + ei, nv[j], vv);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                w[8 * j + e] = ww[e];
+                g[8 * j + e] = gg[e];
+                m[8 * j + e] = mm[e];
+                v[8 * j + e] = vv[e];
+            }
+        }
+        uint32_t vmin = 0xFFFFFFFFu;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const float gc = g[e] * coef;
+            m[e] = __builtin_fmaf(s.beta1, m[e], s.c1 * gc);
+            v[e] = __builtin_fmaf(s.beta2, v[e], s.c2 * (gc * gc));
+            vmin = min(vmin, __float_as_uint(v[e]) - 1u);
+        }
+        const bool scaled = __builtin_amdgcn_ballot_w64(vmin < 0x0F800000u - 1u) != 0;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const float root = scaled ? sqrtf(v[e]) : sqrt_rn_unscaled(v[e]);
+            const float den = __builtin_fmaf(root, s.rbc2, s.eps);
+            w[e] = __builtin_fmaf(-s.step_size, m[e] / den, w[e] * s.decay);
+        }
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int64_t ei = e0 + kGranule * (lane + 64 * j);
+            float ww[8], mm[8], vv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                ww[e] = w[8 * j + e];
+                mm[e] = m[8 * j + e];
+                vv[e] = v[8 * j + e];
+            }
+            store8f(d.w + ei, nv[j], ww);
+            store8f(d.m + ei, nv[j], mm);
+            store8f(d.v + ei, nv[j], vv);
         }
     }
 }
@@ -1408,6 +1552,103 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
     // The call's work ends on the compute stream once the last copy out is done.
     LT_HIP(hipEventRecord(ev.done, ds));
     LT_HIP(hipStreamWaitEvent(cs, ev.done, 0));
+    return LT_OK;
+}
+
+size_t lt_adamw_fp32_workspace_bytes(int n_tensors)
+{
+    return n_tensors < 1 ? 0 : round_up(round_up(sizeof(int64_t) * (n_tensors + 1), 64) +
+                                            sizeof(Fp32Tensor) * size_t(n_tensors), 256);
+}
+
+lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int grad_dtype,
+                          float* const* exp_avg, float* const* exp_avg_sq, const int64_t* numels,
+                          int n_tensors, double lr, double beta1, double beta2, double eps,
+                          double weight_decay, int64_t step, const float* coef,
+                          const int32_t* status, void* workspace, size_t workspace_bytes,
+                          void* stream)
+{
+    g_last_error.clear();
+    const int K = n_tensors;
+    if (!params || !grads || !exp_avg || !exp_avg_sq || !valid_list(numels, K))
+        return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 1 entries with numel >= 1");
+    if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
+        return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
+    if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step))
+        return fail(LT_ERR_INVALID_ARG,
+                    "need finite lr, weight_decay, eps >= 0, 0 <= beta1, beta2 < 1 and step >= 1");
+    if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)))
+        return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned");
+    for (int k = 0; k < K; ++k) {
+        if (!params[k] || !grads[k] || !exp_avg[k] || !exp_avg_sq[k])
+            return fail(LT_ERR_INVALID_ARG, "NULL tensor pointer at index " + std::to_string(k));
+        if (!aligned(params[k], 16) || !aligned(grads[k], 16) || !aligned(exp_avg[k], 16) ||
+            !aligned(exp_avg_sq[k], 16))
+            return fail(LT_ERR_ALIGNMENT, "tensor " + std::to_string(k) + " is not 16-byte aligned");
+    }
+    const size_t desc_at = round_up(sizeof(int64_t) * (K + 1), 64);
+    const size_t total = lt_adamw_fp32_workspace_bytes(K);
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < total)
+        return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
+                                          std::to_string(total) + " bytes");
+    constexpr int64_t span = 64 * kFp32ElemsPerLane;
+    std::vector<uint8_t> host(total, 0);
+    auto* prefix = reinterpret_cast<int64_t*>(host.data());
+    auto* desc = reinterpret_cast<Fp32Tensor*>(host.data() + desc_at);
+    prefix[0] = 0;
+    for (int k = 0; k < K; ++k) {
+        prefix[k + 1] = prefix[k] + (numels[k] + span - 1) / span;
+        desc[k] = Fp32Tensor{params[k], grads[k], exp_avg[k], exp_avg_sq[k], numels[k], {0, 0, 0}};
+    }
+    const int64_t units = prefix[K];
+    const StepScalars sc = make_scalars(lr, beta1, beta2, eps, weight_decay, step);
+    auto* ws = static_cast<uint8_t*>(workspace);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (lt_err e = upload(host.data(), host.size(), ws, st))
+        return e;
+    const auto* d_prefix = reinterpret_cast<const int64_t*>(ws);
+    const auto* d_desc = reinterpret_cast<const Fp32Tensor*>(ws + desc_at);
+    int grid;
+    if (grad_dtype == LT_DTYPE_BF16) {
+        if (lt_err e = grid_size(k_adamw32_step<uint16_t>, (units + 3) / 4, &grid))
+            return e;
+        k_adamw32_step<uint16_t><<<grid, kThreads, 0, st>>>(d_prefix, d_desc, K, units, sc, coef,
+                                                            status);
+    } else {
+        if (lt_err e = grid_size(k_adamw32_step<float>, (units + 3) / 4, &grid))
+            return e;
+        k_adamw32_step<float><<<grid, kThreads, 0, st>>>(d_prefix, d_desc, K, units, sc, coef,
+                                                         status);
+    }
+    LT_HIP(hipGetLastError());
+    return LT_OK;
+}
+
+lt_err lt_select_8bit_slice(const int64_t* numels, int n_tensors, double fraction,
+                            uint8_t* is_8bit, int64_t* n_8bit_params)
+{
+    g_last_error.clear();
+    if (!valid_list(numels, n_tensors) || !is_8bit || !(fraction >= 0.0 && fraction <= 1.0))
+        return fail(LT_ERR_INVALID_ARG, "need n_tensors >= 1 numels >= 1, is_8bit and 0 <= fraction <= 1");
+    int64_t total = 0;
+    for (int k = 0; k < n_tensors; ++k)
+        total += numels[k];
+    const double target = fraction * double(total);
+    std::vector<int> order(n_tensors);
+    for (int k = 0; k < n_tensors; ++k)
+        order[k] = k;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int a, int b) { return numels[a] > numels[b]; });
+    int64_t chosen = 0;
+    for (int k = 0; k < n_tensors; ++k)
+        is_8bit[k] = 0;
+    for (int k : order)
+        if (double(chosen + numels[k]) <= target) {
+            is_8bit[k] = 1;
+            chosen += numels[k];
+        }
+    if (n_8bit_params)
+        *n_8bit_params = chosen;
     return LT_OK;
 }
 

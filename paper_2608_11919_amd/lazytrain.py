@@ -63,12 +63,20 @@ def lib() -> ctypes.CDLL:
         vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, i64p, ctypes.c_int, ip, ctypes.c_int,
         ctypes.c_int] + [ctypes.c_double] * 5 + [ctypes.c_int64, ctypes.c_float, ctypes.c_int, vp,
                                                  ctypes.c_size_t, vp, vp, vp, vp, vp, vp, vp]
+    L.lt_adamw_fp32_workspace_bytes.argtypes = [ctypes.c_int]
+    L.lt_adamw_fp32_workspace_bytes.restype = ctypes.c_size_t
+    L.lt_adamw_fp32_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, i64p, ctypes.c_int] + [
+        ctypes.c_double] * 5 + [ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp]
+    L.lt_select_8bit_slice.argtypes = [i64p, ctypes.c_int, ctypes.c_double,
+                                       ctypes.POINTER(ctypes.c_uint8),
+                                       ctypes.POINTER(ctypes.c_int64)]
     L.lt_read_status.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32)]
     L.lt_set_max_workgroups.argtypes = [ctypes.c_int]
     L.lt_last_error.argtypes = []
     L.lt_last_error.restype = ctypes.c_char_p
     for name in ("lt_grad_sqnorm", "lt_clip_coef", "lt_hybrid8bit_adamw_step", "lt_read_status",
-                 "lt_set_max_workgroups", "lt_streamed_hybrid8bit_adamw_step"):
+                 "lt_set_max_workgroups", "lt_streamed_hybrid8bit_adamw_step",
+                 "lt_adamw_fp32_step", "lt_select_8bit_slice"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -281,6 +289,48 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
         cs, hs, ds))
 
 
+def lt_adamw_fp32_workspace_bytes(n_tensors: int) -> int:
+    return int(lib().lt_adamw_fp32_workspace_bytes(n_tensors))
+
+
+def lt_adamw_fp32_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Tensor],
+                       exp_avg: Sequence[torch.Tensor], exp_avg_sq: Sequence[torch.Tensor],
+                       lr: float, beta1: float, beta2: float, eps: float, weight_decay: float,
+                       step: int, coef: Optional[torch.Tensor] = None,
+                       status: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """fp32-state AdamW, in place on params, exp_avg and exp_avg_sq (device tensors)."""
+    k = len(params)
+    if k == 0 or not (len(grads) == len(exp_avg) == len(exp_avg_sq) == k):
+        raise ValueError("tensor lists must be non-empty and of equal length")
+    device = params[0].device
+    _check_tensors(params, device, torch.float32, "params")
+    _check_tensors(grads, device, what="grads")
+    _check_tensors(exp_avg, device, torch.float32, "exp_avg")
+    _check_tensors(exp_avg_sq, device, torch.float32, "exp_avg_sq")
+    gdt = _grad_dtype(grads)
+    for i in range(k):
+        n = params[i].numel()
+        if grads[i].numel() != n or exp_avg[i].numel() != n or exp_avg_sq[i].numel() != n:
+            raise ValueError(f"tensor {i}: params, grads and states must have {n} elements")
+    ws = _workspace(device, lt_adamw_fp32_workspace_bytes(k), workspace, stream)
+    _check(lib().lt_adamw_fp32_step(
+        _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(exp_avg), _ptr_array(exp_avg_sq),
+        _numel_array(params), k, float(lr), float(beta1), float(beta2), float(eps),
+        float(weight_decay), int(step), _scalar(coef, device, torch.float32, "coef"),
+        _scalar(status, device, torch.int32, "status"), ws.data_ptr(),
+        ws.numel() * ws.element_size(), _stream_handle(stream, device)))
+
+
+def lt_select_8bit_slice(numels: Sequence[int], fraction: float):
+    """Returns (list of bools: tensor takes 8-bit states, parameters chosen)."""
+    n = (ctypes.c_int64 * len(numels))(*numels)
+    out = (ctypes.c_uint8 * len(numels))()
+    chosen = ctypes.c_int64()
+    _check(lib().lt_select_8bit_slice(n, len(numels), float(fraction), out, ctypes.byref(chosen)))
+    return [bool(x) for x in out], chosen.value
+
+
 def lt_read_status(status: torch.Tensor, stream=None) -> int:
     """Reads the device status word (synchronizes the stream)."""
     out = ctypes.c_int32()
@@ -297,25 +347,39 @@ def lt_set_max_workgroups(max_workgroups: int) -> None:
 # ------------------------------------------------------------- optimizer object
 
 class Hybrid8bitAdamW:
-    """Holds the 8-bit states of a list of fp32 master tensors and runs one clipped
-    step per call: lt_grad_sqnorm -> lt_clip_coef -> lt_hybrid8bit_adamw_step, all
-    enqueued on one stream without a host synchronization.  The caller owns the
-    skip/abort policy: ``last_status()`` reads the status word of the last step."""
+    """Runs one clipped step per call over a list of fp32 master tensors:
+    lt_grad_sqnorm -> lt_clip_coef -> the fused steps, all enqueued on one stream
+    without a host synchronization.  With ``slice_fraction`` None every tensor keeps
+    8-bit states; otherwise lt_select_8bit_slice picks the tensors that do (the
+    paper's 2% slice) and the others keep fp32 states (lt_adamw_fp32_step), all under
+    one global norm.  The caller owns the skip/abort policy: ``last_status()`` reads
+    the status word of the last step."""
 
     def __init__(self, params: Sequence[torch.Tensor], lr: float = 1e-5,
                  betas=(0.9, 0.999), eps: float = 1e-8, weight_decay: float = 0.01,
-                 max_norm: float = 1.0, block_size: int = 4096):
+                 max_norm: float = 1.0, block_size: int = 4096,
+                 slice_fraction: Optional[float] = None):
         self.params = list(params)
         if not self.params:
             raise ValueError("no parameters")
         dev = self.params[0].device
         self.lr, self.betas, self.eps, self.weight_decay = lr, betas, eps, weight_decay
         self.max_norm, self.block_size = max_norm, block_size
-        self.m_codes = [torch.zeros(p.numel(), dtype=torch.int8, device=dev) for p in self.params]
-        self.v_codes = [torch.zeros(p.numel(), dtype=torch.uint8, device=dev) for p in self.params]
-        nb = [-(-p.numel() // block_size) for p in self.params]
+        if slice_fraction is None:
+            self.is_8bit = [True] * len(self.params)
+        else:
+            self.is_8bit, _ = lt_select_8bit_slice([p.numel() for p in self.params],
+                                                   slice_fraction)
+        self.idx8 = [i for i, b in enumerate(self.is_8bit) if b]
+        self.idx32 = [i for i, b in enumerate(self.is_8bit) if not b]
+        p8 = [self.params[i] for i in self.idx8]
+        self.m_codes = [torch.zeros(p.numel(), dtype=torch.int8, device=dev) for p in p8]
+        self.v_codes = [torch.zeros(p.numel(), dtype=torch.uint8, device=dev) for p in p8]
+        nb = [-(-p.numel() // block_size) for p in p8]
         self.m_absmax = [torch.zeros(n, dtype=torch.float32, device=dev) for n in nb]
         self.v_absmax = [torch.zeros(n, dtype=torch.float32, device=dev) for n in nb]
+        self.exp_avg = [torch.zeros_like(self.params[i]).reshape(-1) for i in self.idx32]
+        self.exp_avg_sq = [torch.zeros_like(self.params[i]).reshape(-1) for i in self.idx32]
         self.sq_total = torch.zeros(1, dtype=torch.float64, device=dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
         self.coef = torch.ones(1, dtype=torch.float32, device=dev)
@@ -330,10 +394,17 @@ class Hybrid8bitAdamW:
         lt_grad_sqnorm(grads, self.sq_total, self.status, stream=stream)
         clip = self.max_norm if self.max_norm is not None else math.inf
         lt_clip_coef(self.sq_total, clip, self.coef, self.total_norm, stream=stream)
-        lt_hybrid8bit_adamw_step(self.params, grads, self.m_codes, self.m_absmax, self.v_codes,
-                                 self.v_absmax, self.block_size, self.lr, self.betas[0],
-                                 self.betas[1], self.eps, self.weight_decay, t, coef=self.coef,
-                                 status=self.status, stream=stream)
+        hyper = dict(lr=self.lr, beta1=self.betas[0], beta2=self.betas[1], eps=self.eps,
+                     weight_decay=self.weight_decay, step=t, coef=self.coef, status=self.status,
+                     stream=stream)
+        if self.idx8:
+            lt_hybrid8bit_adamw_step([self.params[i] for i in self.idx8],
+                                     [grads[i] for i in self.idx8], self.m_codes, self.m_absmax,
+                                     self.v_codes, self.v_absmax, self.block_size, **hyper)
+        if self.idx32:
+            lt_adamw_fp32_step([self.params[i] for i in self.idx32],
+                               [grads[i] for i in self.idx32], self.exp_avg, self.exp_avg_sq,
+                               **hyper)
         self.step_count = t
         self._unchecked = True
 

@@ -1,0 +1,77 @@
+"""fp32-state AdamW (the non-8-bit part of the hybrid operator) and the hybrid
+optimizer (an 8-bit slice plus fp32 states under one global norm) against the
+oracle, bitwise."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_11919_amd as lt
+from golden_io import f32_to_bf16_bits
+from gpu_helpers import DEV, HYPER, State, assert_state_equal, gpu_norm_and_coef, oracle_step, \
+    to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+SIZES = [1, 7, 8, 1023, 1024, 1025, 5000, 65537, 300001]
+
+
+@pytest.mark.parametrize("as_bf16", [False, True])
+def test_fp32_state_step_matches_oracle(as_bf16):
+    rng = np.random.default_rng(40 + as_bf16)
+    w = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in SIZES]
+    m = [(rng.standard_normal(n) * 1e-3).astype(np.float32) for n in SIZES]
+    v = [(rng.random(n) * 1e-6).astype(np.float32) for n in SIZES]
+    g32 = [(rng.standard_t(3, size=n) * 1e-3).astype(np.float32) for n in SIZES]
+    g = [f32_to_bf16_bits(x) for x in g32] if as_bf16 else g32
+    dw, dm, dv = [to_dev(x) for x in w], [to_dev(x) for x in m], [to_dev(x) for x in v]
+    gdev = [to_dev(x) for x in g]
+    _, S, status, _, coef = gpu_norm_and_coef(gdev, 1.0)
+    lt.lt_adamw_fp32_step(dw, gdev, dm, dv, step=3, coef=coef, status=status, **HYPER)
+    _, rS, rst = oracle.grad_sqnorm(g)
+    _, rc = oracle.clip_coef(rS, 1.0)
+    for k in range(len(SIZES)):
+        oracle.adamw_fp32_step(w[k], g[k], m[k], v[k], step=3, coef=float(rc), **HYPER)
+        assert to_host(dw[k]).tobytes() == w[k].tobytes(), k
+        assert to_host(dm[k]).tobytes() == m[k].tobytes(), k
+        assert to_host(dv[k]).tobytes() == v[k].tobytes(), k
+
+
+def test_fp32_state_step_skips_on_nonfinite():
+    x = torch.ones(5000, device=DEV)
+    m = torch.zeros(5000, device=DEV)
+    v = torch.zeros(5000, device=DEV)
+    g = torch.full((5000,), float("inf"), device=DEV)
+    _, S, status, _, coef = gpu_norm_and_coef([g], 1.0)
+    lt.lt_adamw_fp32_step([x], [g], [m], [v], step=1, coef=coef, status=status, **HYPER)
+    assert lt.lt_read_status(status) == lt.LT_STATUS_NONFINITE
+    assert bool(torch.all(x == 1)) and not bool(m.any()) and not bool(v.any())
+
+
+def test_hybrid_optimizer_matches_oracle():
+    rng = np.random.default_rng(44)
+    sizes = [40000, 300001, 5000, 123457, 2048, 7]
+    w0 = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
+    params = [to_dev(x) for x in w0]
+    opt = lt.Hybrid8bitAdamW(params, lr=1e-4, block_size=2048, slice_fraction=0.3)
+    assert opt.idx8 and opt.idx32
+    ref8 = State.zero_host([w0[i] for i in opt.idx8], 2048)
+    ref32 = [(w0[i].copy(), np.zeros_like(w0[i]), np.zeros_like(w0[i])) for i in opt.idx32]
+    for t in (1, 2, 3):
+        g = [f32_to_bf16_bits((rng.standard_t(3, size=n) * 1e-2).astype(np.float32))
+             for n in sizes]
+        opt.step([to_dev(x) for x in g])
+        assert opt.last_status() == lt.LT_STATUS_OK
+        _, S, st = oracle.grad_sqnorm(g)
+        _, c = oracle.clip_coef(S, 1.0)
+        oracle_step(ref8, [g[i] for i in opt.idx8], 2048, t, coef=float(c), status=st, lr=1e-4)
+        for (wr, mr, vr), i in zip(ref32, opt.idx32):
+            oracle.adamw_fp32_step(wr, g[i], mr, vr, step=t, coef=float(c),
+                                   **dict(HYPER, lr=1e-4))
+    got8 = State([to_host(params[i]) for i in opt.idx8], [to_host(x) for x in opt.m_codes],
+                  [to_host(x) for x in opt.m_absmax], [to_host(x) for x in opt.v_codes],
+                  [to_host(x) for x in opt.v_absmax])
+    assert_state_equal(got8, ref8, "8-bit slice")
+    for (wr, mr, vr), i, m, v in zip(ref32, opt.idx32, opt.exp_avg, opt.exp_avg_sq):
+        assert to_host(params[i]).tobytes() == wr.tobytes()
+        assert to_host(m).tobytes() == mr.tobytes() and to_host(v).tobytes() == vr.tobytes()

@@ -329,3 +329,31 @@ def test_three_step_drift_against_unquantized_fp64_adamw():
         print(f"step {t}: drift/lr max {drift.max():.3g}, outside hazard max "
               f"{drift[~hazard].max():.3g}, hazard fraction {hazard.mean():.3f}")
         assert drift[~hazard].max() < 2.0
+
+
+@pytest.mark.parametrize("case", CASES[:4])
+def test_fp32_state_adamw_matches_torch(case):
+    """The fp32-state step (the non-8-bit part of the hybrid operator) against
+    torch.optim.AdamW with the same fp32 states, to the rounding-error bound."""
+    t, lr, b1, b2, eps, wd, coef, gs = case
+    rng = np.random.default_rng(abs(hash(case)) % (2 ** 32) + 1)
+    n = 5000
+    g = (rng.standard_t(3, size=n) * gs).astype(np.float32)
+    m0 = (rng.standard_normal(n) * gs).astype(np.float32)
+    v0 = (rng.random(n) * gs * gs).astype(np.float32)
+    if t == 1:
+        m0[:] = 0
+        v0[:] = 0
+    w = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    wo, mo, vo = w.copy(), m0.copy(), v0.copy()
+    oracle.adamw_fp32_step(wo, g, mo, vo, lr=lr, beta1=b1, beta2=b2, eps=eps, weight_decay=wd,
+                           step=t, coef=coef)
+    gc = (g * np.float32(coef)).astype(np.float32)
+    wt, mt, vt = _torch_adamw(w, gc, m0, v0, t, lr, b1, b2, eps, wd)
+    assert np.all(np.abs(mo - mt) <= 4e-7 * (b1 * np.abs(m0) + (1 - b1) * np.abs(gc)) + 1e-38)
+    assert np.all(np.abs(vo - vt) <= 4e-7 * np.abs(vt) + 1e-38)
+    step_size = lr / (1 - b1 ** t)
+    denom = np.sqrt(vt.astype(np.float64)) / np.sqrt(1 - b2 ** t) + eps
+    terms = step_size * (b1 * np.abs(m0.astype(np.float64)) + (1 - b1) * np.abs(gc)) / denom
+    d = np.abs(wo.astype(np.float64) - wt)
+    assert np.all(d <= 5e-7 * (terms + np.abs(w) + np.abs(wt)) + 1e-37)
