@@ -69,6 +69,8 @@ def _load():
                                         ctypes.c_int64] + [ctypes.c_double] * 5 + [
                                             ctypes.c_int64, ctypes.c_float]
     lib.lto_adamw_fp32_step.restype = None
+    lib.lto_round_bf16.argtypes = [fp, ctypes.c_int64, ctypes.POINTER(ctypes.c_uint16)]
+    lib.lto_round_bf16.restype = None
     _lib = lib
     return lib
 
@@ -202,3 +204,12 @@ def adamw_fp32_step(w, grad, m, v, lr, beta1, beta2, eps, weight_decay, step, co
     _contig([w, m, v], np.float32)
     _load().lto_adamw_fp32_step(_fp(w), grad.ctypes.data, _gdt(grad), _fp(m), _fp(v), w.size,
                                 lr, beta1, beta2, eps, weight_decay, step, coef)
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) of float32 values: round to nearest even on the
+    dropped bits, NaN to a quiet NaN of the same sign."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.empty(x.shape, dtype=np.uint16)
+    _load().lto_round_bf16(_fp(x), x.size, y.ctypes.data_as(ctypes.POINTER(ctypes.c_uint16)))
+    return y

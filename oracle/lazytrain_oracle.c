@@ -287,3 +287,21 @@ void lto_adamw_fp32_step(float* w, const void* grad, int gdt, float* m, float* v
     for (int64_t i = 0; i < n; ++i)
         adamw_element(&s, m[i], v[i], grad_value(grad, gdt, i), w[i], &m[i], &v[i], &w[i]);
 }
+
+void lto_round_bf16(const float* x, int64_t n, uint16_t* y)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t u;
+        memcpy(&u, &x[i], 4);
+        uint32_t hi = u >> 16, lo = u & 0xFFFFu;
+        if (isnan(x[i])) {
+            y[i] = (uint16_t)(hi | 0x0040u);  /* quiet, sign kept */
+            continue;
+        }
+        /* above the midpoint, or on it with an odd kept part: round up (the
+         * carry may run into the exponent, up to infinity) */
+        if (lo > 0x8000u || (lo == 0x8000u && (hi & 1u)))
+            hi += 1;
+        y[i] = (uint16_t)hi;
+    }
+}

@@ -120,6 +120,13 @@ void lto_adamw_fp32_step(float* w, const void* grad, int gdt, float* m, float* v
                          double lr, double beta1, double beta2, double eps, double weight_decay,
                          int64_t step, float coef);
 
+/* bf16 copy of fp32 values, as the step's optional low-precision weight copy
+ * (the parameters the layer-streaming executor moves to the GPU for the next
+ * forward pass: Sec. 3.1, and the parameter H2D traffic of Sec. 3.4).  Round to nearest, ties to even, on the 16 dropped bits of the
+ * fp32 pattern (an overflow rounds to infinity, subnormals round like any other
+ * value); a NaN gives a quiet NaN of the same sign. */
+void lto_round_bf16(const float* x, int64_t n, uint16_t* y);
+
 #ifdef __cplusplus
 }
 #endif
