@@ -262,6 +262,9 @@ def run_streamed(args, w, dev, n_threads) -> int:
             host["vq"].append(torch.zeros(n, dtype=torch.uint8, pin_memory=True))
             host["ma"].append(torch.zeros(nb, dtype=torch.float32, pin_memory=True))
             host["va"].append(torch.zeros(nb, dtype=torch.float32, pin_memory=True))
+            if args.bf16_copy:
+                host.setdefault("wb", []).append(torch.empty(n, dtype=torch.bfloat16,
+                                                             pin_memory=True))
         log(f"host layer {r + 1}/{R} ready ({time.time() - t0:.1f} s)")
     lists = {name: [v[(l % R) * per_layer + j] for l in range(L) for j in range(per_layer)]
              for name, v in host.items()}
@@ -272,7 +275,8 @@ def run_streamed(args, w, dev, n_threads) -> int:
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     cs, hs, ds = torch.cuda.Stream(dev), torch.cuda.Stream(dev), torch.cuda.Stream(dev)
     slots = args.ring_slots
-    nbytes = lt.lt_streamed_workspace_bytes(w.numels, first, lt.LT_DTYPE_BF16, B, slots)
+    nbytes = lt.lt_streamed_workspace_bytes(w.numels, first, lt.LT_DTYPE_BF16, B, slots,
+                                            args.bf16_copy)
     workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
 
@@ -281,7 +285,7 @@ def run_streamed(args, w, dev, n_threads) -> int:
             lists["w"], lists["g"], lists["mq"], lists["ma"], lists["vq"], lists["va"], first, B,
             step=t, max_norm=w.max_norm, ring_slots=slots, sq_total=S, coef=coef, status=status,
             total_norm=norm, workspace=workspace, compute_stream=cs, h2d_stream=hs,
-            d2h_stream=ds, **hyper)
+            d2h_stream=ds, params_bf16=lists.get("wb"), **hyper)
 
     t = 1
     for _ in range(args.warmup):
@@ -302,14 +306,15 @@ def run_streamed(args, w, dev, n_threads) -> int:
     n = w.n_params
     nb = sum(-(-x // B) for x in w.numels)
     h2d = n * 2 + n * 8 + nb * 8  # pass 1 gradients; pass 2 weights, gradients, codes, scales
-    d2h = n * 6 + nb * 8          # weights, codes, scales back
+    d2h = n * (8 if args.bf16_copy else 6) + nb * 8  # weights, codes, scales (bf16 copy) back
     bound = max(h2d / (rates["h2d_gbps"] * 1e9), d2h / (rates["d2h_gbps"] * 1e9))
     out = {
         "metric": METRIC, "value": n / per, "unit": "params/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(per * 1e3, 2),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "params": n, "tensors": len(w.shapes), "layers": L,
+        "config": {"workload": w.name + ("+bf16-copy" if args.bf16_copy else ""), "params": n,
+                   "tensors": len(w.shapes), "layers": L,
                    "block_size": B, "grad_dtype": "bf16", "ring_slots": slots,
                    "host_layers": R, "host_state": "pinned, cycled over host_layers"},
         "pcie": {"h2d_bytes_per_step": h2d, "d2h_bytes_per_step": d2h, **rates,
@@ -346,6 +351,8 @@ def main() -> int:
     ap.add_argument("--slice-fraction", type=float, default=None,
                     help="hybrid operator: only this fraction of parameters keeps 8-bit states, "
                          "the rest fp32 states (the paper's run uses 0.02)")
+    ap.add_argument("--bf16-copy", action="store_true",
+                    help="the steps also write a bf16 copy of the updated weights (+2 B/param)")
     ap.add_argument("--host-layers", type=int, default=8,
                     help="streamed workload: distinct pinned host layers the model cycles over")
     ap.add_argument("--ring-slots", type=int, default=3, help="streamed workload: device slots")
@@ -404,6 +411,10 @@ def main() -> int:
     p8, g8 = [params[k] for k in idx8], [grads[k] for k in idx8]
     s8 = [[x[k] for k in idx8] for x in (mq, ma, vq, va)]
     p32, g32 = [params[k] for k in idx32], [grads[k] for k in idx32]
+    wb8 = wb32 = None
+    if args.bf16_copy:
+        wb = [torch.empty(n, dtype=torch.bfloat16, device=dev) for n in w.numels]
+        wb8, wb32 = [wb[k] for k in idx8], [wb[k] for k in idx32]
 
     def one_step(t, ev=None):
         if ev:
@@ -414,10 +425,12 @@ def main() -> int:
             ev[1].record(stream)
         if p8:
             lt.lt_hybrid8bit_adamw_step(p8, g8, *s8, B, step=t, coef=coef, status=status,
-                                        workspace=ws_step, stream=stream, **hyper)
+                                        workspace=ws_step, stream=stream, params_bf16=wb8,
+                                        **hyper)
         if p32:
             lt.lt_adamw_fp32_step(p32, g32, exp_avg, exp_avg_sq, step=t, coef=coef,
-                                  status=status, workspace=ws_32, stream=stream, **hyper)
+                                  status=status, workspace=ws_32, stream=stream,
+                                  params_bf16=wb32, **hyper)
         if ev:
             ev[2].record(stream)
 
@@ -448,6 +461,8 @@ def main() -> int:
     gb = grad_bytes(w.grad_dtype)
     kbytes = step_kernel_bytes([w.numels[k] for k in idx8], B, gb) + \
         sum(w.numels[k] for k in idx32) * (gb + 24)  # fp32 states: w, m, v read and written
+    if args.bf16_copy:
+        kbytes += 2 * w.n_params  # the bf16 weight copy written
     nbytes = norm_bytes(w.numels, gb)
     ms_per_step = elapsed / args.steps * 1e3
     step_total_bytes = kbytes + nbytes
@@ -471,7 +486,8 @@ def main() -> int:
         "data": "synthetic",
         "step_ms_events": {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9)},
         "config": {"workload": w.name + ("" if not idx32 else
-                                         f"-hybrid-{args.slice_fraction:g}-8bit"),
+                                         f"-hybrid-{args.slice_fraction:g}-8bit") +
+                   ("+bf16-copy" if args.bf16_copy else ""),
                    "params": w.n_params, "tensors": K, "block_size": B,
                    "params_8bit": sum(w.numels[k] for k in idx8),
                    "grad_dtype": "bf16" if w.grad_dtype == synth.BF16 else "f32",
@@ -488,7 +504,8 @@ def main() -> int:
                      "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                     "traffic": counter_traffic(w.name) if not idx32 else None,
+                     "traffic": counter_traffic(w.name)
+                     if not idx32 and not args.bf16_copy else None,
                      "bytes_per_launch": kbytes},
         "status": st,
     }

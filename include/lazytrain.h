@@ -130,12 +130,21 @@ size_t lt_step_workspace_bytes(int n_tensors);
  *   status   device int32 or NULL (never skip).  When it holds
  *            LT_STATUS_NONFINITE the kernel writes nothing: weights, codes and
  *            absmax stay bitwise unchanged.
+ *   params_bf16  NULL, or a host list of device uint16[n] arrays (entries may
+ *            be NULL: no copy of that tensor), 16-byte aligned: a bf16 copy of
+ *            the weights for the next forward pass of a layer-streaming
+ *            executor, which moves parameters to the GPU for every layer
+ *            (Sec. 3.1; parameter H2D traffic in Sec. 3.4).  After the call it
+ *            holds bf16(w1), rounded to nearest even (a NaN becomes a quiet
+ *            NaN of the same sign), written by the step kernel from registers
+ *            (+2 B/param); after a skipped step, bf16 of the unchanged weights.
  * The tensors of one call must not overlap.
  */
 lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int grad_dtype,
                                 int8_t* const* m_codes, float* const* m_absmax,
                                 uint8_t* const* v_codes, float* const* v_absmax,
-                                const int64_t* numels, int n_tensors, int block_size, double lr,
+                                uint16_t* const* params_bf16, const int64_t* numels,
+                                int n_tensors, int block_size, double lr,
                                 double beta1, double beta2, double eps, double weight_decay,
                                 int64_t step, const float* coef, const int32_t* status,
                                 void* workspace, size_t workspace_bytes, void* stream);
@@ -143,9 +152,12 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
 /* Bytes of device workspace lt_streamed_hybrid8bit_adamw_step needs: the
  * descriptors of every layer, one fp64 partial per 8192-element chunk of the
  * whole model, and ring_slots slots each large enough for the largest layer's
- * weights, gradients, codes and scales.  0 if an argument is invalid. */
+ * weights, gradients, codes and scales (and its bf16 weight copy when
+ * bf16_copy is nonzero: the call passes a params_bf16 list).  0 if an argument
+ * is invalid. */
 size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const int* layer_first,
-                                   int n_layers, int grad_dtype, int block_size, int ring_slots);
+                                   int n_layers, int grad_dtype, int block_size, int ring_slots,
+                                   int bf16_copy);
 
 /*
  * Step a11: one clipped Hybrid 8-bit AdamW step over a model whose fp32
@@ -157,7 +169,11 @@ size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const i
  * sum of squares over the whole model, so every result is bitwise that of the
  * resident path on the same data.
  *   params .. v_absmax  HOST pointers, one entry per tensor, layouts as in
- *                       lt_hybrid8bit_adamw_step.  Pinned memory (hipHostMalloc)
+ *                       lt_hybrid8bit_adamw_step.
+ *   params_bf16         NULL or a HOST list of host uint16[n] arrays (entries
+ *                       may be NULL) receiving the bf16 weight copy as in
+ *                       lt_hybrid8bit_adamw_step (+2 B/param copied out); the
+ *                       workspace must then be sized with bf16_copy = 1.  Pinned memory (hipHostMalloc)
  *                       lets copies overlap compute; pageable memory works but
  *                       serializes the copies.  Read and written asynchronously:
  *                       the caller must not touch them until compute_stream has
@@ -184,8 +200,9 @@ size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const i
 lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const* grads,
                                          int grad_dtype, int8_t* const* m_codes,
                                          float* const* m_absmax, uint8_t* const* v_codes,
-                                         float* const* v_absmax, const int64_t* numels,
-                                         int n_tensors, const int* layer_first, int n_layers,
+                                         float* const* v_absmax, uint16_t* const* params_bf16,
+                                         const int64_t* numels, int n_tensors,
+                                         const int* layer_first, int n_layers,
                                          int block_size, double lr, double beta1, double beta2,
                                          double eps, double weight_decay, int64_t step,
                                          float max_norm, int ring_slots, void* workspace,
@@ -203,12 +220,13 @@ size_t lt_adamw_fp32_workspace_bytes(int n_tensors);
  * variant table).  exp_avg[k], exp_avg_sq[k] are device float[numels[k]], read
  * and written.  Per element, the same fp32 operations as
  * lt_hybrid8bit_adamw_step with m0, v0 taken from and m1, v1 stored to these
- * arrays.  coef and status as there (NULL: no clipping / never skip).
- * Pointers 16-byte aligned; workspace 256-byte aligned.
+ * arrays.  coef, status and params_bf16 (NULL or a list of device bf16 copies,
+ * entries may be NULL) as there.  Pointers 16-byte aligned; workspace
+ * 256-byte aligned.
  */
 lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int grad_dtype,
-                          float* const* exp_avg, float* const* exp_avg_sq, const int64_t* numels,
-                          int n_tensors, double lr, double beta1, double beta2, double eps,
+                          float* const* exp_avg, float* const* exp_avg_sq,
+                          uint16_t* const* params_bf16, const int64_t* numels, int n_tensors, double lr, double beta1, double beta2, double eps,
                           double weight_decay, int64_t step, const float* coef,
                           const int32_t* status, void* workspace, size_t workspace_bytes,
                           void* stream);

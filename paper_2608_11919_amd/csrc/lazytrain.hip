@@ -60,7 +60,7 @@ struct StepTensor {
     uint8_t* vq;
     float* va;
     int64_t numel;
-    int64_t pad_;
+    uint16_t* wb;  // bf16 copy of the updated weights, or null
 };
 static_assert(sizeof(StepTensor) == 64, "descriptor is one 64-byte line");
 
@@ -219,6 +219,18 @@ lt_err grid_size(Kernel kernel, int64_t units, int* grid)
 }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// True when a nullable list of n pointers holds a non-null entry.
+template <typename T>
+bool any_set(T* const* list, int n)
+{
+    if (!list)
+        return false;
+    for (int k = 0; k < n; ++k)
+        if (list[k])
+            return true;
+    return false;
+}
 
 // ============================================================== device code
 
@@ -676,6 +688,29 @@ __device__ inline void load_step_ragged(const StepTensor& d, int64_t ei, int nv,
                       vb[4] | (vb[5] << 8) | (vb[6] << 16) | (vb[7] << 24));
 }
 
+// bf16 copy of eight updated weights (nv of them exist): round to nearest even,
+// by the hardware's packed conversion.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ inline uint32_t bf16_pair(float lo, float hi)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
+
+__device__ inline void store_bf16x8(uint16_t* p, int nv, const float (&w)[8])
+{
+    const uint4 q = make_uint4(bf16_pair(w[0], w[1]), bf16_pair(w[2], w[3]),
+                               bf16_pair(w[4], w[5]), bf16_pair(w[6], w[7]));
+    if (nv >= kGranule) {
+        *reinterpret_cast<uint4*>(p) = q;
+        return;
+    }
+    const uint32_t word[4] = {q.x, q.y, q.z, q.w};
+    for (int e = 0; e < nv; ++e)
+        p[e] = uint16_t(word[e >> 1] >> (16 * (e & 1)));
+}
+
 // Packs four codes held as exact small integers (as floats) into one word.
 // q must lie in [0, 255] (m codes arrive offset by +128).
 __device__ inline uint32_t pack4(float q0, float q1, float q2, float q3)
@@ -686,7 +721,9 @@ __device__ inline uint32_t pack4(float q0, float q1, float q2, float q3)
     return __builtin_amdgcn_cvt_pk_u8_f32(q3, 3, w);
 }
 
-template <typename GT, int B>
+// WB: some tensor of the launch asks for the bf16 weight copy (a separate
+// instantiation keeps the copy's code out of the launches that do not).
+template <typename GT, int B, bool WB>
 __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restrict__ unit_prefix,
                                                           const StepTensor* __restrict__ desc,
                                                           int n_tensors, int64_t n_units,
@@ -812,6 +849,12 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                     for (int e = 0; e < nv; ++e)
                         d.w[ei + e] = w[e];
                 }
+                if (WB && d.wb) {
+                    const int nv = full ? kGranule
+                                        : int(i64min(i64max(n_span - kGranule * (lane + 64 * j), 0),
+                                                     kGranule));
+                    store_bf16x8(d.wb + ei, nv, w);
+                }
             }
         }
 
@@ -893,7 +936,8 @@ struct Fp32Tensor {
     float* m;
     float* v;
     int64_t numel;
-    int64_t pad_[3];
+    uint16_t* wb;  // bf16 copy of the updated weights, or null
+    int64_t pad_[2];
 };
 static_assert(sizeof(Fp32Tensor) == 64, "descriptor is one 64-byte line");
 
@@ -925,7 +969,7 @@ __device__ inline void store8f(float* p, int nv, const float (&x)[8])
         p[e] = x[e];
 }
 
-template <typename GT>
+template <typename GT, bool WB>
 __global__ __launch_bounds__(kThreads) void k_adamw32_step(const int64_t* __restrict__ unit_prefix,
                                                            const Fp32Tensor* __restrict__ desc,
                                                            int n_tensors, int64_t n_units,
@@ -1003,41 +1047,89 @@ __global__ __launch_bounds__(kThreads) void k_adamw32_step(const int64_t* __rest
             store8f(d.w + ei, nv[j], ww);
             store8f(d.m + ei, nv[j], mm);
             store8f(d.v + ei, nv[j], vv);
+            if (WB && d.wb)
+                store_bf16x8(d.wb + ei, nv[j], ww);
         }
     }
+}
+
+// -------------------------------------- f3: bf16 copy after a skipped step
+//
+// A skipped step (non-finite gradient) leaves the weights unchanged; tensors
+// with a bf16 copy get it refreshed from them, so that after every call the
+// copy is bf16(weights).  The kernel exits at once when the step was not
+// skipped.  Units and their prefix are those of the step launch it follows.
+template <typename Desc>
+__global__ __launch_bounds__(kThreads) void k_bf16_on_skip(const int64_t* __restrict__ unit_prefix,
+                                                           const Desc* __restrict__ desc,
+                                                           int n_tensors, int64_t n_units,
+                                                           int64_t unit_elems,
+                                                           const int32_t* __restrict__ status_ptr)
+{
+    if (*status_ptr != LT_STATUS_NONFINITE)
+        return;
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = int64_t(gridDim.x) * 4;
+    for (int64_t u = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6); u < n_units; u += waves) {
+        const int k = find_tensor(unit_prefix, n_tensors, u);
+        const Desc d = desc[k];
+        if (!d.wb)
+            continue;
+        const int64_t e0 = (u - unit_prefix[k]) * unit_elems;
+        const int64_t e1 = i64min(e0 + unit_elems, d.numel);
+        for (int64_t ei = e0 + kGranule * lane; ei < e1; ei += 64 * kGranule) {
+            const int nv = int(i64min(e1 - ei, kGranule));
+            float w[8];
+            load8f(d.w + ei, nv, w);
+            store_bf16x8(d.wb + ei, nv, w);
+        }
+    }
+}
+
+template <typename Desc>
+lt_err launch_bf16_on_skip(const int64_t* unit_prefix, const Desc* desc, int n_tensors,
+                           int64_t n_units, int64_t unit_elems, const int32_t* status,
+                           hipStream_t st)
+{
+    const int grid = int(std::min<int64_t>((n_units + 3) / 4, 1024));
+    k_bf16_on_skip<Desc><<<grid, kThreads, 0, st>>>(unit_prefix, desc, n_tensors, n_units,
+                                                    unit_elems, status);
+    LT_HIP(hipGetLastError());
+    return LT_OK;
 }
 
 // ================================================================ host side
 
 template <typename GT, int B>
 lt_err launch_step_b(const int64_t* prefix, const StepTensor* desc, int K, int64_t units,
-                     const StepScalars& s, const float* coef, const int32_t* status,
+                     const StepScalars& s, const float* coef, const int32_t* status, bool wb,
                      hipStream_t stream)
 {
     // One workgroup takes four units at a time when each wave works alone.
     const int64_t wg_units = StepGeom<B>::W > 1 ? units : (units + 3) / 4;
+    auto* kernel = wb ? k_adamw8_step<GT, B, true> : k_adamw8_step<GT, B, false>;
     int grid;
-    if (lt_err e = grid_size(k_adamw8_step<GT, B>, wg_units, &grid))
+    if (lt_err e = grid_size(kernel, wg_units, &grid))
         return e;
-    k_adamw8_step<GT, B><<<grid, kThreads, 0, stream>>>(prefix, desc, K, units, s, coef, status);
+    kernel<<<grid, kThreads, 0, stream>>>(prefix, desc, K, units, s, coef, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
 }
 
 template <typename GT>
 lt_err launch_step(int B, const int64_t* prefix, const StepTensor* desc, int K, int64_t tiles,
-                   const StepScalars& s, const float* coef, const int32_t* status,
+                   const StepScalars& s, const float* coef, const int32_t* status, bool wb,
                    hipStream_t stream)
 {
     switch (B) {
-    case 64: return launch_step_b<GT, 64>(prefix, desc, K, tiles, s, coef, status, stream);
-    case 128: return launch_step_b<GT, 128>(prefix, desc, K, tiles, s, coef, status, stream);
-    case 256: return launch_step_b<GT, 256>(prefix, desc, K, tiles, s, coef, status, stream);
-    case 512: return launch_step_b<GT, 512>(prefix, desc, K, tiles, s, coef, status, stream);
-    case 1024: return launch_step_b<GT, 1024>(prefix, desc, K, tiles, s, coef, status, stream);
-    case 2048: return launch_step_b<GT, 2048>(prefix, desc, K, tiles, s, coef, status, stream);
-    case 4096: return launch_step_b<GT, 4096>(prefix, desc, K, tiles, s, coef, status, stream);
-    case 8192: return launch_step_b<GT, 8192>(prefix, desc, K, tiles, s, coef, status, stream);
+    case 64: return launch_step_b<GT, 64>(prefix, desc, K, tiles, s, coef, status, wb, stream);
+    case 128: return launch_step_b<GT, 128>(prefix, desc, K, tiles, s, coef, status, wb, stream);
+    case 256: return launch_step_b<GT, 256>(prefix, desc, K, tiles, s, coef, status, wb, stream);
+    case 512: return launch_step_b<GT, 512>(prefix, desc, K, tiles, s, coef, status, wb, stream);
+    case 1024: return launch_step_b<GT, 1024>(prefix, desc, K, tiles, s, coef, status, wb, stream);
+    case 2048: return launch_step_b<GT, 2048>(prefix, desc, K, tiles, s, coef, status, wb, stream);
+    case 4096: return launch_step_b<GT, 4096>(prefix, desc, K, tiles, s, coef, status, wb, stream);
+    case 8192: return launch_step_b<GT, 8192>(prefix, desc, K, tiles, s, coef, status, wb, stream);
     default: return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
     }
 }
@@ -1135,10 +1227,12 @@ size_t align256(size_t x) { return round_up(x, 256); }
 
 // Bytes of one tensor's arrays inside a slot: w, g, m codes, v codes, m and v absmax.
 struct SlotTensor {
-    size_t w, g, mq, vq, ma, va, end;
+    size_t w, g, mq, vq, ma, va, wb, end;
 };
 
-SlotTensor slot_tensor(size_t at, int64_t n, int gbytes, int B)
+// Offsets of one tensor's arrays inside a slot; the bf16 weight copy takes room
+// only when the call asks for it.
+SlotTensor slot_tensor(size_t at, int64_t n, int gbytes, int B, bool bf16_copy)
 {
     const int64_t nb = (n + B - 1) / B;
     SlotTensor t;
@@ -1148,7 +1242,8 @@ SlotTensor slot_tensor(size_t at, int64_t n, int gbytes, int B)
     t.vq = t.mq + align256(size_t(n));
     t.ma = t.vq + align256(size_t(n));
     t.va = t.ma + align256(size_t(nb) * 4);
-    t.end = t.va + align256(size_t(nb) * 4);
+    t.wb = t.va + align256(size_t(nb) * 4);
+    t.end = t.wb + (bf16_copy ? align256(size_t(n) * 2) : 0);
     return t;
 }
 
@@ -1161,7 +1256,7 @@ struct StreamLayout {
 };
 
 StreamLayout stream_layout(const int64_t* numels, int K, const int* first, int L, int gbytes, int B,
-                           int S)
+                           int S, bool bf16_copy)
 {
     StreamLayout l;
     size_t at = 0;
@@ -1189,7 +1284,7 @@ StreamLayout stream_layout(const int64_t* numels, int K, const int* first, int L
     for (int i = 0; i < L; ++i) {
         size_t b = 0;
         for (int k = first[i]; k < first[i + 1]; ++k)
-            b = slot_tensor(b, numels[k], gbytes, B).end;
+            b = slot_tensor(b, numels[k], gbytes, B, bf16_copy).end;
         biggest = std::max(biggest, b);
     }
     l.slot_bytes = biggest;
@@ -1299,7 +1394,8 @@ size_t lt_step_workspace_bytes(int n_tensors)
 lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int grad_dtype,
                                 int8_t* const* m_codes, float* const* m_absmax,
                                 uint8_t* const* v_codes, float* const* v_absmax,
-                                const int64_t* numels, int n_tensors, int block_size, double lr,
+                                uint16_t* const* params_bf16, const int64_t* numels,
+                                int n_tensors, int block_size, double lr,
                                 double beta1, double beta2, double eps, double weight_decay,
                                 int64_t step, const float* coef, const int32_t* status,
                                 void* workspace, size_t workspace_bytes, void* stream)
@@ -1327,6 +1423,8 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
             return fail(LT_ERR_ALIGNMENT, "params/grads/codes" + at + " must be 16-byte aligned");
         if (!aligned(m_absmax[k], 4) || !aligned(v_absmax[k], 4))
             return fail(LT_ERR_ALIGNMENT, "absmax" + at + " must be 4-byte aligned");
+        if (params_bf16 && !aligned(params_bf16[k], 16))
+            return fail(LT_ERR_ALIGNMENT, "params_bf16" + at + " must be 16-byte aligned");
     }
     const StepLayout lay = step_layout(K);
     if (!workspace || !aligned(workspace, 256) || workspace_bytes < lay.total)
@@ -1341,7 +1439,7 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
     for (int k = 0; k < K; ++k) {
         prefix[k + 1] = prefix[k] + (numels[k] + tile - 1) / tile;
         desc[k] = StepTensor{params[k], grads[k], m_codes[k], m_absmax[k], v_codes[k], v_absmax[k],
-                             numels[k], 0};
+                             numels[k], params_bf16 ? params_bf16[k] : nullptr};
     }
     const int64_t tiles = prefix[K];
 
@@ -1353,27 +1451,37 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
         return e;
     const auto* d_prefix = reinterpret_cast<const int64_t*>(ws + lay.prefix);
     const auto* d_desc = reinterpret_cast<const StepTensor*>(ws + lay.desc);
-    if (grad_dtype == LT_DTYPE_BF16)
-        return launch_step<uint16_t>(block_size, d_prefix, d_desc, K, tiles, s, coef, status, st);
-    return launch_step<float>(block_size, d_prefix, d_desc, K, tiles, s, coef, status, st);
+    const bool wb = any_set(params_bf16, K);
+    if (lt_err e = grad_dtype == LT_DTYPE_BF16
+                       ? launch_step<uint16_t>(block_size, d_prefix, d_desc, K, tiles, s, coef,
+                                               status, wb, st)
+                       : launch_step<float>(block_size, d_prefix, d_desc, K, tiles, s, coef,
+                                            status, wb, st))
+        return e;
+    if (status && wb)
+        return launch_bf16_on_skip(d_prefix, d_desc, K, tiles, tile, status, st);
+    return LT_OK;
 }
 
 size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const int* layer_first,
-                                   int n_layers, int grad_dtype, int block_size, int ring_slots)
+                                   int n_layers, int grad_dtype, int block_size, int ring_slots,
+                                   int bf16_copy)
 {
     if (!valid_list(numels, n_tensors) || !valid_layers(layer_first, n_layers, n_tensors) ||
         (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16) ||
         !valid_block_size(block_size) || ring_slots < 2 || ring_slots > kMaxSlots)
         return 0;
     return stream_layout(numels, n_tensors, layer_first, n_layers,
-                         grad_dtype == LT_DTYPE_BF16 ? 2 : 4, block_size, ring_slots)
+                         grad_dtype == LT_DTYPE_BF16 ? 2 : 4, block_size, ring_slots,
+                         bf16_copy != 0)
         .total;
 }
 
 lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const* grads,
                                          int grad_dtype, int8_t* const* m_codes,
                                          float* const* m_absmax, uint8_t* const* v_codes,
-                                         float* const* v_absmax, const int64_t* numels,
+                                         float* const* v_absmax, uint16_t* const* params_bf16,
+                                         const int64_t* numels,
                                          int n_tensors, const int* layer_first, int n_layers,
                                          int block_size, double lr, double beta1, double beta2,
                                          double eps, double weight_decay, int64_t step,
@@ -1408,7 +1516,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         if (!params[k] || !grads[k] || !m_codes[k] || !m_absmax[k] || !v_codes[k] || !v_absmax[k])
             return fail(LT_ERR_INVALID_ARG, "NULL host pointer at index " + std::to_string(k));
     const int gbytes = grad_dtype == LT_DTYPE_BF16 ? 2 : 4;
-    const StreamLayout lay = stream_layout(numels, K, layer_first, L, gbytes, B, S);
+    const bool bf16_copy = params_bf16 != nullptr;
+    const StreamLayout lay = stream_layout(numels, K, layer_first, L, gbytes, B, S, bf16_copy);
     if (!workspace || !aligned(workspace, 256) || workspace_bytes < lay.total)
         return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
                                           std::to_string(lay.total) + " bytes");
@@ -1435,7 +1544,7 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         sp[0] = 0;
         up[0] = 0;
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
-            const SlotTensor t = slot_tensor(at, numels[k], gbytes, B);
+            const SlotTensor t = slot_tensor(at, numels[k], gbytes, B, bf16_copy);
             places[i].push_back(t);
             at = t.end;
             sp[j + 1] = sp[j] + (numels[k] + kChunk - 1) / kChunk;
@@ -1446,7 +1555,10 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                reinterpret_cast<int8_t*>(base + t.mq),
                                reinterpret_cast<float*>(base + t.ma),
                                reinterpret_cast<uint8_t*>(base + t.vq),
-                               reinterpret_cast<float*>(base + t.va), numels[k], 0};
+                               reinterpret_cast<float*>(base + t.va), numels[k],
+                               bf16_copy && params_bf16[k]
+                                   ? reinterpret_cast<uint16_t*>(base + t.wb)
+                                   : nullptr};
         }
     }
 
@@ -1530,11 +1642,15 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         const auto* up = reinterpret_cast<const int64_t*>(ws + lay.st_prefix[i]);
         const auto* dp = reinterpret_cast<const StepTensor*>(ws + lay.st_desc[i]);
         const int64_t units = reinterpret_cast<int64_t*>(header.data() + lay.st_prefix[i])[Ki];
+        const bool wb = any_set(params_bf16 ? params_bf16 + layer_first[i] : nullptr, Ki);
         lt_err e = grad_dtype == LT_DTYPE_BF16
-                       ? launch_step<uint16_t>(B, up, dp, Ki, units, sc, coef, status, cs)
-                       : launch_step<float>(B, up, dp, Ki, units, sc, coef, status, cs);
+                       ? launch_step<uint16_t>(B, up, dp, Ki, units, sc, coef, status, wb, cs)
+                       : launch_step<float>(B, up, dp, Ki, units, sc, coef, status, wb, cs);
         if (e)
             return e;
+        if (wb)
+            if (lt_err e2 = launch_bf16_on_skip(up, dp, Ki, units, unit, status, cs))
+                return e2;
         LT_HIP(hipEventRecord(ev.computed[sl], cs));
         LT_HIP(hipStreamWaitEvent(ds, ev.computed[sl], 0));
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
@@ -1545,6 +1661,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
             LT_HIP(hipMemcpyAsync(v_codes[k], base + t.vq, n, D2H, ds));
             LT_HIP(hipMemcpyAsync(m_absmax[k], base + t.ma, nb * 4, D2H, ds));
             LT_HIP(hipMemcpyAsync(v_absmax[k], base + t.va, nb * 4, D2H, ds));
+            if (bf16_copy && params_bf16[k])
+                LT_HIP(hipMemcpyAsync(params_bf16[k], base + t.wb, n * 2, D2H, ds));
         }
         LT_HIP(hipEventRecord(ev.freed[sl], ds));
         used[sl] = true;
@@ -1562,8 +1680,8 @@ size_t lt_adamw_fp32_workspace_bytes(int n_tensors)
 }
 
 lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int grad_dtype,
-                          float* const* exp_avg, float* const* exp_avg_sq, const int64_t* numels,
-                          int n_tensors, double lr, double beta1, double beta2, double eps,
+                          float* const* exp_avg, float* const* exp_avg_sq,
+                          uint16_t* const* params_bf16, const int64_t* numels, int n_tensors, double lr, double beta1, double beta2, double eps,
                           double weight_decay, int64_t step, const float* coef,
                           const int32_t* status, void* workspace, size_t workspace_bytes,
                           void* stream)
@@ -1585,6 +1703,9 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
         if (!aligned(params[k], 16) || !aligned(grads[k], 16) || !aligned(exp_avg[k], 16) ||
             !aligned(exp_avg_sq[k], 16))
             return fail(LT_ERR_ALIGNMENT, "tensor " + std::to_string(k) + " is not 16-byte aligned");
+        if (params_bf16 && !aligned(params_bf16[k], 16))
+            return fail(LT_ERR_ALIGNMENT,
+                        "params_bf16[" + std::to_string(k) + "] must be 16-byte aligned");
     }
     const size_t desc_at = round_up(sizeof(int64_t) * (K + 1), 64);
     const size_t total = lt_adamw_fp32_workspace_bytes(K);
@@ -1598,7 +1719,10 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
     prefix[0] = 0;
     for (int k = 0; k < K; ++k) {
         prefix[k + 1] = prefix[k] + (numels[k] + span - 1) / span;
-        desc[k] = Fp32Tensor{params[k], grads[k], exp_avg[k], exp_avg_sq[k], numels[k], {0, 0, 0}};
+        desc[k] = Fp32Tensor{params[k],  grads[k],
+                             exp_avg[k], exp_avg_sq[k],
+                             numels[k],  params_bf16 ? params_bf16[k] : nullptr,
+                             {0, 0}};
     }
     const int64_t units = prefix[K];
     const StepScalars sc = make_scalars(lr, beta1, beta2, eps, weight_decay, step);
@@ -1608,19 +1732,17 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
         return e;
     const auto* d_prefix = reinterpret_cast<const int64_t*>(ws);
     const auto* d_desc = reinterpret_cast<const Fp32Tensor*>(ws + desc_at);
+    const bool wb = any_set(params_bf16, K);
+    auto* kernel = grad_dtype == LT_DTYPE_BF16
+                       ? (wb ? k_adamw32_step<uint16_t, true> : k_adamw32_step<uint16_t, false>)
+                       : (wb ? k_adamw32_step<float, true> : k_adamw32_step<float, false>);
     int grid;
-    if (grad_dtype == LT_DTYPE_BF16) {
-        if (lt_err e = grid_size(k_adamw32_step<uint16_t>, (units + 3) / 4, &grid))
-            return e;
-        k_adamw32_step<uint16_t><<<grid, kThreads, 0, st>>>(d_prefix, d_desc, K, units, sc, coef,
-                                                            status);
-    } else {
-        if (lt_err e = grid_size(k_adamw32_step<float>, (units + 3) / 4, &grid))
-            return e;
-        k_adamw32_step<float><<<grid, kThreads, 0, st>>>(d_prefix, d_desc, K, units, sc, coef,
-                                                         status);
-    }
+    if (lt_err e = grid_size(kernel, (units + 3) / 4, &grid))
+        return e;
+    kernel<<<grid, kThreads, 0, st>>>(d_prefix, d_desc, K, units, sc, coef, status);
     LT_HIP(hipGetLastError());
+    if (status && wb)
+        return launch_bf16_on_skip(d_prefix, d_desc, K, units, span, status, st);
     return LT_OK;
 }
 

@@ -52,20 +52,21 @@ def lib() -> ctypes.CDLL:
     L.lt_clip_coef.argtypes = [vp, ctypes.c_float, vp, vp, vp]
     L.lt_step_workspace_bytes.argtypes = [ctypes.c_int]
     L.lt_step_workspace_bytes.restype = ctypes.c_size_t
-    L.lt_hybrid8bit_adamw_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, i64p,
-                                           ctypes.c_int, ctypes.c_int] + [ctypes.c_double] * 5 + [
+    L.lt_hybrid8bit_adamw_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, vpp,
+                                           i64p, ctypes.c_int, ctypes.c_int] + [
+                                               ctypes.c_double] * 5 + [
                                                ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp]
     ip = ctypes.POINTER(ctypes.c_int)
     L.lt_streamed_workspace_bytes.argtypes = [i64p, ctypes.c_int, ip, ctypes.c_int, ctypes.c_int,
-                                              ctypes.c_int, ctypes.c_int]
+                                              ctypes.c_int, ctypes.c_int, ctypes.c_int]
     L.lt_streamed_workspace_bytes.restype = ctypes.c_size_t
     L.lt_streamed_hybrid8bit_adamw_step.argtypes = [
-        vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, i64p, ctypes.c_int, ip, ctypes.c_int,
+        vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, vpp, i64p, ctypes.c_int, ip, ctypes.c_int,
         ctypes.c_int] + [ctypes.c_double] * 5 + [ctypes.c_int64, ctypes.c_float, ctypes.c_int, vp,
                                                  ctypes.c_size_t, vp, vp, vp, vp, vp, vp, vp]
     L.lt_adamw_fp32_workspace_bytes.argtypes = [ctypes.c_int]
     L.lt_adamw_fp32_workspace_bytes.restype = ctypes.c_size_t
-    L.lt_adamw_fp32_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, i64p, ctypes.c_int] + [
+    L.lt_adamw_fp32_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, i64p, ctypes.c_int] + [
         ctypes.c_double] * 5 + [ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp]
     L.lt_select_8bit_slice.argtypes = [i64p, ctypes.c_int, ctypes.c_double,
                                        ctypes.POINTER(ctypes.c_uint8),
@@ -120,6 +121,25 @@ def _check_tensors(tensors, device, dtype=None, what="tensor"):
             raise ValueError(f"{what}[{i}] must be contiguous")
         if dtype is not None and t.dtype != dtype:
             raise TypeError(f"{what}[{i}] has dtype {t.dtype}, expected {dtype}")
+
+
+def _bf16_list(copies, params, device):
+    """The optional bf16 weight-copy list: None, or one tensor (or None) per parameter
+    with the parameter's element count."""
+    if copies is None:
+        return None
+    if len(copies) != len(params):
+        raise ValueError("params_bf16 needs one entry (a tensor or None) per parameter")
+    for i, (c, p) in enumerate(zip(copies, params)):
+        if c is None:
+            continue
+        if c.device != device or not c.is_contiguous():
+            raise ValueError(f"params_bf16[{i}] must be contiguous on {device}")
+        if c.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+            raise TypeError(f"params_bf16[{i}] must be bfloat16, got {c.dtype}")
+        if c.numel() != p.numel():
+            raise ValueError(f"params_bf16[{i}] must have {p.numel()} elements")
+    return (ctypes.c_void_p * len(copies))(*[0 if c is None else c.data_ptr() for c in copies])
 
 
 def _scalar(t: Optional[torch.Tensor], device, dtype, what) -> int:
@@ -196,8 +216,11 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
                              weight_decay: float, step: int,
                              coef: Optional[torch.Tensor] = None,
                              status: Optional[torch.Tensor] = None,
-                             workspace: Optional[torch.Tensor] = None, stream=None) -> None:
-    """Steps a4-a10 in place on params, codes and absmax (see include/lazytrain.h)."""
+                             workspace: Optional[torch.Tensor] = None, stream=None,
+                             params_bf16=None) -> None:
+    """Steps a4-a10 in place on params, codes and absmax (see include/lazytrain.h);
+    params_bf16 (optional, one bf16 tensor or None per parameter) receives the bf16
+    copy of the updated weights."""
     k = len(params)
     if k == 0 or not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) ==
                       len(v_absmax) == k):
@@ -217,21 +240,24 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
             raise ValueError(f"tensor {i}: params, grads and codes must have {n} elements")
         if m_absmax[i].numel() < nb or v_absmax[i].numel() < nb:
             raise ValueError(f"tensor {i}: absmax arrays need ceil({n}/{block_size}) = {nb} entries")
+    wb = _bf16_list(params_bf16, params, device)
     ws = _workspace(device, lt_step_workspace_bytes(k), workspace, stream)
     _check(lib().lt_hybrid8bit_adamw_step(
         _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
-        _ptr_array(v_codes), _ptr_array(v_absmax), _numel_array(params), k, int(block_size),
+        _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, int(block_size),
         float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
         _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
         ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
 
 
 def lt_streamed_workspace_bytes(numels: Sequence[int], layer_first: Sequence[int],
-                                grad_dtype: int, block_size: int, ring_slots: int) -> int:
+                                grad_dtype: int, block_size: int, ring_slots: int,
+                                bf16_copy: bool = False) -> int:
     n = (ctypes.c_int64 * len(numels))(*numels)
     f = (ctypes.c_int * len(layer_first))(*layer_first)
     return int(lib().lt_streamed_workspace_bytes(n, len(numels), f, len(layer_first) - 1,
-                                                 grad_dtype, block_size, ring_slots))
+                                                 grad_dtype, block_size, ring_slots,
+                                                 int(bool(bf16_copy))))
 
 
 def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes, v_absmax,
@@ -243,9 +269,10 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
                                       total_norm: Optional[torch.Tensor] = None,
                                       workspace: Optional[torch.Tensor] = None,
                                       compute_stream=None, h2d_stream=None,
-                                      d2h_stream=None) -> None:
+                                      d2h_stream=None, params_bf16=None) -> None:
     """Step a11: host-resident tensors (CPU, ideally pinned) streamed layer by layer
-    through HBM; scalar outputs are device tensors (see include/lazytrain.h)."""
+    through HBM; scalar outputs are device tensors (see include/lazytrain.h).
+    params_bf16 (optional, host bf16 tensors or None) receives the bf16 weight copy."""
     k = len(params)
     if k == 0 or not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) ==
                       len(v_absmax) == k):
@@ -266,8 +293,10 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
         if m_absmax[i].numel() < nb or v_absmax[i].numel() < nb:
             raise ValueError(f"tensor {i}: absmax arrays need {nb} entries")
     device = sq_total.device
+    wb = _bf16_list(params_bf16, params, cpu)
     numels = [p.numel() for p in params]
-    nbytes = lt_streamed_workspace_bytes(numels, layer_first, gdt, block_size, ring_slots)
+    nbytes = lt_streamed_workspace_bytes(numels, layer_first, gdt, block_size, ring_slots,
+                                         wb is not None)
     if nbytes == 0:
         raise ValueError("invalid layer_first, block_size or ring_slots")
     cs = _stream_handle(compute_stream, device)
@@ -279,7 +308,7 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
     ds = _stream_handle(d2h_stream, device) if d2h_stream is not None else cs
     _check(lib().lt_streamed_hybrid8bit_adamw_step(
         _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
-        _ptr_array(v_codes), _ptr_array(v_absmax), _numel_array(params), k, first,
+        _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, first,
         len(layer_first) - 1, int(block_size), float(lr), float(beta1), float(beta2), float(eps),
         float(weight_decay), int(step), float(max_norm), int(ring_slots), workspace.data_ptr(),
         workspace.numel() * workspace.element_size(),
@@ -298,8 +327,10 @@ def lt_adamw_fp32_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Ten
                        lr: float, beta1: float, beta2: float, eps: float, weight_decay: float,
                        step: int, coef: Optional[torch.Tensor] = None,
                        status: Optional[torch.Tensor] = None,
-                       workspace: Optional[torch.Tensor] = None, stream=None) -> None:
-    """fp32-state AdamW, in place on params, exp_avg and exp_avg_sq (device tensors)."""
+                       workspace: Optional[torch.Tensor] = None, stream=None,
+                       params_bf16=None) -> None:
+    """fp32-state AdamW, in place on params, exp_avg and exp_avg_sq (device tensors);
+    params_bf16 as in lt_hybrid8bit_adamw_step."""
     k = len(params)
     if k == 0 or not (len(grads) == len(exp_avg) == len(exp_avg_sq) == k):
         raise ValueError("tensor lists must be non-empty and of equal length")
@@ -313,10 +344,11 @@ def lt_adamw_fp32_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Ten
         n = params[i].numel()
         if grads[i].numel() != n or exp_avg[i].numel() != n or exp_avg_sq[i].numel() != n:
             raise ValueError(f"tensor {i}: params, grads and states must have {n} elements")
+    wb = _bf16_list(params_bf16, params, device)
     ws = _workspace(device, lt_adamw_fp32_workspace_bytes(k), workspace, stream)
     _check(lib().lt_adamw_fp32_step(
         _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(exp_avg), _ptr_array(exp_avg_sq),
-        _numel_array(params), k, float(lr), float(beta1), float(beta2), float(eps),
+        wb, _numel_array(params), k, float(lr), float(beta1), float(beta2), float(eps),
         float(weight_decay), int(step), _scalar(coef, device, torch.float32, "coef"),
         _scalar(status, device, torch.int32, "status"), ws.data_ptr(),
         ws.numel() * ws.element_size(), _stream_handle(stream, device)))
@@ -353,12 +385,14 @@ class Hybrid8bitAdamW:
     8-bit states; otherwise lt_select_8bit_slice picks the tensors that do (the
     paper's 2% slice) and the others keep fp32 states (lt_adamw_fp32_step), all under
     one global norm.  The caller owns the skip/abort policy: ``last_status()`` reads
-    the status word of the last step."""
+    the status word of the last step.  With ``bf16_copy`` the steps also keep
+    ``params_bf16``, a bf16 copy of every parameter for the next forward pass,
+    written by the step kernels (valid after the first step)."""
 
     def __init__(self, params: Sequence[torch.Tensor], lr: float = 1e-5,
                  betas=(0.9, 0.999), eps: float = 1e-8, weight_decay: float = 0.01,
                  max_norm: float = 1.0, block_size: int = 4096,
-                 slice_fraction: Optional[float] = None):
+                 slice_fraction: Optional[float] = None, bf16_copy: bool = False):
         self.params = list(params)
         if not self.params:
             raise ValueError("no parameters")
@@ -384,6 +418,8 @@ class Hybrid8bitAdamW:
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
         self.coef = torch.ones(1, dtype=torch.float32, device=dev)
         self.total_norm = torch.zeros(1, dtype=torch.float32, device=dev)
+        self.params_bf16 = [torch.empty(p.numel(), dtype=torch.bfloat16, device=dev)
+                            for p in self.params] if bf16_copy else None
         self.step_count = 0  # steps applied (skipped steps do not count)
         self._unchecked = False
 
@@ -397,13 +433,17 @@ class Hybrid8bitAdamW:
         hyper = dict(lr=self.lr, beta1=self.betas[0], beta2=self.betas[1], eps=self.eps,
                      weight_decay=self.weight_decay, step=t, coef=self.coef, status=self.status,
                      stream=stream)
+        wb = self.params_bf16
         if self.idx8:
             lt_hybrid8bit_adamw_step([self.params[i] for i in self.idx8],
                                      [grads[i] for i in self.idx8], self.m_codes, self.m_absmax,
-                                     self.v_codes, self.v_absmax, self.block_size, **hyper)
+                                     self.v_codes, self.v_absmax, self.block_size,
+                                     params_bf16=None if wb is None else [wb[i] for i in self.idx8],
+                                     **hyper)
         if self.idx32:
             lt_adamw_fp32_step([self.params[i] for i in self.idx32],
                                [grads[i] for i in self.idx32], self.exp_avg, self.exp_avg_sq,
+                               params_bf16=None if wb is None else [wb[i] for i in self.idx32],
                                **hyper)
         self.step_count = t
         self._unchecked = True
