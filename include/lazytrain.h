@@ -94,6 +94,45 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
 lt_err lt_clip_coef(const double* sq_total, float max_norm, float* total_norm, float* coef,
                     void* stream);
 
+/* Number of 8192-element chunks of a tensor list: the number of fp64 partials
+ * the sum of squares keeps for it.  0 if an argument is invalid. */
+int64_t lt_grad_chunk_count(const int64_t* numels, int n_tensors);
+
+/* Bytes of device workspace lt_grad_sqnorm_partials needs (descriptors). */
+size_t lt_grad_sqnorm_partials_workspace_bytes(int n_tensors);
+
+/*
+ * Step a1 on part of a model, as its gradients arrive (f4: norm accumulation
+ * during backward, so that a layer-streaming executor, which offloads
+ * gradients layer by layer, never streams them back in for the norm;
+ * Sec. 3.1 and the gradient D2H traffic of Sec. 3.4).  Writes the fp64 chunk
+ * partials of grads[0..n_tensors) in the fixed order of lt_grad_sqnorm.
+ *   partials  device double[lt_grad_chunk_count(numels, n_tensors)]: the slice
+ *             of the model-wide partials array that starts at these tensors'
+ *             first chunk (the chunk count of the model's earlier tensors).
+ * The parts of a model may arrive in any order, on any streams; once all are
+ * written, lt_grad_sqnorm_finish gives bitwise the result of lt_grad_sqnorm
+ * over the whole list.
+ */
+lt_err lt_grad_sqnorm_partials(const void* const* grads, const int64_t* numels, int n_tensors,
+                               int grad_dtype, double* partials, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* Bytes of device workspace lt_grad_sqnorm_finish needs for n_tensors. */
+size_t lt_grad_sqnorm_finish_workspace_bytes(int n_tensors);
+
+/*
+ * Step a2 from the model-wide partials (f4): S_k, S and the non-finite status
+ * exactly as lt_grad_sqnorm computes them (same accumulators, same trees).
+ *   numels    host int64[n_tensors]: the whole model's tensor sizes.
+ *   partials  device double[lt_grad_chunk_count(numels, n_tensors)], every
+ *             entry written by lt_grad_sqnorm_partials.
+ *   sq_per_tensor (may be NULL), sq_total, status: as in lt_grad_sqnorm.
+ */
+lt_err lt_grad_sqnorm_finish(const int64_t* numels, int n_tensors, const double* partials,
+                             void* workspace, size_t workspace_bytes, double* sq_per_tensor,
+                             double* sq_total, int32_t* status, void* stream);
+
 /* Bytes of device workspace lt_hybrid8bit_adamw_step needs for n_tensors
  * tensors (the uploaded descriptor table).  0 if n_tensors < 1. */
 size_t lt_step_workspace_bytes(int n_tensors);
@@ -182,10 +221,15 @@ size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const i
  *                       [layer_first[i], layer_first[i + 1]); 0 = first, n_tensors
  *                       = last, strictly rising.  Layers are streamed in order.
  *   max_norm            > 0; +INFINITY disables clipping (coef = 1).
+ *   norm_ready          nonzero: *sq_total and *status already hold S and its
+ *                       status (from lt_grad_sqnorm_finish over gradients summed
+ *                       as they arrived); pass 1 and the finish are skipped and
+ *                       the gradients are copied in once.
  *   ring_slots          device slots in the ring, 2..16 (3 lets one layer copy in
  *                       while one computes and one copies out).
  *   sq_total, total_norm (may be NULL), coef, status: device outputs as in
- *                       lt_grad_sqnorm and lt_clip_coef.  A NONFINITE status
+ *                       lt_grad_sqnorm and lt_clip_coef (sq_total and status are
+ *                       inputs when norm_ready is set).  A NONFINITE status
  *                       skips the update: weights, codes and scales are copied
  *                       back unchanged.
  *   compute_stream, h2d_stream, d2h_stream: the copies in, the kernels and the
@@ -205,7 +249,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                          const int* layer_first, int n_layers,
                                          int block_size, double lr, double beta1, double beta2,
                                          double eps, double weight_decay, int64_t step,
-                                         float max_norm, int ring_slots, void* workspace,
+                                         float max_norm, int norm_ready, int ring_slots,
+                                         void* workspace,
                                          size_t workspace_bytes, double* sq_total,
                                          float* total_norm, float* coef, int32_t* status,
                                          void* compute_stream, void* h2d_stream, void* d2h_stream);

@@ -1386,6 +1386,101 @@ lt_err lt_clip_coef(const double* sq_total, float max_norm, float* total_norm, f
     return LT_OK;
 }
 
+int64_t lt_grad_chunk_count(const int64_t* numels, int n_tensors)
+{
+    return valid_list(numels, n_tensors) ? sq_chunks_of(numels, n_tensors) : 0;
+}
+
+size_t lt_grad_sqnorm_partials_workspace_bytes(int n_tensors)
+{
+    return n_tensors < 1 ? 0 : round_up(sq_layout(n_tensors, 0).header_bytes, 256);
+}
+
+lt_err lt_grad_sqnorm_partials(const void* const* grads, const int64_t* numels, int n_tensors,
+                               int grad_dtype, double* partials, void* workspace,
+                               size_t workspace_bytes, void* stream)
+{
+    g_last_error.clear();
+    if (!grads || !valid_list(numels, n_tensors))
+        return fail(LT_ERR_INVALID_ARG, "grads/numels must hold n_tensors >= 1 entries with numel >= 1");
+    if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
+        return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
+    if (!partials)
+        return fail(LT_ERR_INVALID_ARG, "partials must not be NULL");
+    if (!aligned(partials, 8))
+        return fail(LT_ERR_ALIGNMENT, "partials must be 8-byte aligned");
+    for (int k = 0; k < n_tensors; ++k) {
+        if (!grads[k])
+            return fail(LT_ERR_INVALID_ARG, "grads[" + std::to_string(k) + "] is NULL");
+        if (!aligned(grads[k], 16))
+            return fail(LT_ERR_ALIGNMENT, "grads[" + std::to_string(k) + "] is not 16-byte aligned");
+    }
+    const int K = n_tensors;
+    const SqLayout lay = sq_layout(K, 0);
+    const size_t need = lt_grad_sqnorm_partials_workspace_bytes(K);
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < need)
+        return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
+                                          std::to_string(need) + " bytes");
+    std::vector<uint8_t> header(lay.header_bytes, 0);
+    auto* prefix = reinterpret_cast<int64_t*>(header.data() + lay.prefix);
+    auto* ptrs = reinterpret_cast<uint64_t*>(header.data() + lay.ptrs);
+    auto* ns = reinterpret_cast<int64_t*>(header.data() + lay.numels);
+    prefix[0] = 0;
+    for (int k = 0; k < K; ++k) {
+        prefix[k + 1] = prefix[k] + (numels[k] + kChunk - 1) / kChunk;
+        ptrs[k] = reinterpret_cast<uint64_t>(grads[k]);
+        ns[k] = numels[k];
+    }
+    auto* ws = static_cast<uint8_t*>(workspace);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (lt_err e = upload(header.data(), header.size(), ws, st))
+        return e;
+    return launch_sq_chunks(grad_dtype, reinterpret_cast<const int64_t*>(ws + lay.prefix),
+                            reinterpret_cast<const uint64_t*>(ws + lay.ptrs),
+                            reinterpret_cast<const int64_t*>(ws + lay.numels), K, prefix[K],
+                            partials, st);
+}
+
+// Finish workspace: [chunk prefix K+1] | [S_k K]
+size_t lt_grad_sqnorm_finish_workspace_bytes(int n_tensors)
+{
+    return n_tensors < 1 ? 0
+                         : round_up(sizeof(int64_t) * (n_tensors + 1), 256) +
+                               round_up(sizeof(double) * n_tensors, 256);
+}
+
+lt_err lt_grad_sqnorm_finish(const int64_t* numels, int n_tensors, const double* partials,
+                             void* workspace, size_t workspace_bytes, double* sq_per_tensor,
+                             double* sq_total, int32_t* status, void* stream)
+{
+    g_last_error.clear();
+    if (!valid_list(numels, n_tensors))
+        return fail(LT_ERR_INVALID_ARG, "numels must hold n_tensors >= 1 entries >= 1");
+    if (!partials || !sq_total || !status)
+        return fail(LT_ERR_INVALID_ARG, "partials, sq_total and status must not be NULL");
+    if (!aligned(partials, 8) || !aligned(sq_total, 8) || !aligned(status, 4) ||
+        (sq_per_tensor && !aligned(sq_per_tensor, 8)))
+        return fail(LT_ERR_ALIGNMENT, "partials and scalar outputs must be naturally aligned");
+    const int K = n_tensors;
+    const size_t need = lt_grad_sqnorm_finish_workspace_bytes(K);
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < need)
+        return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
+                                          std::to_string(need) + " bytes");
+    std::vector<int64_t> prefix(K + 1, 0);
+    for (int k = 0; k < K; ++k)
+        prefix[k + 1] = prefix[k] + (numels[k] + kChunk - 1) / kChunk;
+    auto* ws = static_cast<uint8_t*>(workspace);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (lt_err e = upload(prefix.data(), sizeof(int64_t) * (K + 1), ws, st))
+        return e;
+    auto* d_sk = reinterpret_cast<double*>(ws + round_up(sizeof(int64_t) * (K + 1), 256));
+    k_sqnorm_finish<<<K, kThreads, 0, st>>>(reinterpret_cast<const int64_t*>(ws), partials, d_sk);
+    LT_HIP(hipGetLastError());
+    k_sqnorm_total<<<1, 256, 0, st>>>(d_sk, K, sq_per_tensor, sq_total, status);
+    LT_HIP(hipGetLastError());
+    return LT_OK;
+}
+
 size_t lt_step_workspace_bytes(int n_tensors)
 {
     return n_tensors < 1 ? 0 : step_layout(n_tensors).total;
@@ -1485,7 +1580,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                          int n_tensors, const int* layer_first, int n_layers,
                                          int block_size, double lr, double beta1, double beta2,
                                          double eps, double weight_decay, int64_t step,
-                                         float max_norm, int ring_slots, void* workspace,
+                                         float max_norm, int norm_ready, int ring_slots,
+                                         void* workspace,
                                          size_t workspace_bytes, double* sq_total,
                                          float* total_norm, float* coef, int32_t* status,
                                          void* compute_stream, void* h2d_stream, void* d2h_stream)
@@ -1589,8 +1685,9 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
     auto* d_sk = reinterpret_cast<double*>(ws + lay.sk);
     const auto H2D = hipMemcpyHostToDevice, D2H = hipMemcpyDeviceToHost;
 
-    // Pass 1: gradients in, chunk sums at their global indices.
-    for (int i = 0; i < L; ++i) {
+    // Pass 1: gradients in, chunk sums at their global indices.  Skipped when the
+    // caller summed the gradients as they arrived (sq_total and status are given).
+    for (int i = 0; i < (norm_ready ? 0 : L); ++i) {
         const int sl = i % S;
         if (used[sl])
             LT_HIP(hipStreamWaitEvent(hs, ev.freed[sl], 0));
@@ -1611,11 +1708,13 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         LT_HIP(hipEventRecord(ev.freed[sl], cs));
         used[sl] = true;
     }
-    const auto* d_gprefix = reinterpret_cast<const int64_t*>(ws + lay.gprefix);
-    k_sqnorm_finish<<<K, kThreads, 0, cs>>>(d_gprefix, d_partials, d_sk);
-    LT_HIP(hipGetLastError());
-    k_sqnorm_total<<<1, 256, 0, cs>>>(d_sk, K, nullptr, sq_total, status);
-    LT_HIP(hipGetLastError());
+    if (!norm_ready) {
+        const auto* d_gprefix = reinterpret_cast<const int64_t*>(ws + lay.gprefix);
+        k_sqnorm_finish<<<K, kThreads, 0, cs>>>(d_gprefix, d_partials, d_sk);
+        LT_HIP(hipGetLastError());
+        k_sqnorm_total<<<1, 256, 0, cs>>>(d_sk, K, nullptr, sq_total, status);
+        LT_HIP(hipGetLastError());
+    }
     k_clip_coef<<<1, 64, 0, cs>>>(sq_total, max_norm, total_norm, coef);
     LT_HIP(hipGetLastError());
 

@@ -50,6 +50,16 @@ def lib() -> ctypes.CDLL:
     L.lt_grad_sqnorm.argtypes = [vpp, i64p, ctypes.c_int, ctypes.c_int, vp, ctypes.c_size_t,
                                  vp, vp, vp, vp]
     L.lt_clip_coef.argtypes = [vp, ctypes.c_float, vp, vp, vp]
+    L.lt_grad_chunk_count.argtypes = [i64p, ctypes.c_int]
+    L.lt_grad_chunk_count.restype = ctypes.c_int64
+    L.lt_grad_sqnorm_partials_workspace_bytes.argtypes = [ctypes.c_int]
+    L.lt_grad_sqnorm_partials_workspace_bytes.restype = ctypes.c_size_t
+    L.lt_grad_sqnorm_partials.argtypes = [vpp, i64p, ctypes.c_int, ctypes.c_int, vp, vp,
+                                          ctypes.c_size_t, vp]
+    L.lt_grad_sqnorm_finish_workspace_bytes.argtypes = [ctypes.c_int]
+    L.lt_grad_sqnorm_finish_workspace_bytes.restype = ctypes.c_size_t
+    L.lt_grad_sqnorm_finish.argtypes = [i64p, ctypes.c_int, vp, vp, ctypes.c_size_t, vp, vp, vp,
+                                        vp]
     L.lt_step_workspace_bytes.argtypes = [ctypes.c_int]
     L.lt_step_workspace_bytes.restype = ctypes.c_size_t
     L.lt_hybrid8bit_adamw_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, vpp,
@@ -62,8 +72,9 @@ def lib() -> ctypes.CDLL:
     L.lt_streamed_workspace_bytes.restype = ctypes.c_size_t
     L.lt_streamed_hybrid8bit_adamw_step.argtypes = [
         vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, vpp, i64p, ctypes.c_int, ip, ctypes.c_int,
-        ctypes.c_int] + [ctypes.c_double] * 5 + [ctypes.c_int64, ctypes.c_float, ctypes.c_int, vp,
-                                                 ctypes.c_size_t, vp, vp, vp, vp, vp, vp, vp]
+        ctypes.c_int] + [ctypes.c_double] * 5 + [ctypes.c_int64, ctypes.c_float, ctypes.c_int,
+                                                 ctypes.c_int, vp, ctypes.c_size_t, vp, vp, vp,
+                                                 vp, vp, vp, vp]
     L.lt_adamw_fp32_workspace_bytes.argtypes = [ctypes.c_int]
     L.lt_adamw_fp32_workspace_bytes.restype = ctypes.c_size_t
     L.lt_adamw_fp32_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, i64p, ctypes.c_int] + [
@@ -76,6 +87,7 @@ def lib() -> ctypes.CDLL:
     L.lt_last_error.argtypes = []
     L.lt_last_error.restype = ctypes.c_char_p
     for name in ("lt_grad_sqnorm", "lt_clip_coef", "lt_hybrid8bit_adamw_step", "lt_read_status",
+                 "lt_grad_sqnorm_partials", "lt_grad_sqnorm_finish",
                  "lt_set_max_workgroups", "lt_streamed_hybrid8bit_adamw_step",
                  "lt_adamw_fp32_step", "lt_select_8bit_slice"):
         getattr(L, name).restype = ctypes.c_int
@@ -209,6 +221,77 @@ def lt_clip_coef(sq_total: torch.Tensor, max_norm: float, coef: torch.Tensor,
                               _stream_handle(stream, device)))
 
 
+def lt_grad_chunk_count(numels: Sequence[int]) -> int:
+    arr = (ctypes.c_int64 * len(numels))(*numels)
+    return int(lib().lt_grad_chunk_count(arr, len(numels)))
+
+
+def lt_grad_sqnorm_partials(grads: Sequence[torch.Tensor], partials: torch.Tensor,
+                            workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """a1 on part of a model as its gradients arrive: chunk partials into
+    ``partials``, a float64 device view of the model-wide array starting at these
+    tensors' first chunk (see include/lazytrain.h)."""
+    if not grads:
+        raise ValueError("empty gradient list")
+    device = grads[0].device
+    _check_tensors(grads, device, what="grads")
+    gdt = _grad_dtype(grads)
+    need = lt_grad_chunk_count([g.numel() for g in grads])
+    if partials.device != device or partials.dtype != torch.float64 or \
+            not partials.is_contiguous() or partials.numel() < need:
+        raise ValueError(f"partials must be a contiguous float64 device view of >= {need} entries")
+    ws = _workspace(device, int(lib().lt_grad_sqnorm_partials_workspace_bytes(len(grads))),
+                    workspace, stream)
+    _check(lib().lt_grad_sqnorm_partials(
+        _ptr_array(grads), _numel_array(grads), len(grads), gdt, partials.data_ptr(),
+        ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
+
+
+def lt_grad_sqnorm_finish(numels: Sequence[int], partials: torch.Tensor, sq_total: torch.Tensor,
+                          status: torch.Tensor, sq_per_tensor: Optional[torch.Tensor] = None,
+                          workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """a2 from the model-wide partials: S_k, S and the status, bitwise as
+    lt_grad_sqnorm over the whole list."""
+    device = partials.device
+    if partials.dtype != torch.float64 or partials.numel() < lt_grad_chunk_count(numels):
+        raise ValueError("partials must hold one float64 per chunk of the model")
+    if sq_per_tensor is not None and sq_per_tensor.numel() < len(numels):
+        raise ValueError("sq_per_tensor needs one float64 per tensor")
+    ws = _workspace(device, int(lib().lt_grad_sqnorm_finish_workspace_bytes(len(numels))),
+                    workspace, stream)
+    arr = (ctypes.c_int64 * len(numels))(*numels)
+    _check(lib().lt_grad_sqnorm_finish(
+        arr, len(numels), partials.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
+        _scalar(sq_per_tensor, device, torch.float64, "sq_per_tensor"),
+        _scalar(sq_total, device, torch.float64, "sq_total"),
+        _scalar(status, device, torch.int32, "status"), _stream_handle(stream, device)))
+
+
+class GradNormAccumulator:
+    """Sums a model's gradients part by part as they arrive (in any order), then
+    finishes S and the status: lt_grad_sqnorm_partials on each part at its chunk
+    offset, lt_grad_sqnorm_finish at the end."""
+
+    def __init__(self, numels: Sequence[int], device):
+        self.numels = [int(n) for n in numels]
+        self.offsets = [0]
+        for n in self.numels:
+            self.offsets.append(self.offsets[-1] + -(-n // 8192))
+        self.partials = torch.empty(self.offsets[-1], dtype=torch.float64, device=device)
+
+    def add(self, first: int, grads: Sequence[torch.Tensor], stream=None) -> None:
+        """Gradients of tensors first .. first + len(grads) - 1 of the model."""
+        if first < 0 or first + len(grads) > len(self.numels) or \
+                any(g.numel() != self.numels[first + i] for i, g in enumerate(grads)):
+            raise ValueError("gradients do not match the model's tensors at this index")
+        lt_grad_sqnorm_partials(grads, self.partials[self.offsets[first]:], stream=stream)
+
+    def finish(self, sq_total: torch.Tensor, status: torch.Tensor,
+               sq_per_tensor: Optional[torch.Tensor] = None, stream=None) -> None:
+        lt_grad_sqnorm_finish(self.numels, self.partials, sq_total, status, sq_per_tensor,
+                              stream=stream)
+
+
 def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Tensor],
                              m_codes: Sequence[torch.Tensor], m_absmax: Sequence[torch.Tensor],
                              v_codes: Sequence[torch.Tensor], v_absmax: Sequence[torch.Tensor],
@@ -269,10 +352,13 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
                                       total_norm: Optional[torch.Tensor] = None,
                                       workspace: Optional[torch.Tensor] = None,
                                       compute_stream=None, h2d_stream=None,
-                                      d2h_stream=None, params_bf16=None) -> None:
+                                      d2h_stream=None, params_bf16=None,
+                                      norm_ready: bool = False) -> None:
     """Step a11: host-resident tensors (CPU, ideally pinned) streamed layer by layer
     through HBM; scalar outputs are device tensors (see include/lazytrain.h).
-    params_bf16 (optional, host bf16 tensors or None) receives the bf16 weight copy."""
+    params_bf16 (optional, host bf16 tensors or None) receives the bf16 weight copy.
+    With norm_ready, sq_total and status already hold S and its status (summed as the
+    gradients arrived) and the first streamed pass is skipped."""
     k = len(params)
     if k == 0 or not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) ==
                       len(v_absmax) == k):
@@ -310,7 +396,8 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
         _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
         _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, first,
         len(layer_first) - 1, int(block_size), float(lr), float(beta1), float(beta2), float(eps),
-        float(weight_decay), int(step), float(max_norm), int(ring_slots), workspace.data_ptr(),
+        float(weight_decay), int(step), float(max_norm), int(bool(norm_ready)), int(ring_slots),
+        workspace.data_ptr(),
         workspace.numel() * workspace.element_size(),
         _scalar(sq_total, device, torch.float64, "sq_total"),
         _scalar(total_norm, device, torch.float32, "total_norm"),
