@@ -55,16 +55,20 @@ def _load():
     lib.lto_step_scalars.restype = None
     lib.lto_hybrid8bit_adamw_step.argtypes = [
         _vpp, _vpp, ctypes.c_int, _vpp, _vpp, _vpp, _vpp, _i64p, ctypes.c_int, ctypes.c_int64,
-        ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+        ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+        ctypes.c_double,
         ctypes.c_int64, fp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
     lib.lto_hybrid8bit_adamw_step.restype = ctypes.c_int
-    for name, qt in (("signed", ctypes.c_int8), ("unsigned", ctypes.c_uint8)):
+    for name, qt in (("signed", ctypes.c_int8), ("unsigned", ctypes.c_uint8),
+                     ("dynamic_signed", ctypes.c_int8), ("dynamic_unsigned", ctypes.c_uint8)):
         qf = getattr(lib, "lto_quantize_" + name)
         qf.argtypes = [fp, ctypes.c_int64, ctypes.POINTER(qt), fp]
         qf.restype = None
         df = getattr(lib, "lto_dequantize_" + name)
         df.argtypes = [ctypes.POINTER(qt), ctypes.c_int64, ctypes.c_float, fp]
         df.restype = None
+    lib.lto_dynamic_map.argtypes = [ctypes.c_int, fp]
+    lib.lto_dynamic_map.restype = None
     lib.lto_adamw_fp32_step.argtypes = [fp, ctypes.c_void_p, ctypes.c_int, fp, fp,
                                         ctypes.c_int64] + [ctypes.c_double] * 5 + [
                                             ctypes.c_int64, ctypes.c_float]
@@ -132,9 +136,13 @@ def step_scalars(lr, beta1, beta2, eps, weight_decay, step):
     return {n: np.float32(getattr(out, n)) for n, _ in _Scalars._fields_}
 
 
+MAP_LINEAR, MAP_DYNAMIC = 0, 1
+
+
 def hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes, v_absmax, block_size: int,
                           lr: float, beta1: float, beta2: float, eps: float, weight_decay: float,
-                          step: int, coef=None, status=None, n_threads: int = 1) -> None:
+                          step: int, coef=None, status=None, n_threads: int = 1,
+                          code_map: int = MAP_LINEAR) -> None:
     """In-place step over lists of numpy arrays (see lazytrain_oracle.h)."""
     k = len(params)
     if not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) == len(v_absmax) == k):
@@ -154,7 +162,8 @@ def hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes, v_absmax, b
     st = ctypes.byref(ctypes.c_int32(status)) if status is not None else None
     rc = _load().lto_hybrid8bit_adamw_step(
         _ptrs(params), _ptrs(grads), gdt, _ptrs(m_codes), _ptrs(m_absmax), _ptrs(v_codes),
-        _ptrs(v_absmax), _numels(params), k, block_size, lr, beta1, beta2, eps, weight_decay,
+        _ptrs(v_absmax), _numels(params), k, block_size, code_map, lr, beta1, beta2, eps,
+        weight_decay,
         step, c, st, n_threads)
     if rc != 0:
         raise ValueError(f"lto_hybrid8bit_adamw_step failed ({rc})")
@@ -213,3 +222,46 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     y = np.empty(x.shape, dtype=np.uint16)
     _load().lto_round_bf16(_fp(x), x.size, y.ctypes.data_as(ctypes.POINTER(ctypes.c_uint16)))
     return y
+
+
+def dynamic_map(signed: bool) -> np.ndarray:
+    """The dynamic code map's magnitudes: 128 (signed) or 256 (unsigned) float32."""
+    t = np.zeros(128 if signed else 256, dtype=np.float32)
+    _load().lto_dynamic_map(1 if signed else 0, _fp(t))
+    return t
+
+
+def _quantize(name, x, qtype):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    q = np.zeros(x.size, dtype=qtype)
+    a = ctypes.c_float()
+    ct = ctypes.c_int8 if qtype == np.int8 else ctypes.c_uint8
+    getattr(_load(), "lto_quantize_" + name)(_fp(x), x.size, q.ctypes.data_as(ctypes.POINTER(ct)),
+                                              ctypes.byref(a))
+    return q, a.value
+
+
+def _dequantize(name, q, absmax, qtype):
+    q = np.ascontiguousarray(q, dtype=qtype)
+    x = np.zeros(q.size, dtype=np.float32)
+    ct = ctypes.c_int8 if qtype == np.int8 else ctypes.c_uint8
+    getattr(_load(), "lto_dequantize_" + name)(q.ctypes.data_as(ctypes.POINTER(ct)), q.size,
+                                                absmax, _fp(x))
+    return x
+
+
+def quantize_dynamic_signed(x):
+    """Sign-magnitude dynamic codes (int8 storage) and the absmax of one block."""
+    return _quantize("dynamic_signed", x, np.int8)
+
+
+def quantize_dynamic_unsigned(x):
+    return _quantize("dynamic_unsigned", x, np.uint8)
+
+
+def dequantize_dynamic_signed(q, absmax: float):
+    return _dequantize("dynamic_signed", q, absmax, np.int8)
+
+
+def dequantize_dynamic_unsigned(q, absmax: float):
+    return _dequantize("dynamic_unsigned", q, absmax, np.uint8)

@@ -177,6 +177,94 @@ void lto_dequantize_unsigned(const uint8_t* q, int64_t n, float absmax, float* x
         x[i] = (float)q[i] * step;
 }
 
+/* ------------------------------------------------- dynamic code map (f2) */
+
+/* Powers of ten of the map's decades, as correctly rounded double literals. */
+static const double pow10_neg[8] = {1.0, 1e-1, 1e-2, 1e-3, 1e-4, 1e-5, 1e-6, 1e-7};
+
+void lto_dynamic_map(int is_signed, float* table)
+{
+    const int bits = is_signed ? 7 : 8; /* magnitude bits of a code */
+    const int n = 1 << bits;
+    table[0] = 0.0f;
+    for (int c = 1; c < n; ++c) {
+        int p = 0; /* position of the leading one: p fraction bits follow it */
+        while ((c >> (p + 1)) != 0)
+            ++p;
+        const int zeros = bits - 1 - p; /* leading zero bits: the decade */
+        const int f = c - (1 << p);      /* the fraction bits */
+        const double frac = 0.1 + 0.9 * ((double)(f + 1) / (double)(1 << p));
+        table[c] = (float)(frac * pow10_neg[zeros]);
+    }
+}
+
+/* The code whose magnitude is nearest to a: the smallest c with the least
+ * fabsf(a - table[c]) (a NaN a gives 0). */
+static int nearest_code(const float* table, int n, float a)
+{
+    int best = 0;
+    float bd = fabsf(a - table[0]);
+    for (int c = 1; c < n; ++c) {
+        const float d = fabsf(a - table[c]);
+        if (d < bd) {
+            bd = d;
+            best = c;
+        }
+    }
+    return best;
+}
+
+void lto_quantize_dynamic_signed(const float* x, int64_t n, int8_t* q, float* absmax)
+{
+    float T[128];
+    lto_dynamic_map(1, T);
+    float A = 0.0f;
+    for (int64_t i = 0; i < n; ++i)
+        A = fmaxf(A, fabsf(x[i]));
+    const float inv = 1.0f / A;
+    const int ok = isfinite(A) && isfinite(inv);
+    for (int64_t i = 0; i < n; ++i) {
+        int c = ok ? nearest_code(T, 128, fabsf(x[i]) * inv) : 0;
+        if (c != 0 && signbit(x[i]))
+            c |= 0x80; /* sign-magnitude byte */
+        q[i] = (int8_t)(uint8_t)c;
+    }
+    *absmax = ok ? A : 0.0f;
+}
+
+void lto_quantize_dynamic_unsigned(const float* x, int64_t n, uint8_t* q, float* absmax)
+{
+    float U[256];
+    lto_dynamic_map(0, U);
+    float A = 0.0f;
+    for (int64_t i = 0; i < n; ++i)
+        A = fmaxf(A, x[i]);
+    const float inv = 1.0f / A;
+    const int ok = isfinite(A) && isfinite(inv);
+    for (int64_t i = 0; i < n; ++i)
+        q[i] = ok ? (uint8_t)nearest_code(U, 256, x[i] * inv) : (uint8_t)0;
+    *absmax = ok ? A : 0.0f;
+}
+
+void lto_dequantize_dynamic_signed(const int8_t* q, int64_t n, float absmax, float* x)
+{
+    float T[128];
+    lto_dynamic_map(1, T);
+    for (int64_t i = 0; i < n; ++i) {
+        const uint8_t b = (uint8_t)q[i];
+        const float mag = T[b & 0x7F];
+        x[i] = ((b & 0x80) ? -mag : mag) * absmax;
+    }
+}
+
+void lto_dequantize_dynamic_unsigned(const uint8_t* q, int64_t n, float absmax, float* x)
+{
+    float U[256];
+    lto_dynamic_map(0, U);
+    for (int64_t i = 0; i < n; ++i)
+        x[i] = U[q[i]] * absmax;
+}
+
 /* --------------------------------------------------------- AdamW step (a4-a10) */
 
 void lto_step_scalars(double lr, double beta1, double beta2, double eps, double weight_decay,
@@ -217,14 +305,15 @@ static void adamw_element(const adamw_scalars* s, float m0, float v0, float grad
 
 /* One quantization block: elements [off, off + len) of a tensor; *am, *av are
  * this block's stored scales. */
-static void step_block(const adamw_scalars* s, float* w, const void* g, int gdt, int64_t off,
-                       int64_t len, int8_t* qm, float* am, uint8_t* qv, float* av, float* m1,
-                       float* v1)
+static void step_block(const adamw_scalars* s, int code_map, float* w, const void* g, int gdt,
+                       int64_t off, int64_t len, int8_t* qm, float* am, uint8_t* qv, float* av,
+                       float* m1, float* v1)
 {
     float* m0 = m1; /* reuse the scratch: dequantize in place, then update */
     float* v0 = v1;
-    lto_dequantize_signed(qm + off, len, *am, m0);
-    lto_dequantize_unsigned(qv + off, len, *av, v0);
+    const int dyn = code_map == LTO_MAP_DYNAMIC;
+    (dyn ? lto_dequantize_dynamic_signed : lto_dequantize_signed)(qm + off, len, *am, m0);
+    (dyn ? lto_dequantize_dynamic_unsigned : lto_dequantize_unsigned)(qv + off, len, *av, v0);
     for (int64_t i = 0; i < len; ++i) {
         float mn, vn, wn;
         adamw_element(s, m0[i], v0[i], grad_value(g, gdt, off + i), w[off + i], &mn, &vn, &wn);
@@ -232,19 +321,20 @@ static void step_block(const adamw_scalars* s, float* w, const void* g, int gdt,
         m1[i] = mn; /* the update uses the unquantized m1, v1; codes are storage */
         v1[i] = vn;
     }
-    lto_quantize_signed(m1, len, qm + off, am);
-    lto_quantize_unsigned(v1, len, qv + off, av);
+    (dyn ? lto_quantize_dynamic_signed : lto_quantize_signed)(m1, len, qm + off, am);
+    (dyn ? lto_quantize_dynamic_unsigned : lto_quantize_unsigned)(v1, len, qv + off, av);
 }
 
 int lto_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int gdt,
                               int8_t* const* m_codes, float* const* m_absmax,
                               uint8_t* const* v_codes, float* const* v_absmax,
-                              const int64_t* numels, int n_tensors, int64_t block_size, double lr,
-                              double beta1, double beta2, double eps, double weight_decay,
-                              int64_t step, const float* coef, const int32_t* status,
-                              int n_threads)
+                              const int64_t* numels, int n_tensors, int64_t block_size,
+                              int code_map, double lr, double beta1, double beta2, double eps,
+                              double weight_decay, int64_t step, const float* coef,
+                              const int32_t* status, int n_threads)
 {
-    if (n_tensors < 0 || block_size < 1 || step < 1 || (gdt != LTO_F32 && gdt != LTO_BF16))
+    if (n_tensors < 0 || block_size < 1 || step < 1 || (gdt != LTO_F32 && gdt != LTO_BF16) ||
+        (code_map != LTO_MAP_LINEAR && code_map != LTO_MAP_DYNAMIC))
         return LTO_ERR_INVALID_ARG;
     if (n_tensors > 0 && (!params || !grads || !m_codes || !m_absmax || !v_codes || !v_absmax ||
                           !numels))
@@ -267,8 +357,8 @@ int lto_hybrid8bit_adamw_step(float* const* params, const void* const* grads, in
             for (int64_t b = 0; b < n_blocks; ++b) {
                 int64_t off = b * block_size;
                 int64_t len = (n - off < block_size) ? n - off : block_size;
-                step_block(&s, params[k], grads[k], gdt, off, len, m_codes[k], &m_absmax[k][b],
-                           v_codes[k], &v_absmax[k][b], m1, v1);
+                step_block(&s, code_map, params[k], grads[k], gdt, off, len, m_codes[k],
+                           &m_absmax[k][b], v_codes[k], &v_absmax[k][b], m1, v1);
             }
             free(m1);
             free(v1);

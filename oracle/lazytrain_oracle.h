@@ -36,6 +36,7 @@ extern "C" {
 enum { LTO_F32 = 0, LTO_BF16 = 1 };
 enum { LTO_STATUS_OK = 0, LTO_STATUS_NONFINITE = 1 };
 enum { LTO_OK = 0, LTO_ERR_INVALID_ARG = 1 };
+enum { LTO_MAP_LINEAR = 0, LTO_MAP_DYNAMIC = 1 };
 
 /* Chunk length and lane layout of the fixed sum-of-squares order. */
 #define LTO_CHUNK 8192
@@ -94,15 +95,17 @@ void lto_step_scalars(double lr, double beta1, double beta2, double eps, double 
  * d = fmaf(sqrtf(v1), rbc2, eps), w1 = fmaf(-step_size, m1/d, w*decay);
  * per block the new absmax A'_m = max|m1|, A'_v = max v1 and the codes
  * rint(m1*127/A'_m), rint(v1*255/A'_v) (clamped); a block whose absmax or
- * reciprocal is not finite stores zero codes and absmax 0.
+ * reciprocal is not finite stores zero codes and absmax 0.  code_map
+ * LTO_MAP_LINEAR is that map; LTO_MAP_DYNAMIC decodes and encodes with the
+ * dynamic map below instead (the same absmax and zero-block rule).
  */
 int lto_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int gdt,
                               int8_t* const* m_codes, float* const* m_absmax,
                               uint8_t* const* v_codes, float* const* v_absmax,
-                              const int64_t* numels, int n_tensors, int64_t block_size, double lr,
-                              double beta1, double beta2, double eps, double weight_decay,
-                              int64_t step, const float* coef, const int32_t* status,
-                              int n_threads);
+                              const int64_t* numels, int n_tensors, int64_t block_size,
+                              int code_map, double lr, double beta1, double beta2, double eps,
+                              double weight_decay, int64_t step, const float* coef,
+                              const int32_t* status, int n_threads);
 
 /* Block quantizers used by the step (exported for the quantizer tests).
  * Signed (first moment): A = max|x|, q = clamp(rint(x * (127/A)), -127, 127).
@@ -112,6 +115,31 @@ void lto_quantize_signed(const float* x, int64_t n, int8_t* q, float* absmax);
 void lto_quantize_unsigned(const float* x, int64_t n, uint8_t* q, float* absmax);
 void lto_dequantize_signed(const int8_t* q, int64_t n, float absmax, float* x);
 void lto_dequantize_unsigned(const uint8_t* q, int64_t n, float absmax, float* x);
+
+/*
+ * Dynamic (non-linear) code map.  The paper names block-wise 8-bit AdamW
+ * states without giving a code map (Sec. 3.5); besides the linear absmax map,
+ * the common reading is the dynamic tree quantization of Dettmers et al.
+ * (8-bit optimizers via block-wise quantization, 2022), restated here.  A code's
+ * magnitude bits read: leading zero bits give the decade 10^-zeros, the first
+ * one bit is an indicator, and the p bits after it are a linear fraction f:
+ *   magnitude = fp32((0.1 + 0.9 * ((f + 1) / 2^p)) * 10^-zeros), in fp64 in
+ *   that order (10^-zeros a double literal), 0 for the all-zero code.
+ * Signed (first moment): a sign bit and 7 magnitude bits (sign-magnitude byte;
+ * magnitudes 1e-6 .. 1; -0 is never written).  Unsigned (second moment): 8
+ * magnitude bits (1e-7 .. 1).  Magnitudes rise with the code and the top code
+ * is exactly 1, so a block's absmax element is stored exactly.
+ * lto_dynamic_map writes the 128 (signed) or 256 (unsigned) magnitudes.
+ * Quantize: A = max |x| (max x), inv = 1/A in fp32; code = the nearest
+ * magnitude to |x| * inv by fp32 distance (ties to the smaller code, NaN to 0),
+ * with the sign bit of x for a nonzero signed code; a block whose A or inv is
+ * not finite stores zero codes and absmax 0.  Dequantize: +-magnitude * A.
+ */
+void lto_dynamic_map(int is_signed, float* table);
+void lto_quantize_dynamic_signed(const float* x, int64_t n, int8_t* q, float* absmax);
+void lto_quantize_dynamic_unsigned(const float* x, int64_t n, uint8_t* q, float* absmax);
+void lto_dequantize_dynamic_signed(const int8_t* q, int64_t n, float absmax, float* x);
+void lto_dequantize_dynamic_unsigned(const uint8_t* q, int64_t n, float absmax, float* x);
 
 /* fp32-state AdamW with the same operation order as the 8-bit step (states
  * m, v stay fp32 and are updated in place).  Used to check that the 8-bit
