@@ -225,8 +225,8 @@ void lto_quantize_dynamic_signed(const float* x, int64_t n, int8_t* q, float* ab
     const int ok = isfinite(A) && isfinite(inv);
     for (int64_t i = 0; i < n; ++i) {
         int c = ok ? nearest_code(T, 128, fabsf(x[i]) * inv) : 0;
-        if (c != 0 && signbit(x[i]))
-            c |= 0x80; /* sign-magnitude byte */
+        if (ok && x[i] < 0.0f)
+            c |= 0x80; /* sign-magnitude byte: the sign of x, also on magnitude 0 */
         q[i] = (int8_t)(uint8_t)c;
     }
     *absmax = ok ? A : 0.0f;

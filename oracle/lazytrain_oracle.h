@@ -125,15 +125,16 @@ void lto_dequantize_unsigned(const uint8_t* q, int64_t n, float absmax, float* x
  * one bit is an indicator, and the p bits after it are a linear fraction f:
  *   magnitude = fp32((0.1 + 0.9 * ((f + 1) / 2^p)) * 10^-zeros), in fp64 in
  *   that order (10^-zeros a double literal), 0 for the all-zero code.
- * Signed (first moment): a sign bit and 7 magnitude bits (sign-magnitude byte;
- * magnitudes 1e-6 .. 1; -0 is never written).  Unsigned (second moment): 8
+ * Signed (first moment): a sign bit and 7 magnitude bits (sign-magnitude byte,
+ * the sign bit set for x < 0, so a negative value below half the smallest
+ * magnitude is stored as -0; magnitudes 1e-6 .. 1).  Unsigned (second moment): 8
  * magnitude bits (1e-7 .. 1).  Magnitudes rise with the code and the top code
  * is exactly 1, so a block's absmax element is stored exactly.
  * lto_dynamic_map writes the 128 (signed) or 256 (unsigned) magnitudes.
  * Quantize: A = max |x| (max x), inv = 1/A in fp32; code = the nearest
  * magnitude to |x| * inv by fp32 distance (ties to the smaller code, NaN to 0),
- * with the sign bit of x for a nonzero signed code; a block whose A or inv is
- * not finite stores zero codes and absmax 0.  Dequantize: +-magnitude * A.
+ * with the sign bit for x < 0; a block whose A or inv is not finite stores zero
+ * codes and absmax 0.  Dequantize: +-magnitude * A (-0 * A for the code 0x80).
  */
 void lto_dynamic_map(int is_signed, float* table);
 void lto_quantize_dynamic_signed(const float* x, int64_t n, int8_t* q, float* absmax);

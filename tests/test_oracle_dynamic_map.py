@@ -71,7 +71,7 @@ def test_quantizer_against_exact_nearest(signed):
         q, A = oracle.quantize_dynamic_signed(x)
         c = q.view(np.uint8) & 0x7F
         neg = (q.view(np.uint8) & 0x80) != 0
-        assert np.array_equal(neg, (x < 0) & (c != 0))
+        assert np.array_equal(neg, x < 0)
     else:
         q, A = oracle.quantize_dynamic_unsigned(x)
         c = q
@@ -129,11 +129,14 @@ def test_zero_block_nan_and_signs():
     x = np.array([1e-39, 2e-39], np.float32)  # 1/A overflows: zero block
     q, A = oracle.quantize_dynamic_unsigned(x)
     assert A == 0 and not q.any()
-    x = np.array([0.5, np.nan, -0.0, -0.25, 1e-9, -1.0], np.float32)
+    x = np.array([0.5, np.nan, -0.0, -0.25, 1e-9, -1.0, -1e-9], np.float32)
     q, A = oracle.quantize_dynamic_signed(x)
     b = q.view(np.uint8)
     assert A == 1.0 and b[1] == 0 and b[2] == 0 and b[4] == 0
     assert b[5] == 0x80 | 127 and b[3] & 0x80 and not b[0] & 0x80
+    assert b[6] == 0x80  # a negative value below the smallest magnitude keeps its sign
+    back = oracle.dequantize_dynamic_signed(q, A)
+    assert back[6] == 0 and np.signbit(back[6]) and not np.signbit(back[4])
     # odd symmetry
     y = np.linspace(-1, 1, 1001).astype(np.float32)
     q, _ = oracle.quantize_dynamic_signed(y)
