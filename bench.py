@@ -54,7 +54,7 @@ def norm_bytes(numels, gbytes) -> int:
     return sum(numels) * gbytes
 
 
-def build_device_workload(w, dev, n_threads):
+def build_device_workload(w, dev, n_threads, code_map=0):
     """Generates the workload on the host (pinned staging, one tensor at a time),
     copies it to HBM and builds the 8-bit states with one step from zero state at
     t = 1 on an unclipped prior gradient with lr = 0 (weights stay as drawn)."""
@@ -87,7 +87,7 @@ def build_device_workload(w, dev, n_threads):
     hyper = dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay)
     if w.state_init == "prior_step":
         lt.lt_hybrid8bit_adamw_step(params, grads, mq, ma, vq, va, B, step=1,
-                                    **dict(hyper, lr=0.0))
+                                    code_map=code_map, **dict(hyper, lr=0.0))
         torch.cuda.synchronize()
     # the gradient of the measured steps replaces the prior gradient in place
     first = w.step if w.state_init == "prior_step" else 1
@@ -100,7 +100,7 @@ def build_device_workload(w, dev, n_threads):
     return params, grads, mq, ma, vq, va, first
 
 
-def _oracle_pass(w, ks, n_threads):
+def _oracle_pass(w, ks, n_threads, code_map=0):
     """Generates whole tensors ks of the workload on the host, then times one oracle
     pass over them: sum of squares + clip + step."""
     import numpy as np
@@ -120,7 +120,7 @@ def _oracle_pass(w, ks, n_threads):
     _, S, st = oracle.grad_sqnorm(gs, n_threads=n_threads)
     _, c = oracle.clip_coef(S, w.max_norm)
     oracle.hybrid8bit_adamw_step(ws, gs, mq, ma, vq, va, B, step=w.step, coef=float(c), status=st,
-                                 n_threads=n_threads, **hyper)
+                                 n_threads=n_threads, code_map=code_map, **hyper)
     return time.perf_counter() - t0
 
 
@@ -135,7 +135,7 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(w, n_threads, target_s: float):
+def cpu_baseline(w, n_threads, target_s: float, code_map=0):
     """The oracle as it stands, on a bounded sample of the same workload (whole
     tensors, decoder layers first, the embedding last), timed on this host's cores.
     One decoder layer is timed first to size a sample of about target_s seconds;
@@ -146,9 +146,9 @@ def cpu_baseline(w, n_threads, target_s: float):
         order = order[1:] + order[:1]
     first = order[:min(K, 9)]
     n_first = sum(w.numels[k] for k in first)
-    dt = _oracle_pass(w, first, n_threads)
+    dt = _oracle_pass(w, first, n_threads, code_map)
     rate = n_first / dt
-    dt1 = _oracle_pass(w, first, 1)
+    dt1 = _oracle_pass(w, first, 1, code_map)
     ks, total = [], 0
     for k in order:
         if ks and total + w.numels[k] > rate * target_s:
@@ -156,7 +156,7 @@ def cpu_baseline(w, n_threads, target_s: float):
         ks.append(k)
         total += w.numels[k]
     if ks != first:
-        dt = _oracle_pass(w, ks, n_threads)
+        dt = _oracle_pass(w, ks, n_threads, code_map)
     desc = f"{len(ks)} of {K} tensors ({total} of {w.n_params} params) of {w.name}"
     return {"value": total / dt, "unit": "params/s", "cores": n_threads, "kind": "oracle",
             "sample": desc + ": sum of squares + clip + step, one pass", "seconds": round(dt, 3),
@@ -297,7 +297,9 @@ def run_streamed(args, w, dev, n_threads) -> int:
             lists["w"], lists["g"], lists["mq"], lists["ma"], lists["vq"], lists["va"], first, B,
             step=t, max_norm=w.max_norm, ring_slots=slots, sq_total=S, coef=coef, status=status,
             total_norm=norm, workspace=workspace, compute_stream=cs, h2d_stream=hs,
-            d2h_stream=ds, params_bf16=lists.get("wb"), norm_ready=acc is not None, **hyper)
+            d2h_stream=ds, params_bf16=lists.get("wb"), norm_ready=acc is not None,
+            code_map=lt.LT_MAP_DYNAMIC if args.code_map == "dynamic" else lt.LT_MAP_LINEAR,
+            **hyper)
 
     t = 1
     for _ in range(args.warmup):
@@ -328,7 +330,8 @@ def run_streamed(args, w, dev, n_threads) -> int:
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name + ("+bf16-copy" if args.bf16_copy else "") +
-                   ("+norm-on-arrival" if args.norm_on_arrival else ""), "params": n,
+                   ("+norm-on-arrival" if args.norm_on_arrival else "") +
+                   ("+dynamic-map" if args.code_map == "dynamic" else ""), "params": n,
                    "tensors": len(w.shapes), "layers": L,
                    "block_size": B, "grad_dtype": "bf16", "ring_slots": slots,
                    "host_layers": R, "host_state": "pinned, cycled over host_layers"},
@@ -366,6 +369,8 @@ def main() -> int:
     ap.add_argument("--slice-fraction", type=float, default=None,
                     help="hybrid operator: only this fraction of parameters keeps 8-bit states, "
                          "the rest fp32 states (the paper's run uses 0.02)")
+    ap.add_argument("--code-map", choices=["linear", "dynamic"], default="linear",
+                    help="code map of the 8-bit moments")
     ap.add_argument("--bf16-copy", action="store_true",
                     help="the steps also write a bf16 copy of the updated weights (+2 B/param)")
     ap.add_argument("--norm-on-arrival", action="store_true",
@@ -404,7 +409,8 @@ def main() -> int:
     if args.workload == "streamed":
         return run_streamed(args, w, dev, n_threads)
 
-    params, grads, mq, ma, vq, va, t_first = build_device_workload(w, dev, n_threads)
+    code_map = lt.LT_MAP_DYNAMIC if args.code_map == "dynamic" else lt.LT_MAP_LINEAR
+    params, grads, mq, ma, vq, va, t_first = build_device_workload(w, dev, n_threads, code_map)
     idx8, idx32 = list(range(K)), []
     if args.slice_fraction is not None:
         mask, _ = lt.lt_select_8bit_slice(w.numels, args.slice_fraction)
@@ -445,7 +451,7 @@ def main() -> int:
         if p8:
             lt.lt_hybrid8bit_adamw_step(p8, g8, *s8, B, step=t, coef=coef, status=status,
                                         workspace=ws_step, stream=stream, params_bf16=wb8,
-                                        **hyper)
+                                        code_map=code_map, **hyper)
         if p32:
             lt.lt_adamw_fp32_step(p32, g32, exp_avg, exp_avg_sq, step=t, coef=coef,
                                   status=status, workspace=ws_32, stream=stream,
@@ -506,11 +512,13 @@ def main() -> int:
         "step_ms_events": {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9)},
         "config": {"workload": w.name + ("" if not idx32 else
                                          f"-hybrid-{args.slice_fraction:g}-8bit") +
-                   ("+bf16-copy" if args.bf16_copy else ""),
+                   ("+bf16-copy" if args.bf16_copy else "") +
+                   ("+dynamic-map" if args.code_map == "dynamic" else ""),
                    "params": w.n_params, "tensors": K, "block_size": B,
                    "params_8bit": sum(w.numels[k] for k in idx8),
                    "grad_dtype": "bf16" if w.grad_dtype == synth.BF16 else "f32",
-                   "states": "int8 m / uint8 v, fp32 absmax per block",
+                   "states": "int8 m / uint8 v, fp32 absmax per block, " + args.code_map +
+                             " code map",
                    "master": "fp32", "norm_accumulation": "f64",
                    "hyper": {"lr": w.lr, "betas": [w.beta1, w.beta2], "eps": w.eps,
                              "weight_decay": w.weight_decay, "max_norm": w.max_norm}},
@@ -524,13 +532,13 @@ def main() -> int:
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": counter_traffic(w.name)
-                     if not idx32 and not args.bf16_copy else None,
+                     if not idx32 and not args.bf16_copy and args.code_map == "linear" else None,
                      "bytes_per_launch": kbytes},
         "status": st,
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
-        out["cpu_baseline"] = cpu_baseline(w, n_threads, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, n_threads, args.cpu_seconds, code_map)
     print(json.dumps(out), flush=True)
     return 0
 

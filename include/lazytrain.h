@@ -58,6 +58,12 @@ typedef enum lt_dtype {
     LT_DTYPE_BF16 = 1
 } lt_dtype;
 
+/* Code map of the 8-bit moments (see lt_hybrid8bit_adamw_step). */
+typedef enum lt_code_map {
+    LT_MAP_LINEAR = 0, /* linear absmax codes: m = q * A / 127 (int8), v = q * A / 255 (uint8) */
+    LT_MAP_DYNAMIC = 1 /* dynamic tree codes: sign-magnitude m, unsigned v, magnitudes 1e-7 .. 1 */
+} lt_code_map;
+
 /* Bytes of device workspace lt_grad_sqnorm needs for this list (descriptors,
  * one fp64 partial per 8192-element chunk, one fp64 per tensor).  Returns 0 if
  * n_tensors < 1, numels is NULL or a numel is < 1. */
@@ -162,7 +168,22 @@ size_t lt_step_workspace_bytes(int n_tensors);
  * arguments.  Per block: A'_m = max |m1|, A'_v = max v1; codes
  * rint(m1 * (127 / A'_m)) clamped to [-127, 127] and rint(v1 * (255 / A'_v))
  * clamped to [0, 255] (round half to even); a block whose new absmax or its
- * reciprocal is not finite stores zero codes and absmax 0.
+ * reciprocal is not finite stores zero codes and absmax 0.  These are the
+ * codes of code_map = LT_MAP_LINEAR.
+ *   code_map LT_MAP_DYNAMIC: both moments use dynamic tree codes instead (the
+ *            paper names block-wise 8-bit AdamW states without a code map;
+ *            this is the non-linear map of Dettmers et al.'s block-wise 8-bit
+ *            optimizers).  A code's magnitude bits are leading zeros z (decade
+ *            10^-z), an indicator one and p fraction bits f: magnitude
+ *            fp32((0.1 + 0.9 * ((f + 1) / 2^p)) * 10^-z), computed in fp64 in
+ *            that order, 0 for the zero code.  m codes are sign-magnitude
+ *            bytes (sign bit 0x80 set for m1 < 0, 7 magnitude bits, 1e-6 .. 1),
+ *            v codes 8 magnitude bits (1e-7 .. 1).  Decode: m0 = +-magnitude *
+ *            A_m (0x80 gives -0), v0 = magnitude * A_v.  Encode: inv = 1 / A'
+ *            (fp32), the code whose magnitude is nearest |m1| * inv (v1 * inv)
+ *            by fp32 distance, ties to the smaller code, NaN to magnitude 0; the
+ *            same absmax and zero-block rule.  A second moment down to 5e-8 of its
+ *            block's absmax keeps a nonzero code (2e-3 with the linear map).
  *   step     1-based index t of the step being applied (>= 1).
  *   lr, weight_decay >= 0; 0 <= beta1, beta2 < 1; eps >= 0; all finite.
  *   coef     device float or NULL (no clipping, 1.0f).
@@ -183,7 +204,7 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
                                 int8_t* const* m_codes, float* const* m_absmax,
                                 uint8_t* const* v_codes, float* const* v_absmax,
                                 uint16_t* const* params_bf16, const int64_t* numels,
-                                int n_tensors, int block_size, double lr,
+                                int n_tensors, int block_size, int code_map, double lr,
                                 double beta1, double beta2, double eps, double weight_decay,
                                 int64_t step, const float* coef, const int32_t* status,
                                 void* workspace, size_t workspace_bytes, void* stream);
@@ -247,7 +268,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                          float* const* v_absmax, uint16_t* const* params_bf16,
                                          const int64_t* numels, int n_tensors,
                                          const int* layer_first, int n_layers,
-                                         int block_size, double lr, double beta1, double beta2,
+                                         int block_size, int code_map, double lr, double beta1,
+                                         double beta2,
                                          double eps, double weight_decay, int64_t step,
                                          float max_norm, int norm_ready, int ring_slots,
                                          void* workspace,

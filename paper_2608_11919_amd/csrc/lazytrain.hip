@@ -598,11 +598,23 @@ __global__ __launch_bounds__(64) void k_clip_coef(const double* __restrict__ sq_
 // loads occupy: about 150 VGPRs, three waves per SIMD.  One, two and four phases
 // time within 0.5% of each other; four is the fastest of them.
 constexpr int kStepElemsPerLane = 32;
+// With the dynamic code map the per-element work adds LDS table reads, whose
+// latency more waves hide better: 16 elements per lane (about 126 VGPRs, four
+// waves per SIMD) measured 5% faster than 32 and 1% faster than 8 on the
+// 3B-class step.  Block sizes whose block would then span more than the four
+// waves of a workgroup keep 32.
+constexpr int kStepElemsDynamic = 16;
 constexpr int kStepPhases = 4;
 
-template <int B>
+// Elements per lane at most, by block size and code map.
+constexpr int step_elems_max(int B, bool dynamic)
+{
+    return dynamic && B <= 64 * 4 * kStepElemsDynamic ? kStepElemsDynamic : kStepElemsPerLane;
+}
+
+template <int B, bool DYN = false>
 struct StepGeom {
-    static constexpr int E_MAX = kStepElemsPerLane;
+    static constexpr int E_MAX = step_elems_max(B, DYN);
     static constexpr int E = B >= 64 * E_MAX ? E_MAX : (B >= 512 ? B / 64 : 8);  // elements per lane
     static constexpr int G = E / kGranule;                             // granules per lane
     static constexpr int WAVE_SPAN = 64 * E;                           // elements per wave pass
@@ -721,9 +733,174 @@ __device__ inline uint32_t pack4(float q0, float q1, float q2, float q3)
     return __builtin_amdgcn_cvt_pk_u8_f32(q3, 3, w);
 }
 
+// ------------------------------------------- f2: dynamic code map tables
+//
+// Sign-magnitude dynamic tree codes (Dettmers et al., block-wise 8-bit
+// optimizers): a code's magnitude bits are leading zeros z (the decade
+// 10^-z), an indicator one and p fraction bits f, with magnitude
+// fp32((0.1 + 0.9 * ((f + 1) / 2^p)) * 10^-z) computed in fp64 in that order;
+// the first moment has a sign bit (set for m < 0) and 7 magnitude bits
+// (1e-6 .. 1), the second 8 magnitude bits (1e-7 .. 1).  Encoding picks the
+// magnitude nearest to the normalized value a by fp32 distance (ties to the
+// smaller code).
+//
+// The kernel encodes with one LDS read and one integer add.  The fp32
+// pattern's exponent and top 7 mantissa bits (pattern >> 16) index a bucket.
+// No bucket holds two decision points of the map (the builder checks it), so
+// inside bucket i the answer is the nearest code c_i at the bucket's lower end
+// up to some pattern, and c_i + 1 above it.  The bucket's entry is
+// (c_i << 16) + (0xFFFF - l_i), l_i the low 16 bits of the last pattern that
+// still takes c_i: adding the pattern's low 16 bits carries into the code
+// exactly when they exceed l_i.  Patterns below the first bucket take code 0;
+// patterns above the last bucket (only NaN and negative values reach them)
+// take the sentinel entry 0: code 0.  Decoding reads one of 256 signed (or
+// unsigned) magnitudes per byte.  All tables are built at compile time and
+// copied to LDS by each workgroup.
+namespace dyn {
+
+constexpr double kPow10[8] = {1.0, 1e-1, 1e-2, 1e-3, 1e-4, 1e-5, 1e-6, 1e-7};
+
+constexpr float magnitude(int c, int bits)
+{
+    if (c == 0)
+        return 0.0f;
+    int p = 0;
+    while ((c >> (p + 1)) != 0)
+        ++p;
+    const int zeros = bits - 1 - p;
+    const int f = c - (1 << p);
+    return float((0.1 + 0.9 * (double(f + 1) / double(1 << p))) * kPow10[zeros]);
+}
+
+// Buckets: (pattern >> 16) - base.  Bucket 0 starts at 2^-21 (signed) or 2^-25
+// (unsigned), below half the smallest nonzero magnitude; bucket `top` starts
+// at 1.0 (normalized values never exceed 1 + 2^-23); bucket top + 1 is the
+// sentinel.
+constexpr int kBaseM = (127 - 21) << 7, kTopM = (127 << 7) - kBaseM;
+constexpr int kBaseV = (127 - 25) << 7, kTopV = (127 << 7) - kBaseV;
+
+struct Tables {
+    float dm[256];               // decoding: +-magnitude of every m byte (0x80 is -0)
+    float dv[256];               // decoding: magnitude of every v byte
+    uint32_t em[kTopM + 2];      // bucket entries: (code << 16) + 0xFFFF - last low half
+    uint32_t ev[kTopV + 2];
+    float tm[128];               // signed magnitudes (building only)
+    float tv[256];               // unsigned magnitudes (building only)
+    uint32_t one_decision_per_bucket;  // checked at compile time
+};
+
+constexpr float from_bits(uint32_t u) { return __builtin_bit_cast(float, u); }
+
+// The rule between neighbours: code c + 1 beats c when its fp32 distance is smaller.
+constexpr bool next_wins(const float* t, int n, int c, float a)
+{
+    return c + 1 < n && (t[c + 1] - a) < (a - t[c]);
+}
+
+// Nearest magnitude to a >= 0 among t[0..n): the largest c with t[c] <= a by
+// binary search (t rises strictly, t[0] = 0), then that code or the next.
+constexpr int nearest(const float* t, int n, float a)
+{
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (t[mid] <= a)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return next_wins(t, n, lo, a) ? lo + 1 : lo;
+}
+
+// A bucket's entry; *ok is cleared when the bucket holds two decision points.
+constexpr uint32_t bucket_entry(const float* t, int n, int bucket_hi16, uint32_t* ok)
+{
+    const uint32_t p0 = uint32_t(bucket_hi16) << 16;
+    const int c = nearest(t, n, from_bits(p0));
+    if (nearest(t, n, from_bits(p0 | 0xFFFFu)) > c + 1)
+        *ok = 0;
+    if (!next_wins(t, n, c, from_bits(p0 | 0xFFFFu)))
+        return uint32_t(c) << 16;
+    // the first low half where c + 1 wins (the rule is monotone in a), in (0, 0xFFFF]
+    uint32_t a = 1, b = 0xFFFF;
+    while (a < b) {
+        const uint32_t mid = (a + b) / 2;
+        if (next_wins(t, n, c, from_bits(p0 | mid)))
+            b = mid;
+        else
+            a = mid + 1;
+    }
+    return (uint32_t(c) << 16) + (0xFFFFu - (a - 1));
+}
+
+constexpr Tables make_tables()
+{
+    Tables x{};
+    for (int c = 0; c < 128; ++c)
+        x.tm[c] = magnitude(c, 7);
+    for (int c = 0; c < 256; ++c)
+        x.tv[c] = magnitude(c, 8);
+    for (int b = 0; b < 256; ++b) {
+        x.dm[b] = (b & 0x80) ? -x.tm[b & 0x7F] : x.tm[b & 0x7F];
+        x.dv[b] = x.tv[b];
+    }
+    x.one_decision_per_bucket = 1;
+    for (int i = 0; i <= kTopM; ++i)
+        x.em[i] = bucket_entry(x.tm, 128, kBaseM + i, &x.one_decision_per_bucket);
+    for (int i = 0; i <= kTopV; ++i)
+        x.ev[i] = bucket_entry(x.tv, 256, kBaseV + i, &x.one_decision_per_bucket);
+    x.em[kTopM + 1] = 0;  // sentinel: code 0
+    x.ev[kTopV + 1] = 0;
+    return x;
+}
+
+constexpr Tables kTablesHost = make_tables();
+static_assert(kTablesHost.one_decision_per_bucket, "a bucket holds two decision points");
+// the first bucket must take code 0 throughout (smaller patterns are clamped into it)
+static_assert(kTablesHost.em[0] == 0 && kTablesHost.ev[0] == 0, "first bucket");
+
+// What the kernels read, copied to LDS (the building tables stay out).
+struct LdsTables {
+    float dm[256];
+    float dv[256];
+    uint32_t em[kTopM + 2];
+    uint32_t ev[kTopV + 2];
+};
+
+constexpr LdsTables lds_tables()
+{
+    LdsTables y{};
+    for (int i = 0; i < 256; ++i) {
+        y.dm[i] = kTablesHost.dm[i];
+        y.dv[i] = kTablesHost.dv[i];
+    }
+    for (int i = 0; i < kTopM + 2; ++i)
+        y.em[i] = kTablesHost.em[i];
+    for (int i = 0; i < kTopV + 2; ++i)
+        y.ev[i] = kTablesHost.ev[i];
+    return y;
+}
+
+__constant__ const LdsTables kTables = lds_tables();
+
+// Code of the normalized magnitude a (>= 0; NaN and negative values give 0).
+template <int BASE, int TOP>
+__device__ inline uint32_t encode(const uint32_t* entries, float a)
+{
+    const uint32_t bits = __float_as_uint(a);
+    int i = int(bits >> 16) - BASE;
+    i = i < 0 ? 0 : (i > TOP + 1 ? TOP + 1 : i);
+    return (entries[i] + (bits & 0xFFFFu)) >> 16;
+}
+
+}  // namespace dyn
+
+constexpr int kMapLinear = 0, kMapDynamic = 1;
+
 // WB: some tensor of the launch asks for the bf16 weight copy (a separate
 // instantiation keeps the copy's code out of the launches that do not).
-template <typename GT, int B, bool WB>
+// MAP: the code map of both moments, kMapLinear or kMapDynamic.
+template <typename GT, int B, bool WB, int MAP>
 __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restrict__ unit_prefix,
                                                           const StepTensor* __restrict__ desc,
                                                           int n_tensors, int64_t n_units,
@@ -731,7 +908,7 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                                                           const float* __restrict__ coef_ptr,
                                                           const int32_t* __restrict__ status_ptr)
 {
-    using Geo = StepGeom<B>;
+    using Geo = StepGeom<B, MAP == kMapDynamic>;
     constexpr int E = Geo::E, G = Geo::G, W = Geo::W, L = Geo::L, UNIT = Geo::UNIT, PH = Geo::PH;
     __shared__ float red[2][2][4];  // [buffer][m, v][wave], used when W > 1
 
@@ -740,6 +917,18 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
     const float coef = coef_ptr ? *coef_ptr : 1.0f;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
+
+    // Dynamic map: the workgroup copies the code tables into LDS once.
+    __shared__ __align__(16) uint8_t dyn_lds[MAP == kMapDynamic ? sizeof(dyn::LdsTables) : 16];
+    const dyn::LdsTables& tab = *reinterpret_cast<const dyn::LdsTables*>(dyn_lds);
+    if constexpr (MAP == kMapDynamic) {
+        static_assert(sizeof(dyn::LdsTables) % 4 == 0, "tables copy in words");
+        const auto* src = reinterpret_cast<const uint32_t*>(&dyn::kTables);
+        auto* dst = reinterpret_cast<uint32_t*>(dyn_lds);
+        for (int i = threadIdx.x; i < int(sizeof(dyn::LdsTables) / 4); i += kThreads)
+            dst[i] = src[i];
+        __syncthreads();
+    }
 
     // Work units: wave spans (W == 1, each wave on its own) or workgroup spans.
     int64_t u_begin, u_end;
@@ -771,8 +960,9 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
             a_m = exists ? d.ma[blk] : 0.0f;
             a_v = exists ? d.va[blk] : 0.0f;
         }
-        const float step_m = div_by_const<127>(a_m);
-        const float step_v = div_by_const<255>(a_v);
+        // linear map: the code steps A/127 and A/255
+        const float step_m = MAP == kMapLinear ? div_by_const<127>(a_m) : 0.0f;
+        const float step_v = MAP == kMapLinear ? div_by_const<255>(a_v) : 0.0f;
 
         // The lane's granules go through load -> moments -> sqrt/divide -> weight
         // store in PH phases, which bounds the registers the loads occupy.  m1 and
@@ -807,11 +997,17 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                 for (int e = 0; e < 8; ++e) {
                     const uint32_t mw = e < 4 ? in[jj].m.x : in[jj].m.y;
                     const uint32_t vw = e < 4 ? in[jj].v.x : in[jj].v.y;
-                    const float qm = float(int8_t(mw >> (8 * (e & 3))));
-                    const float qv = float((vw >> (8 * (e & 3))) & 0xFFu);
+                    float m0, v0;
+                    if constexpr (MAP == kMapLinear) {
+                        m0 = float(int8_t(mw >> (8 * (e & 3)))) * step_m;
+                        v0 = float((vw >> (8 * (e & 3))) & 0xFFu) * step_v;
+                    } else {
+                        m0 = tab.dm[(mw >> (8 * (e & 3))) & 0xFFu] * a_m;
+                        v0 = tab.dv[(vw >> (8 * (e & 3))) & 0xFFu] * a_v;
+                    }
                     const float gc = g[e] * coef;
-                    m1[8 * j + e] = __builtin_fmaf(s.beta1, qm * step_m, s.c1 * gc);
-                    v1[8 * j + e] = __builtin_fmaf(s.beta2, qv * step_v, s.c2 * (gc * gc));
+                    m1[8 * j + e] = __builtin_fmaf(s.beta1, m0, s.c1 * gc);
+                    v1[8 * j + e] = __builtin_fmaf(s.beta2, v0, s.c2 * (gc * gc));
                 }
             }
             // sqrt: the short correction sequence is exact unless some v1 of the
@@ -876,25 +1072,46 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                 amax_v = fmaxf(amax_v, red[buf][1][first + i]);
             }
         }
-        const float inv_m = 127.0f / amax_m;
-        const float inv_v = 255.0f / amax_v;
+        const float inv_m = (MAP == kMapLinear ? 127.0f : 1.0f) / amax_m;
+        const float inv_v = (MAP == kMapLinear ? 255.0f : 1.0f) / amax_v;
         const bool ok_m = isfinite(amax_m) && isfinite(inv_m);
         const bool ok_v = isfinite(amax_v) && isfinite(inv_v);
 
 #pragma unroll
         for (int j = 0; j < G; ++j) {
-            float qm[8], qv[8];
+            uint32_t pm0, pm1, pv0, pv1;
+            if constexpr (MAP == kMapLinear) {
+                float qm[8], qv[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                // clamp, then shift m codes by +128 (exact) so both pack as unsigned bytes
-                qm[e] = fminf(fmaxf(rintf(m1[8 * j + e] * inv_m), -127.0f), 127.0f) + 128.0f;
-                qv[e] = fminf(fmaxf(rintf(v1[8 * j + e] * inv_v), 0.0f), 255.0f);
+                for (int e = 0; e < 8; ++e) {
+                    // clamp, then shift m codes by +128 (exact) so both pack as unsigned bytes
+                    qm[e] = fminf(fmaxf(rintf(m1[8 * j + e] * inv_m), -127.0f), 127.0f) + 128.0f;
+                    qv[e] = fminf(fmaxf(rintf(v1[8 * j + e] * inv_v), 0.0f), 255.0f);
+                }
+                // m: undo the offset on all four bytes at once (two's complement int8)
+                pm0 = pack4(qm[0], qm[1], qm[2], qm[3]) ^ 0x80808080u;
+                pm1 = pack4(qm[4], qm[5], qm[6], qm[7]) ^ 0x80808080u;
+                pv0 = pack4(qv[0], qv[1], qv[2], qv[3]);
+                pv1 = pack4(qv[4], qv[5], qv[6], qv[7]);
+            } else {
+                uint32_t bm[8], bv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float m = m1[8 * j + e];
+                    const uint32_t c = dyn::encode<dyn::kBaseM, dyn::kTopM>(tab.em,
+                                                                           fabsf(m) * inv_m);
+                    bm[e] = c | (m < 0.0f ? 0x80u : 0u);
+                    bv[e] = dyn::encode<dyn::kBaseV, dyn::kTopV>(tab.ev, v1[8 * j + e] * inv_v);
+                }
+                pm0 = bm[0] | (bm[1] << 8) | (bm[2] << 16) | (bm[3] << 24);
+                pm1 = bm[4] | (bm[5] << 8) | (bm[6] << 16) | (bm[7] << 24);
+                pv0 = bv[0] | (bv[1] << 8) | (bv[2] << 16) | (bv[3] << 24);
+                pv1 = bv[4] | (bv[5] << 8) | (bv[6] << 16) | (bv[7] << 24);
             }
-            // m: undo the offset on all four bytes at once (two's complement int8)
-            const uint32_t pm0 = ok_m ? pack4(qm[0], qm[1], qm[2], qm[3]) ^ 0x80808080u : 0u;
-            const uint32_t pm1 = ok_m ? pack4(qm[4], qm[5], qm[6], qm[7]) ^ 0x80808080u : 0u;
-            const uint32_t pv0 = ok_v ? pack4(qv[0], qv[1], qv[2], qv[3]) : 0u;
-            const uint32_t pv1 = ok_v ? pack4(qv[4], qv[5], qv[6], qv[7]) : 0u;
+            if (!ok_m)
+                pm0 = pm1 = 0u;
+            if (!ok_v)
+                pv0 = pv1 = 0u;
             const int64_t ei = e0 + kGranule * (lane + 64 * j);
             if (full) {
                 *reinterpret_cast<uint2*>(d.mq + ei) = make_uint2(pm0, pm1);
@@ -1103,11 +1320,17 @@ lt_err launch_bf16_on_skip(const int64_t* unit_prefix, const Desc* desc, int n_t
 template <typename GT, int B>
 lt_err launch_step_b(const int64_t* prefix, const StepTensor* desc, int K, int64_t units,
                      const StepScalars& s, const float* coef, const int32_t* status, bool wb,
-                     hipStream_t stream)
+                     int map, hipStream_t stream)
 {
     // One workgroup takes four units at a time when each wave works alone.
-    const int64_t wg_units = StepGeom<B>::W > 1 ? units : (units + 3) / 4;
-    auto* kernel = wb ? k_adamw8_step<GT, B, true> : k_adamw8_step<GT, B, false>;
+    const int64_t wg_units = (map == kMapDynamic ? StepGeom<B, true>::W : StepGeom<B, false>::W) > 1
+                                 ? units
+                                 : (units + 3) / 4;
+    auto* kernel = map == kMapDynamic
+                       ? (wb ? k_adamw8_step<GT, B, true, kMapDynamic>
+                             : k_adamw8_step<GT, B, false, kMapDynamic>)
+                       : (wb ? k_adamw8_step<GT, B, true, kMapLinear>
+                             : k_adamw8_step<GT, B, false, kMapLinear>);
     int grid;
     if (lt_err e = grid_size(kernel, wg_units, &grid))
         return e;
@@ -1119,25 +1342,26 @@ lt_err launch_step_b(const int64_t* prefix, const StepTensor* desc, int K, int64
 template <typename GT>
 lt_err launch_step(int B, const int64_t* prefix, const StepTensor* desc, int K, int64_t tiles,
                    const StepScalars& s, const float* coef, const int32_t* status, bool wb,
-                   hipStream_t stream)
+                   int map, hipStream_t stream)
 {
     switch (B) {
-    case 64: return launch_step_b<GT, 64>(prefix, desc, K, tiles, s, coef, status, wb, stream);
-    case 128: return launch_step_b<GT, 128>(prefix, desc, K, tiles, s, coef, status, wb, stream);
-    case 256: return launch_step_b<GT, 256>(prefix, desc, K, tiles, s, coef, status, wb, stream);
-    case 512: return launch_step_b<GT, 512>(prefix, desc, K, tiles, s, coef, status, wb, stream);
-    case 1024: return launch_step_b<GT, 1024>(prefix, desc, K, tiles, s, coef, status, wb, stream);
-    case 2048: return launch_step_b<GT, 2048>(prefix, desc, K, tiles, s, coef, status, wb, stream);
-    case 4096: return launch_step_b<GT, 4096>(prefix, desc, K, tiles, s, coef, status, wb, stream);
-    case 8192: return launch_step_b<GT, 8192>(prefix, desc, K, tiles, s, coef, status, wb, stream);
+    case 64: return launch_step_b<GT, 64>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 128: return launch_step_b<GT, 128>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 256: return launch_step_b<GT, 256>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 512: return launch_step_b<GT, 512>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 1024: return launch_step_b<GT, 1024>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 2048: return launch_step_b<GT, 2048>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 4096: return launch_step_b<GT, 4096>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 8192: return launch_step_b<GT, 8192>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
     default: return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
     }
 }
 
-// Elements per work unit of the step kernel (StepGeom<B>::UNIT).
-int64_t step_unit_elems(int B)
+// Elements per work unit of the step kernel (StepGeom<B, map>::UNIT).
+int64_t step_unit_elems(int B, int map)
 {
-    const int64_t E = B >= 64 * kStepElemsPerLane ? kStepElemsPerLane : (B >= 512 ? B / 64 : 8);
+    const int64_t EM = step_elems_max(B, map == kMapDynamic);
+    const int64_t E = B >= 64 * EM ? EM : (B >= 512 ? B / 64 : 8);
     return B > 64 * E ? 4 * 64 * E : 64 * E;
 }
 
@@ -1490,7 +1714,7 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
                                 int8_t* const* m_codes, float* const* m_absmax,
                                 uint8_t* const* v_codes, float* const* v_absmax,
                                 uint16_t* const* params_bf16, const int64_t* numels,
-                                int n_tensors, int block_size, double lr,
+                                int n_tensors, int block_size, int code_map, double lr,
                                 double beta1, double beta2, double eps, double weight_decay,
                                 int64_t step, const float* coef, const int32_t* status,
                                 void* workspace, size_t workspace_bytes, void* stream)
@@ -1503,6 +1727,8 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
     if (!valid_block_size(block_size))
         return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
+    if (code_map != LT_MAP_LINEAR && code_map != LT_MAP_DYNAMIC)
+        return fail(LT_ERR_INVALID_ARG, "code_map must be LT_MAP_LINEAR or LT_MAP_DYNAMIC");
     if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step))
         return fail(LT_ERR_INVALID_ARG,
                     "need finite lr, weight_decay, eps >= 0, 0 <= beta1, beta2 < 1 and step >= 1");
@@ -1526,7 +1752,7 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
         return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
                                           std::to_string(lay.total) + " bytes");
 
-    const int64_t tile = step_unit_elems(block_size);
+    const int64_t tile = step_unit_elems(block_size, code_map);
     std::vector<uint8_t> host(lay.total, 0);
     auto* prefix = reinterpret_cast<int64_t*>(host.data() + lay.prefix);
     auto* desc = reinterpret_cast<StepTensor*>(host.data() + lay.desc);
@@ -1549,9 +1775,9 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
     const bool wb = any_set(params_bf16, K);
     if (lt_err e = grad_dtype == LT_DTYPE_BF16
                        ? launch_step<uint16_t>(block_size, d_prefix, d_desc, K, tiles, s, coef,
-                                               status, wb, st)
+                                               status, wb, code_map, st)
                        : launch_step<float>(block_size, d_prefix, d_desc, K, tiles, s, coef,
-                                            status, wb, st))
+                                            status, wb, code_map, st))
         return e;
     if (status && wb)
         return launch_bf16_on_skip(d_prefix, d_desc, K, tiles, tile, status, st);
@@ -1578,7 +1804,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                          float* const* v_absmax, uint16_t* const* params_bf16,
                                          const int64_t* numels,
                                          int n_tensors, const int* layer_first, int n_layers,
-                                         int block_size, double lr, double beta1, double beta2,
+                                         int block_size, int code_map, double lr, double beta1,
+                                         double beta2,
                                          double eps, double weight_decay, int64_t step,
                                          float max_norm, int norm_ready, int ring_slots,
                                          void* workspace,
@@ -1598,6 +1825,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
     if (!valid_block_size(B))
         return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
+    if (code_map != LT_MAP_LINEAR && code_map != LT_MAP_DYNAMIC)
+        return fail(LT_ERR_INVALID_ARG, "code_map must be LT_MAP_LINEAR or LT_MAP_DYNAMIC");
     if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step) || !(max_norm > 0.0f))
         return fail(LT_ERR_INVALID_ARG, "need finite lr, weight_decay, eps >= 0, 0 <= beta1, "
                                         "beta2 < 1, step >= 1 and max_norm > 0");
@@ -1620,7 +1849,7 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
 
     auto* ws = static_cast<uint8_t*>(workspace);
     auto slot_base = [&](int layer) { return ws + lay.slots + lay.slot_bytes * size_t(layer % S); };
-    const int64_t unit = step_unit_elems(B);
+    const int64_t unit = step_unit_elems(B, code_map);
 
     // Descriptors of every layer, each pointing into the slot the layer will use.
     std::vector<uint8_t> header(lay.header, 0);
@@ -1743,8 +1972,10 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         const int64_t units = reinterpret_cast<int64_t*>(header.data() + lay.st_prefix[i])[Ki];
         const bool wb = any_set(params_bf16 ? params_bf16 + layer_first[i] : nullptr, Ki);
         lt_err e = grad_dtype == LT_DTYPE_BF16
-                       ? launch_step<uint16_t>(B, up, dp, Ki, units, sc, coef, status, wb, cs)
-                       : launch_step<float>(B, up, dp, Ki, units, sc, coef, status, wb, cs);
+                       ? launch_step<uint16_t>(B, up, dp, Ki, units, sc, coef, status, wb,
+                                               code_map, cs)
+                       : launch_step<float>(B, up, dp, Ki, units, sc, coef, status, wb, code_map,
+                                            cs);
         if (e)
             return e;
         if (wb)

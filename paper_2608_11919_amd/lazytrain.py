@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(_HERE, "liblazytrain.so")
 LT_OK, LT_ERR_INVALID_ARG, LT_ERR_ALIGNMENT, LT_ERR_WORKSPACE, LT_ERR_HIP = range(5)
 LT_STATUS_OK, LT_STATUS_NONFINITE = 0, 1
 LT_DTYPE_F32, LT_DTYPE_BF16 = 0, 1
+LT_MAP_LINEAR, LT_MAP_DYNAMIC = 0, 1
 ERROR_NAMES = {1: "LT_ERR_INVALID_ARG", 2: "LT_ERR_ALIGNMENT", 3: "LT_ERR_WORKSPACE",
                4: "LT_ERR_HIP"}
 
@@ -63,7 +64,7 @@ def lib() -> ctypes.CDLL:
     L.lt_step_workspace_bytes.argtypes = [ctypes.c_int]
     L.lt_step_workspace_bytes.restype = ctypes.c_size_t
     L.lt_hybrid8bit_adamw_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, vpp,
-                                           i64p, ctypes.c_int, ctypes.c_int] + [
+                                           i64p, ctypes.c_int, ctypes.c_int, ctypes.c_int] + [
                                                ctypes.c_double] * 5 + [
                                                ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp]
     ip = ctypes.POINTER(ctypes.c_int)
@@ -72,7 +73,7 @@ def lib() -> ctypes.CDLL:
     L.lt_streamed_workspace_bytes.restype = ctypes.c_size_t
     L.lt_streamed_hybrid8bit_adamw_step.argtypes = [
         vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, vpp, i64p, ctypes.c_int, ip, ctypes.c_int,
-        ctypes.c_int] + [ctypes.c_double] * 5 + [ctypes.c_int64, ctypes.c_float, ctypes.c_int,
+        ctypes.c_int, ctypes.c_int] + [ctypes.c_double] * 5 + [ctypes.c_int64, ctypes.c_float, ctypes.c_int,
                                                  ctypes.c_int, vp, ctypes.c_size_t, vp, vp, vp,
                                                  vp, vp, vp, vp]
     L.lt_adamw_fp32_workspace_bytes.argtypes = [ctypes.c_int]
@@ -300,10 +301,10 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
                              coef: Optional[torch.Tensor] = None,
                              status: Optional[torch.Tensor] = None,
                              workspace: Optional[torch.Tensor] = None, stream=None,
-                             params_bf16=None) -> None:
+                             params_bf16=None, code_map: int = LT_MAP_LINEAR) -> None:
     """Steps a4-a10 in place on params, codes and absmax (see include/lazytrain.h);
     params_bf16 (optional, one bf16 tensor or None per parameter) receives the bf16
-    copy of the updated weights."""
+    copy of the updated weights; code_map selects the linear or dynamic codes."""
     k = len(params)
     if k == 0 or not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) ==
                       len(v_absmax) == k):
@@ -328,6 +329,7 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
     _check(lib().lt_hybrid8bit_adamw_step(
         _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
         _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, int(block_size),
+        int(code_map),
         float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
         _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
         ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
@@ -353,7 +355,8 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
                                       workspace: Optional[torch.Tensor] = None,
                                       compute_stream=None, h2d_stream=None,
                                       d2h_stream=None, params_bf16=None,
-                                      norm_ready: bool = False) -> None:
+                                      norm_ready: bool = False,
+                                      code_map: int = LT_MAP_LINEAR) -> None:
     """Step a11: host-resident tensors (CPU, ideally pinned) streamed layer by layer
     through HBM; scalar outputs are device tensors (see include/lazytrain.h).
     params_bf16 (optional, host bf16 tensors or None) receives the bf16 weight copy.
@@ -395,7 +398,8 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
     _check(lib().lt_streamed_hybrid8bit_adamw_step(
         _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
         _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, first,
-        len(layer_first) - 1, int(block_size), float(lr), float(beta1), float(beta2), float(eps),
+        len(layer_first) - 1, int(block_size), int(code_map), float(lr), float(beta1),
+        float(beta2), float(eps),
         float(weight_decay), int(step), float(max_norm), int(bool(norm_ready)), int(ring_slots),
         workspace.data_ptr(),
         workspace.numel() * workspace.element_size(),
@@ -479,13 +483,14 @@ class Hybrid8bitAdamW:
     def __init__(self, params: Sequence[torch.Tensor], lr: float = 1e-5,
                  betas=(0.9, 0.999), eps: float = 1e-8, weight_decay: float = 0.01,
                  max_norm: float = 1.0, block_size: int = 4096,
-                 slice_fraction: Optional[float] = None, bf16_copy: bool = False):
+                 slice_fraction: Optional[float] = None, bf16_copy: bool = False,
+                 code_map: int = LT_MAP_LINEAR):
         self.params = list(params)
         if not self.params:
             raise ValueError("no parameters")
         dev = self.params[0].device
         self.lr, self.betas, self.eps, self.weight_decay = lr, betas, eps, weight_decay
-        self.max_norm, self.block_size = max_norm, block_size
+        self.max_norm, self.block_size, self.code_map = max_norm, block_size, code_map
         if slice_fraction is None:
             self.is_8bit = [True] * len(self.params)
         else:
@@ -526,7 +531,7 @@ class Hybrid8bitAdamW:
                                      [grads[i] for i in self.idx8], self.m_codes, self.m_absmax,
                                      self.v_codes, self.v_absmax, self.block_size,
                                      params_bf16=None if wb is None else [wb[i] for i in self.idx8],
-                                     **hyper)
+                                     code_map=self.code_map, **hyper)
         if self.idx32:
             lt_adamw_fp32_step([self.params[i] for i in self.idx32],
                                [grads[i] for i in self.idx32], self.exp_avg, self.exp_avg_sq,

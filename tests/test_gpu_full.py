@@ -66,17 +66,17 @@ class Device:
             self.grads[k].copy_(self.stage_g[:n])
         torch.cuda.synchronize()
 
-    def step(self, t, clip=True, **over):
+    def step(self, t, clip=True, code_map=lt.LT_MAP_LINEAR, **over):
         h = dict(_hyper(self.w), **over)
         if clip:
             lt.lt_grad_sqnorm(self.grads, self.S, self.status, sq_per_tensor=self.sk)
             lt.lt_clip_coef(self.S, self.w.max_norm, self.coef, total_norm=self.norm)
             lt.lt_hybrid8bit_adamw_step(self.params, self.grads, self.mq, self.ma, self.vq,
                                         self.va, self.B, step=t, coef=self.coef,
-                                        status=self.status, **h)
+                                        status=self.status, code_map=code_map, **h)
         else:
             lt.lt_hybrid8bit_adamw_step(self.params, self.grads, self.mq, self.ma, self.vq,
-                                        self.va, self.B, step=t, **h)
+                                        self.va, self.B, step=t, code_map=code_map, **h)
         torch.cuda.synchronize()
 
     def read_blocks(self, blocks):
@@ -129,15 +129,19 @@ def _compare_blocks(got, want, what):
                                      f"positions (first {bad[:3]})")
 
 
-def _check_code_properties(dev):
+def _check_code_properties(dev, code_map=lt.LT_MAP_LINEAR):
     """At any size: a block with a positive stored absmax holds a code of magnitude
     127 (m) or 255 (v), since its largest element maps to full scale; a block with
-    absmax 0 holds only zero codes; every m code lies in [-127, 127]."""
+    absmax 0 holds only zero codes; every m code magnitude lies in [0, 127] (linear
+    codes are two's complement, dynamic codes sign-magnitude)."""
     B = dev.B
     for k, n in enumerate(dev.w.numels):
         nb_full = n // B
         for codes, absmax, top in ((dev.mq[k], dev.ma[k], 127), (dev.vq[k], dev.va[k], 255)):
-            c = codes.to(torch.int16).abs()
+            if code_map == lt.LT_MAP_DYNAMIC and top == 127:
+                c = codes.view(torch.uint8).to(torch.int16) & 0x7F
+            else:
+                c = codes.to(torch.int16).abs()
             assert int(c.max()) <= top
             if nb_full:
                 blk_max = c[:nb_full * B].view(nb_full, B).amax(dim=1)
@@ -146,17 +150,18 @@ def _check_code_properties(dev):
                 assert bool(torch.all(torch.isfinite(a)))
 
 
-def test_full_3b_model_step_parity():
+@pytest.mark.parametrize("code_map", [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC])
+def test_full_3b_model_step_parity(code_map):
     w = synth.full_3b()
     n_threads = synth.default_threads()
     B, K = w.block_size, len(w.shapes)
     _say(f"{w.name}: generating {w.n_params} params on the host and in HBM")
     dev = Device(w, n_threads)
     dev.load_grads(synth.STREAM_PRIOR_GRAD)
-    dev.step(1, clip=False, lr=0.0)  # 8-bit states from one prior step (weights unchanged)
+    dev.step(1, clip=False, code_map=code_map, lr=0.0)  # states from one prior step
     dev.load_grads(synth.grad_stream(w.step))
-    _say("GPU step at t = 2 (sum of squares, clip, fused step)")
-    dev.step(w.step)
+    _say(f"GPU step at t = 2 (sum of squares, clip, fused step), code map {code_map}")
+    dev.step(w.step, code_map=code_map)
     assert lt.lt_read_status(dev.status) == lt.LT_STATUS_OK
 
     _say("oracle sum of squares over all gradients")
@@ -182,12 +187,12 @@ def test_full_3b_model_step_parity():
     va = [np.zeros(1, np.float32) for _ in ws]
     h = _hyper(w)
     oracle.hybrid8bit_adamw_step(ws, g0s, mq, ma, vq, va, B, step=1, n_threads=n_threads,
-                                 **dict(h, lr=0.0))
+                                 code_map=code_map, **dict(h, lr=0.0))
     oracle.hybrid8bit_adamw_step(ws, gs, mq, ma, vq, va, B, step=w.step, coef=float(rcoef),
-                                 status=rst, n_threads=n_threads, **h)
+                                 status=rst, n_threads=n_threads, code_map=code_map, **h)
     _compare_blocks(dev.read_blocks(blocks), list(zip(ws, mq, ma, vq, va)), w.name)
     _say("sampled blocks bitwise equal; checking code properties of every block")
-    _check_code_properties(dev)
+    _check_code_properties(dev, code_map)
 
 
 def test_clip_stress_three_steps():
