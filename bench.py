@@ -167,25 +167,26 @@ def cpu_baseline(w, n_threads, target_s: float, code_map=0):
             "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
-COUNTERS = os.path.join(ROOT, "profiles", "adamw8_step_3b_full_counters.json")
-
-
 def counter_traffic(workload_name: str):
     """HBM bytes per launch of the fused step kernel from the committed rocprofv3
-    counter summary (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy of known
-    size).  None unless the summary covers this workload and the kernel source is the
-    one the counters were taken on."""
+    counter summaries (profiles/*_counters.json: FETCH_SIZE and WRITE_SIZE, each
+    scaled by a plain copy of known size).  None unless a summary covers this
+    workload and the kernel source is the one its counters were taken on."""
+    import glob
     import hashlib
-    try:
-        with open(COUNTERS) as f:
-            c = json.load(f)
-        with open(os.path.join(ROOT, c["source"]), "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
-    except (OSError, KeyError, ValueError):
-        return None
-    if sha != c.get("source_sha256") or workload_name != c.get("workload"):
-        return None
-    return c["kernels"]["k_adamw8_step"]["traffic_bytes"]
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_counters.json"))):
+        try:
+            with open(path) as f:
+                c = json.load(f)
+            if c.get("workload") != workload_name:
+                continue
+            with open(os.path.join(ROOT, c["source"]), "rb") as f:
+                sha = hashlib.sha256(f.read()).hexdigest()
+        except (OSError, KeyError, ValueError):
+            continue
+        if sha == c.get("source_sha256"):
+            return c["kernels"]["k_adamw8_step"]["traffic_bytes"]
+    return None
 
 
 def pcie_rates(dev, nbytes: int):
@@ -496,6 +497,9 @@ def main() -> int:
         f"{avg_step_s * 1e3:.3f} ms ({achieved:.0f} GB/s), norm pass {avg_norm_s * 1e3:.3f} ms "
         f"({nbytes / avg_norm_s / 1e9:.0f} GB/s)")
 
+    out_workload = (w.name + ("" if not idx32 else f"-hybrid-{args.slice_fraction:g}-8bit") +
+                    ("+bf16-copy" if args.bf16_copy else "") +
+                    ("+dynamic-map" if args.code_map == "dynamic" else ""))
     out = {
         "metric": METRIC,
         "value": w.n_params / (elapsed / args.steps),
@@ -510,10 +514,7 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "step_ms_events": {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9)},
-        "config": {"workload": w.name + ("" if not idx32 else
-                                         f"-hybrid-{args.slice_fraction:g}-8bit") +
-                   ("+bf16-copy" if args.bf16_copy else "") +
-                   ("+dynamic-map" if args.code_map == "dynamic" else ""),
+        "config": {"workload": out_workload,
                    "params": w.n_params, "tensors": K, "block_size": B,
                    "params_8bit": sum(w.numels[k] for k in idx8),
                    "grad_dtype": "bf16" if w.grad_dtype == synth.BF16 else "f32",
@@ -531,8 +532,7 @@ def main() -> int:
                      "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                     "traffic": counter_traffic(w.name)
-                     if not idx32 and not args.bf16_copy and args.code_map == "linear" else None,
+                     "traffic": counter_traffic(out_workload) if not idx32 else None,
                      "bytes_per_launch": kbytes},
         "status": st,
     }
