@@ -135,11 +135,11 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(w, n_threads, target_s: float, code_map=0):
+def cpu_baseline(w, n_threads, target_s: float, code_map=0, max_tensors=None):
     """The oracle as it stands, on a bounded sample of the same workload (whole
     tensors, decoder layers first, the embedding last), timed on this host's cores.
-    One decoder layer is timed first to size a sample of about target_s seconds;
-    the same layer is also timed on one thread."""
+    One decoder layer is timed first to size a sample of about target_s seconds (at
+    most max_tensors tensors); the same layer is also timed on one thread."""
     K = len(w.shapes)
     order = list(range(K))
     if len(w.shapes[0]) == 2 and w.shapes[0][0] > 100000:
@@ -151,7 +151,8 @@ def cpu_baseline(w, n_threads, target_s: float, code_map=0):
     dt1 = _oracle_pass(w, first, 1, code_map)
     ks, total = [], 0
     for k in order:
-        if ks and total + w.numels[k] > rate * target_s:
+        if ks and (total + w.numels[k] > rate * target_s or
+                   (max_tensors is not None and len(ks) >= max_tensors)):
             break
         ks.append(k)
         total += w.numels[k]
@@ -343,6 +344,13 @@ def run_streamed(args, w, dev, n_threads) -> int:
                  "frac_of_link_bound": round(bound / per, 4)},
         "status": st, "norm": float(norm.item()), "coef": float(coef.item()),
     }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample of 4 layers")
+        cb = cpu_baseline(w, n_threads, args.cpu_seconds,
+                          code_map=lt.LT_MAP_DYNAMIC if args.code_map == "dynamic"
+                          else lt.LT_MAP_LINEAR, max_tensors=4 * per_layer)
+        cb["extrapolated_step_s"] = round(n / cb["value"], 2)
+        out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
     return 0
 
@@ -386,8 +394,9 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(see DESIGN.md for how the step would shard)", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the step has no multi-GPU path (it would "
+              "shard by chunk-aligned block ranges, with one all-gather of the fp64 chunk "
+              "partials for the norm)", file=sys.stderr)
         return 2
 
     import torch
@@ -477,10 +486,14 @@ def main() -> int:
 
     norm_ms = [e[0].elapsed_time(e[1]) for e in events]
     step_ms = [e[1].elapsed_time(e[2]) for e in events]
-    whole_ms = sorted(e[0].elapsed_time(e[2]) for e in events)
+    whole_ms = [e[0].elapsed_time(e[2]) for e in events]
 
-    def pct(q):  # nearest-rank percentile of the per-step times
-        return round(whole_ms[min(len(whole_ms) - 1, max(0, math.ceil(q * len(whole_ms)) - 1))], 4)
+    def pct(xs, q):  # nearest-rank percentile
+        xs = sorted(xs)
+        return round(xs[min(len(xs) - 1, max(0, math.ceil(q * len(xs)) - 1))], 4)
+
+    def spread(xs):
+        return {"p10": pct(xs, 0.1), "median": pct(xs, 0.5), "p90": pct(xs, 0.9)}
 
     avg_step_s = sum(step_ms) / len(step_ms) * 1e-3
     avg_norm_s = sum(norm_ms) / len(norm_ms) * 1e-3
@@ -513,7 +526,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "step_ms_events": {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9)},
+        "step_ms_events": spread(whole_ms),
         "config": {"workload": out_workload,
                    "params": w.n_params, "tensors": K, "block_size": B,
                    "params_8bit": sum(w.numels[k] for k in idx8),
@@ -528,6 +541,7 @@ def main() -> int:
         "bytes_per_param": round(step_total_bytes / w.n_params, 4),
         "kernels_ms": {"norm_pass": round(avg_norm_s * 1e3, 4),
                        "adamw8_step": round(avg_step_s * 1e3, 4)},
+        "kernels_ms_spread": {"norm_pass": spread(norm_ms), "adamw8_step": spread(step_ms)},
         "roofline": {"kernel": "k_adamw8_step" if not idx32 else "k_adamw8_step + k_adamw32_step",
                      "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s",
