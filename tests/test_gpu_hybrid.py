@@ -75,3 +75,50 @@ def test_hybrid_optimizer_matches_oracle():
     for (wr, mr, vr), i, m, v in zip(ref32, opt.idx32, opt.exp_avg, opt.exp_avg_sq):
         assert to_host(params[i]).tobytes() == wr.tobytes()
         assert to_host(m).tobytes() == mr.tobytes() and to_host(v).tobytes() == vr.tobytes()
+
+
+def test_optimizer_dynamic_map_bf16_copy_and_a_skipped_step():
+    """The optimizer object with every option: a 30% 8-bit slice on the dynamic
+    code map, the bf16 weight copy, and a non-finite gradient at the third call,
+    which skips the step (weights, states and copies unchanged, step count kept)."""
+    rng = np.random.default_rng(45)
+    sizes = [40000, 300001, 5000, 123457, 2048, 7]
+    w0 = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
+    params = [to_dev(x) for x in w0]
+    opt = lt.Hybrid8bitAdamW(params, lr=1e-4, block_size=2048, slice_fraction=0.3,
+                             bf16_copy=True, code_map=lt.LT_MAP_DYNAMIC)
+    ref8 = State.zero_host([w0[i] for i in opt.idx8], 2048)
+    ref32 = [(w0[i].copy(), np.zeros_like(w0[i]), np.zeros_like(w0[i])) for i in opt.idx32]
+    t = 0
+    for call in range(4):
+        g = [f32_to_bf16_bits((rng.standard_t(3, size=n) * 1e-2).astype(np.float32))
+             for n in sizes]
+        if call == 2:
+            g[1][12345] = 0x7FC0  # NaN: this call is skipped
+        opt.step([to_dev(x) for x in g])
+        st_gpu = opt.last_status()
+        _, S, st = oracle.grad_sqnorm(g)
+        assert st_gpu == st
+        if st == lt.LT_STATUS_NONFINITE:
+            assert opt.step_count == t
+            continue
+        t += 1
+        assert opt.step_count == t
+        _, c = oracle.clip_coef(S, 1.0)
+        oracle.hybrid8bit_adamw_step(ref8.w, [g[i] for i in opt.idx8], ref8.mq, ref8.ma, ref8.vq,
+                                     ref8.va, 2048, step=t, coef=float(c), status=st,
+                                     n_threads=8, code_map=oracle.MAP_DYNAMIC,
+                                     **dict(HYPER, lr=1e-4))
+        for (wr, mr, vr), i in zip(ref32, opt.idx32):
+            oracle.adamw_fp32_step(wr, g[i], mr, vr, step=t, coef=float(c),
+                                   **dict(HYPER, lr=1e-4))
+    got8 = State([to_host(params[i]) for i in opt.idx8], [to_host(x) for x in opt.m_codes],
+                 [to_host(x) for x in opt.m_absmax], [to_host(x) for x in opt.v_codes],
+                 [to_host(x) for x in opt.v_absmax])
+    assert_state_equal(got8, ref8, "8-bit slice, dynamic map")
+    for (wr, mr, vr), i in zip(ref32, opt.idx32):
+        assert to_host(params[i]).tobytes() == wr.tobytes()
+    for k, i in enumerate(opt.idx8):
+        assert np.array_equal(to_host(opt.params_bf16[i]), oracle.round_bf16(ref8.w[k]))
+    for (wr, _, _), i in zip(ref32, opt.idx32):
+        assert np.array_equal(to_host(opt.params_bf16[i]), oracle.round_bf16(wr))
