@@ -168,24 +168,35 @@ def cpu_baseline(w, n_threads, target_s: float, code_map=0, max_tensors=None):
             "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
+def source_digest(path: str) -> str:
+    """SHA-256 of a C/HIP source with comments and blank lines dropped and runs of
+    whitespace folded, so that edits to comments keep recorded counters valid."""
+    import hashlib
+    import re
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    lines = [" ".join(line.split()) for line in text.splitlines()]
+    return hashlib.sha256("\n".join(x for x in lines if x).encode()).hexdigest()
+
+
 def counter_traffic(workload_name: str):
     """HBM bytes per launch of the fused step kernel from the committed rocprofv3
     counter summaries (profiles/*_counters.json: FETCH_SIZE and WRITE_SIZE, each
     scaled by a plain copy of known size).  None unless a summary covers this
     workload and the kernel source is the one its counters were taken on."""
     import glob
-    import hashlib
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_counters.json"))):
         try:
             with open(path) as f:
                 c = json.load(f)
             if c.get("workload") != workload_name:
                 continue
-            with open(os.path.join(ROOT, c["source"]), "rb") as f:
-                sha = hashlib.sha256(f.read()).hexdigest()
+            sha = source_digest(os.path.join(ROOT, c["source"]))
         except (OSError, KeyError, ValueError):
             continue
-        if sha == c.get("source_sha256"):
+        if sha == c.get("source_digest"):
             return c["kernels"]["k_adamw8_step"]["traffic_bytes"]
     return None
 

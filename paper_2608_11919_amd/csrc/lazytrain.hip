@@ -8,7 +8,14 @@
 //   k_sqnorm_finish  per-tensor fixed-order combine of the chunk sums.
 //   k_sqnorm_total   list-order global sum and the non-finite status.
 //   k_clip_coef      fp32(sqrt(S)) (fp64 root, then fp32) and the clip coefficient.
-//   k_adamw8_step    fused dequantize -> AdamW -> block absmax -> requantize.
+//   k_adamw8_step    fused dequantize -> AdamW -> block absmax -> requantize,
+//                    with the linear or the dynamic code map and an optional
+//                    bf16 copy of the updated weights.
+//   k_adamw32_step   the same update with fp32 moments (the hybrid operator's
+//                    non-8-bit part).
+//   k_bf16_on_skip   bf16 copies of unchanged weights after a skipped step.
+// Host side: the C ABI, descriptor uploads through a pinned staging ring, and
+// the layer-streamed step (a ring of device slots on three streams).
 // The reduction order and the fp32 operation order are fixed (see
 // include/lazytrain.h); every kernel's result is independent of its grid.
 
@@ -586,17 +593,19 @@ __global__ __launch_bounds__(64) void k_clip_coef(const double* __restrict__ sq_
 //
 // Geometry.  A lane owns E consecutive-granule slots (granule j of lane l is
 // elements 8*(l + 64*j) .. +7 of its wave's span), so each load instruction of
-// a wave covers one contiguous 1-2 KB run.  E = 32 for B >= 2048, B/64 for
-// B = 512, 1024 and 8 below.  For B <= 2048 a wave owns whole blocks and the
-// block absmax is a wave reduction; for B = 4096 and 8192, B/2048 waves of a
-// workgroup share a block and combine their maxima in LDS.
+// a wave covers one contiguous 1-2 KB run.  E = 32 for B >= 2048 (16 with the
+// dynamic map for B <= 4096), B/64 for B = 512, 1024 and 8 below.  When a block
+// is no longer than a wave's span, a wave owns whole blocks and the block
+// absmax is a wave reduction; otherwise B / (64 E) <= 4 waves of a workgroup
+// share a block and combine their maxima in LDS.
 
 // 32 elements per lane amortizes the per-block work (scales, maxima, the sqrt
 // ballot) over long contiguous runs; measured on the 3B-class step it beats 16
 // and 8 per lane.  The lane's granules are loaded and updated in kStepPhases
 // phases (when its granule count divides evenly), which bounds the registers the
-// loads occupy: about 150 VGPRs, three waves per SIMD.  One, two and four phases
-// time within 0.5% of each other; four is the fastest of them.
+// loads occupy: about 160 VGPRs, three waves per SIMD, against about 210 and two
+// waves with every load issued first.  One, two and four phases time within 0.5%
+// of each other; four is the fastest of them.
 constexpr int kStepElemsPerLane = 32;
 // With the dynamic code map the per-element work adds LDS table reads, whose
 // latency more waves hide better: 16 elements per lane (about 126 VGPRs, four
