@@ -39,3 +39,14 @@ def test_cpu_baseline_on_the_small_workload():
     assert cb["kind"] == "oracle" and cb["unit"] == "params/s" and cb["cores"] == 2
     assert cb["value"] > 0 and cb["single_thread"]["value"] > 0
     assert "of 4 tensors" in cb["sample"]
+
+
+def test_source_digest_ignores_comments_only(tmp_path):
+    a = tmp_path / "a.hip"
+    b = tmp_path / "b.hip"
+    c = tmp_path / "c.hip"
+    a.write_text("int f(int x) {\n  return x + 1;  // one\n}\n")
+    b.write_text("/* header */\nint f(int x)   {\n\n  return x + 1;\n}  // end\n")
+    c.write_text("int f(int x) {\n  return x + 2;\n}\n")
+    assert bench.source_digest(str(a)) == bench.source_digest(str(b))
+    assert bench.source_digest(str(a)) != bench.source_digest(str(c))
