@@ -54,3 +54,19 @@ def test_product_path_never_imports_the_oracle():
             if f.endswith((".py", ".hip", ".h", ".cpp")):
                 src = open(os.path.join(dirpath, f)).read()
                 assert "import oracle" not in src and "lazytrain_oracle" not in src, f
+
+
+def test_host_side_queries_of_the_next_rows():
+    import paper_2608_11919_amd as lt
+    assert lt.lt_grad_chunk_count([8192, 8193, 1]) == 4
+    L = lt.lib()
+    assert L.lt_grad_sqnorm_partials_workspace_bytes(0) == 0
+    assert L.lt_grad_sqnorm_partials_workspace_bytes(9) % 256 == 0
+    assert L.lt_grad_sqnorm_finish_workspace_bytes(325) >= 326 * 8 + 325 * 8
+    assert L.lt_adamw_fp32_workspace_bytes(4) >= 4 * 64
+    numels, first = [4096, 300001, 9, 2048], [0, 2, 4]
+    plain = lt.lt_streamed_workspace_bytes(numels, first, lt.LT_DTYPE_BF16, 2048, 3)
+    copy = lt.lt_streamed_workspace_bytes(numels, first, lt.LT_DTYPE_BF16, 2048, 3, True)
+    assert plain > 0 and copy > plain  # the bf16 copy needs room in every slot
+    assert lt.lt_streamed_workspace_bytes(numels, [0, 5], lt.LT_DTYPE_BF16, 2048, 3) == 0
+    assert lt.lt_streamed_workspace_bytes(numels, first, lt.LT_DTYPE_BF16, 2048, 1) == 0
