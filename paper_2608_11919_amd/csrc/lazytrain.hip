@@ -182,11 +182,17 @@ lt_err compute_units(int* cus)
     if (lt_err e = current_device(&dev))
         return e;
     DeviceState& ds = g_dev[dev];
-    if (ds.cu_count <= 0) {
-        int n = 0;
-        LT_HIP(hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev));
-        ds.cu_count = n > 0 ? n : 1;
+    {
+        std::lock_guard<std::mutex> lock(ds.mu);
+        if (ds.cu_count > 0) {
+            *cus = ds.cu_count;
+            return LT_OK;
+        }
     }
+    int n = 0;
+    LT_HIP(hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev));
+    std::lock_guard<std::mutex> lock(ds.mu);
+    ds.cu_count = n > 0 ? n : 1;
     *cus = ds.cu_count;
     return LT_OK;
 }
