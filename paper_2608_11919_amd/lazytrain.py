@@ -167,6 +167,9 @@ _workspaces = {}
 
 
 def _workspace(device, nbytes: int, workspace: Optional[torch.Tensor], stream) -> torch.Tensor:
+    """The caller's workspace, or one cached per (device, stream).  A cached workspace
+    is allocated on the stream that uses it, so that when a larger one replaces it
+    the caching allocator hands its memory out again only in that stream's order."""
     if workspace is not None:
         if workspace.device != device or workspace.numel() * workspace.element_size() < nbytes:
             raise ValueError(f"workspace must hold {nbytes} bytes on {device}")
@@ -174,7 +177,14 @@ def _workspace(device, nbytes: int, workspace: Optional[torch.Tensor], stream) -
     key = (device, _stream_handle(stream, device))
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
-        ws = torch.empty(max(nbytes, 4096), dtype=torch.uint8, device=device)
+        if stream is None:
+            s = torch.cuda.current_stream(device)
+        elif hasattr(stream, "cuda_stream"):
+            s = stream
+        else:
+            s = torch.cuda.ExternalStream(int(stream), device=device)
+        with torch.cuda.stream(s):
+            ws = torch.empty(max(nbytes, 4096), dtype=torch.uint8, device=device)
         _workspaces[key] = ws
     return ws
 
