@@ -400,6 +400,8 @@ def main() -> int:
     ap.add_argument("--slice-fraction", type=float, default=None,
                     help="hybrid operator: only this fraction of parameters keeps 8-bit states, "
                          "the rest fp32 states (the paper's run uses 0.02)")
+    ap.add_argument("--block-size", type=int, default=0,
+                    help="override the workload's quantization block size (the paper uses 4096)")
     ap.add_argument("--code-map", choices=["linear", "dynamic"], default="linear",
                     help="code map of the 8-bit moments")
     ap.add_argument("--bf16-copy", action="store_true",
@@ -433,6 +435,9 @@ def main() -> int:
     lt.lib()  # fails loudly when the HIP library is not built
     n_threads = synth.default_threads()
     w = getattr(synth, WORKLOADS[args.workload])()
+    if args.block_size:
+        import dataclasses
+        w = dataclasses.replace(w, block_size=args.block_size)
     K, B = len(w.shapes), w.block_size
     log(f"workload {w.name}: {K} tensors, {w.n_params} params, block {B}")
 
@@ -532,7 +537,8 @@ def main() -> int:
         f"{avg_step_s * 1e3:.3f} ms ({achieved:.0f} GB/s), norm pass {avg_norm_s * 1e3:.3f} ms "
         f"({nbytes / avg_norm_s / 1e9:.0f} GB/s)")
 
-    out_workload = (w.name + ("" if not idx32 else f"-hybrid-{args.slice_fraction:g}-8bit") +
+    out_workload = (w.name + (f"-block{B}" if args.block_size else "") +
+                    ("" if not idx32 else f"-hybrid-{args.slice_fraction:g}-8bit") +
                     ("+bf16-copy" if args.bf16_copy else "") +
                     ("+dynamic-map" if args.code_map == "dynamic" else ""))
     out = {
