@@ -558,3 +558,45 @@ class Hybrid8bitAdamW:
             self.step_count -= 1
         self._unchecked = False
         return st
+
+    def state_dict(self, stream=None) -> dict:
+        """The optimizer state for a checkpoint: the step count, the hyperparameters,
+        which tensors are 8-bit, and host copies of the codes, scales and fp32 moments
+        (the master weights are the caller's parameters).  Reads the last status first,
+        so the step count is exact."""
+        if self._unchecked:
+            self.last_status(stream)
+        host = lambda ts: [t.detach().cpu().clone() for t in ts]
+        return {
+            "step_count": self.step_count,
+            "hyper": {"lr": self.lr, "betas": tuple(self.betas), "eps": self.eps,
+                      "weight_decay": self.weight_decay, "max_norm": self.max_norm,
+                      "block_size": self.block_size, "code_map": self.code_map},
+            "is_8bit": list(self.is_8bit),
+            "m_codes": host(self.m_codes), "m_absmax": host(self.m_absmax),
+            "v_codes": host(self.v_codes), "v_absmax": host(self.v_absmax),
+            "exp_avg": host(self.exp_avg), "exp_avg_sq": host(self.exp_avg_sq),
+        }
+
+    def load_state_dict(self, state: dict) -> None:
+        """Restores a state_dict() into an optimizer built over parameters of the same
+        shapes with the same slice; the next step continues bitwise as if never
+        interrupted."""
+        if list(state["is_8bit"]) != list(self.is_8bit):
+            raise ValueError("the checkpoint's 8-bit slice differs from this optimizer's")
+        h = state["hyper"]
+        if h["block_size"] != self.block_size or h["code_map"] != self.code_map:
+            raise ValueError("the checkpoint's block size or code map differs")
+        self.lr, self.betas, self.eps = h["lr"], tuple(h["betas"]), h["eps"]
+        self.weight_decay, self.max_norm = h["weight_decay"], h["max_norm"]
+        for name in ("m_codes", "m_absmax", "v_codes", "v_absmax", "exp_avg", "exp_avg_sq"):
+            mine, saved = getattr(self, name), state[name]
+            if len(mine) != len(saved):
+                raise ValueError(f"{name}: {len(saved)} tensors in the checkpoint, "
+                                 f"{len(mine)} here")
+            for a, b in zip(mine, saved):
+                if a.shape != b.shape or a.dtype != b.dtype:
+                    raise ValueError(f"{name}: shape or dtype differs from the checkpoint")
+                a.copy_(b)
+        self.step_count = int(state["step_count"])
+        self._unchecked = False

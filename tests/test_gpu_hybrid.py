@@ -122,3 +122,39 @@ def test_optimizer_dynamic_map_bf16_copy_and_a_skipped_step():
         assert np.array_equal(to_host(opt.params_bf16[i]), oracle.round_bf16(ref8.w[k]))
     for (wr, _, _), i in zip(ref32, opt.idx32):
         assert np.array_equal(to_host(opt.params_bf16[i]), oracle.round_bf16(wr))
+
+
+@pytest.mark.parametrize("code_map", [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC])
+def test_checkpoint_resume_is_bitwise_uninterrupted(code_map, tmp_path):
+    """Step twice, save (weights and optimizer state through torch.save), restore into
+    a fresh optimizer and step twice more: bitwise the four uninterrupted steps."""
+    rng = np.random.default_rng(46)
+    sizes = [40000, 300001, 5000, 123457, 2048, 7]
+    w0 = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
+    grads = [[f32_to_bf16_bits((rng.standard_t(3, size=n) * 1e-2).astype(np.float32))
+              for n in sizes] for _ in range(4)]
+    kw = dict(lr=1e-4, block_size=2048, slice_fraction=0.3, code_map=code_map)
+
+    params = [to_dev(x) for x in w0]
+    opt = lt.Hybrid8bitAdamW(params, **kw)
+    for g in grads:
+        opt.step([to_dev(x) for x in g])
+    want = [to_host(p) for p in params]
+
+    params = [to_dev(x) for x in w0]
+    opt = lt.Hybrid8bitAdamW(params, **kw)
+    for g in grads[:2]:
+        opt.step([to_dev(x) for x in g])
+    path = tmp_path / "ckpt.pt"
+    torch.save({"params": [p.cpu() for p in params], "opt": opt.state_dict()}, path)
+    del opt, params
+    ck = torch.load(path, weights_only=True)
+    params = [p.to(DEV) for p in ck["params"]]
+    opt = lt.Hybrid8bitAdamW(params, **kw)
+    opt.load_state_dict(ck["opt"])
+    assert opt.step_count == 2
+    for g in grads[2:]:
+        opt.step([to_dev(x) for x in g])
+    assert opt.last_status() == lt.LT_STATUS_OK and opt.step_count == 4
+    for a, b in zip((to_host(p) for p in params), want):
+        assert a.tobytes() == b.tobytes()
