@@ -1,0 +1,43 @@
+// Drives the HIP library's host-only entry points and argument checks (no GPU
+// needed); built with AddressSanitizer and UndefinedBehaviorSanitizer by
+// tests/test_host_sanitizers.py.
+#include <cstdio>
+#include <cstdint>
+#include <cmath>
+#include <vector>
+#include "lazytrain.h"
+int main() {
+    int bad = 0;
+    // host-only entry points
+    std::vector<int64_t> numels = {5, 100, 7, 300001, 2048, 65536};
+    std::vector<uint8_t> is8(numels.size());
+    int64_t chosen = 0;
+    if (lt_select_8bit_slice(numels.data(), (int)numels.size(), 0.3, is8.data(), &chosen) != LT_OK) ++bad;
+    if (lt_select_8bit_slice(numels.data(), (int)numels.size(), 1.5, is8.data(), &chosen) == LT_OK) ++bad;
+    if (lt_grad_sqnorm_workspace_bytes(numels.data(), (int)numels.size()) == 0) ++bad;
+    if (lt_step_workspace_bytes(0) != 0 || lt_step_workspace_bytes(7) == 0) ++bad;
+    if (lt_grad_chunk_count(numels.data(), (int)numels.size()) != 1 + 1 + 1 + 37 + 1 + 8) ++bad;
+    int first[3] = {0, 3, 6};
+    for (int bf = 0; bf < 2; ++bf)
+        if (lt_streamed_workspace_bytes(numels.data(), 6, first, 2, LT_DTYPE_BF16, 2048, 3, bf) == 0) ++bad;
+    if (lt_adamw_fp32_workspace_bytes(6) == 0 || lt_grad_sqnorm_partials_workspace_bytes(6) == 0 ||
+        lt_grad_sqnorm_finish_workspace_bytes(6) == 0) ++bad;
+    // argument errors are reported before any device call
+    float* p[1] = {nullptr};
+    const void* g[1] = {nullptr};
+    int8_t* mq[1] = {nullptr}; uint8_t* vq[1] = {nullptr}; float* a[1] = {nullptr};
+    int64_t n1[1] = {16};
+    if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, 2048, LT_MAP_LINEAR,
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, 1000, LT_MAP_LINEAR,
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, 2048, 7,
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    if (lt_grad_sqnorm(g, n1, 1, 9, nullptr, 0, nullptr, nullptr, nullptr, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    if (lt_clip_coef(nullptr, 1.0f, nullptr, nullptr, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    if (lt_adamw_fp32_step(p, g, LT_DTYPE_F32, p, p, nullptr, n1, 1, NAN, 0.9, 0.999, 1e-8, 0.01, 1,
+                           nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    if (lt_last_error() == nullptr || lt_last_error()[0] == 0) ++bad;
+    printf("host checks: %d failures; last error: %s\n", bad, lt_last_error());
+    return bad != 0;
+}

@@ -1,11 +1,17 @@
-"""The oracle and the synthetic-input generator built with AddressSanitizer and
-UndefinedBehaviorSanitizer (host code only; gcc, no GPU) and driven through every
-entry point on ragged sizes, both gradient dtypes, both code maps, one and four
-threads, the non-finite skip and the zero block.  Any out-of-bounds access, leak
-or undefined operation fails the run."""
+"""Host code under AddressSanitizer and UndefinedBehaviorSanitizer, without a GPU.
+
+The oracle and the synthetic-input generator (gcc) are driven through every entry
+point on ragged sizes, both gradient dtypes, both code maps, one and four threads,
+the non-finite skip and the zero block.  The HIP library is rebuilt with the
+sanitizers on its host half only and driven through its host-only entry points and
+its argument checks (tests/sanitize_abi_driver.cpp).  Any out-of-bounds access,
+leak or undefined operation fails the run."""
+import glob
 import os
 import subprocess
 import tempfile
+
+import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -96,3 +102,32 @@ def test_oracle_and_generator_under_asan_and_ubsan():
         r = subprocess.run([exe], capture_output=True, text=True, timeout=600, env=env)
         assert r.returncode == 0, r.stdout[-3000:] + r.stderr[-3000:]
         assert "sanitized run ok" in r.stdout
+
+
+def _clang_rt_dir():
+    dirs = sorted(glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux"))
+    return dirs[-1] if dirs else None
+
+
+@pytest.mark.skipif(_clang_rt_dir() is None, reason="no clang sanitizer runtime")
+def test_library_host_code_under_asan_and_ubsan():
+    from paper_2608_11919_amd import build as lib_build
+    rt = _clang_rt_dir()
+    with tempfile.TemporaryDirectory() as d:
+        so = os.path.join(d, "liblazytrain_asan.so")
+        flags = [f for f in lib_build.HIPCC_FLAGS if f != "-O3"]
+        cmd = [lib_build.hipcc()] + flags + [
+            "-O1", "-g", "-Xarch_host", "-fsanitize=address", "-Xarch_host",
+            "-fsanitize=undefined", "-Xarch_host", "-shared-libsan",
+            "-I", os.path.join(ROOT, "include"), "-o", so] + lib_build.SOURCES
+        subprocess.run(cmd, check=True, capture_output=True)
+        exe = os.path.join(d, "drv")
+        clang = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "llvm", "bin", "clang++")
+        subprocess.run([clang, "-g", "-std=c++17", "-fsanitize=address,undefined",
+                        "-shared-libsan", "-I", os.path.join(ROOT, "include"), "-o", exe,
+                        os.path.join(ROOT, "tests", "sanitize_abi_driver.cpp"), so,
+                        f"-Wl,-rpath,{d}", f"-Wl,-rpath,{rt}"], check=True)
+        env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1", UBSAN_OPTIONS="print_stacktrace=1")
+        r = subprocess.run([exe], capture_output=True, text=True, timeout=300, env=env)
+        assert r.returncode == 0, r.stdout[-3000:] + r.stderr[-3000:]
+        assert "0 failures" in r.stdout
