@@ -524,6 +524,19 @@ class Hybrid8bitAdamW:
                             for p in self.params] if bf16_copy else None
         self.step_count = 0  # steps applied (skipped steps do not count)
         self._unchecked = False
+        # the status of the last step, copied to pinned host memory behind it on its
+        # stream, so reading it waits for that step only, not for later work
+        self._status_host = torch.zeros(1, dtype=torch.int32, pin_memory=True)
+        self._status_event = torch.cuda.Event()
+        self._status_pending = False
+
+    def _torch_stream(self, stream):
+        dev = self.params[0].device
+        if stream is None:
+            return torch.cuda.current_stream(dev)
+        if hasattr(stream, "cuda_stream"):
+            return stream
+        return torch.cuda.ExternalStream(int(stream), device=dev)
 
     def step(self, grads: Sequence[torch.Tensor], stream=None) -> None:
         if self._unchecked:
@@ -547,13 +560,22 @@ class Hybrid8bitAdamW:
                                [grads[i] for i in self.idx32], self.exp_avg, self.exp_avg_sq,
                                params_bf16=None if wb is None else [wb[i] for i in self.idx32],
                                **hyper)
+        s = self._torch_stream(stream)
+        with torch.cuda.stream(s):
+            self._status_host.copy_(self.status, non_blocking=True)
+        self._status_event.record(s)
+        self._status_pending = True
         self.step_count = t
         self._unchecked = True
 
     def last_status(self, stream=None) -> int:
-        """Reads the status of the last step (synchronizes the stream); a skipped step
-        is taken off the step count once."""
-        st = lt_read_status(self.status, stream)
+        """Reads the status of the last step, waiting for that step only (not for work
+        enqueued after it); a skipped step is taken off the step count once."""
+        if self._status_pending:
+            self._status_event.synchronize()
+            st = int(self._status_host[0])
+        else:
+            st = lt_read_status(self.status, stream)
         if self._unchecked and st == LT_STATUS_NONFINITE:
             self.step_count -= 1
         self._unchecked = False
