@@ -54,11 +54,11 @@ def sqnorm_cases():
         yield rec["name"], tensors, sk, s
 
 
-def adamw_examples():
+def adamw_examples(name: str = "adamw8_worked_examples.txt"):
     """Yields dicts with scalar hyperparameters and numpy arrays."""
     ints = {"m_codes": np.int8, "v_codes": np.uint8, "expect_m_codes": np.int8,
             "expect_v_codes": np.uint8}
-    for rec in _records("adamw8_worked_examples.txt", "example"):
+    for rec in _records(name, "example"):
         ex = {"name": rec["name"]}
         for key, toks in rec["_lines"]:
             if key in ("block_size", "t"):

@@ -140,3 +140,26 @@ def test_rejects_unknown_code_map():
     a = [torch.zeros(1, device=DEV)]
     with pytest.raises(lt.LazyTrainError):
         lt.lt_hybrid8bit_adamw_step(w, g, q, a, u, a, 2048, step=1, code_map=2, **HYPER)
+
+
+def test_hand_worked_dynamic_examples():
+    """The exact blocks of tests/golden/dynamic_map_worked_examples.txt through the
+    HIP path (each 4-element block is one partial block at the GPU's block size 64)."""
+    from golden_io import adamw_examples
+    n = 0
+    for ex in adamw_examples("dynamic_map_worked_examples.txt"):
+        st = State([ex["w"].copy()], [ex["m_codes"].copy()], [ex["m_absmax"].copy()],
+                   [ex["v_codes"].copy()], [ex["v_absmax"].copy()]).to_dev()
+        c = torch.tensor([ex["coef"]], dtype=torch.float32, device=DEV)
+        lt.lt_hybrid8bit_adamw_step(st.w, [to_dev(ex["grad"].copy())], st.mq, st.ma, st.vq,
+                                    st.va, 64, step=ex["t"], coef=c, code_map=DYN,
+                                    lr=ex["lr"], beta1=ex["beta1"], beta2=ex["beta2"],
+                                    eps=ex["eps"], weight_decay=ex["weight_decay"])
+        got = st.to_host()
+        assert np.array_equal(got.w[0], ex["expect_w"]), ex["name"]
+        assert np.array_equal(got.mq[0], ex["expect_m_codes"]), ex["name"]
+        assert np.array_equal(got.vq[0], ex["expect_v_codes"]), ex["name"]
+        assert got.ma[0][0] == ex["expect_m_absmax"][0], ex["name"]
+        assert got.va[0][0] == ex["expect_v_absmax"][0], ex["name"]
+        n += 1
+    assert n == 2

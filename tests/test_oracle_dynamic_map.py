@@ -195,3 +195,26 @@ def test_dynamic_map_removes_the_small_v_hazard():
         print(f"step {t}: drift/lr max {drift.max():.3g}, hazard fraction {hazard.mean():.4f}")
         assert hazard.mean() < 0.01
         assert drift.max() < 1.0
+
+
+@pytest.mark.parametrize("as_bf16", [False, True])
+def test_hand_worked_dynamic_examples(as_bf16):
+    from golden_io import adamw_examples, f32_to_bf16_bits
+    n = 0
+    for ex in adamw_examples("dynamic_map_worked_examples.txt"):
+        g = f32_to_bf16_bits(ex["grad"]) if as_bf16 else ex["grad"]
+        w, qm, qv = ex["w"].copy(), ex["m_codes"].copy(), ex["v_codes"].copy()
+        am, av = ex["m_absmax"].copy(), ex["v_absmax"].copy()
+        oracle.hybrid8bit_adamw_step([w], [g], [qm], [am], [qv], [av], ex["block_size"],
+                                     lr=ex["lr"], beta1=ex["beta1"], beta2=ex["beta2"],
+                                     eps=ex["eps"], weight_decay=ex["weight_decay"],
+                                     step=ex["t"], coef=ex["coef"],
+                                     code_map=oracle.MAP_DYNAMIC)
+        name = ex["name"]
+        assert np.array_equal(w, ex["expect_w"]), (name, w)
+        assert np.array_equal(qm, ex["expect_m_codes"]), (name, qm)
+        assert np.array_equal(am, ex["expect_m_absmax"]), (name, am)
+        assert np.array_equal(qv, ex["expect_v_codes"]), (name, qv)
+        assert np.array_equal(av, ex["expect_v_absmax"]), (name, av)
+        n += 1
+    assert n == 2
