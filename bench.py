@@ -377,6 +377,22 @@ def run_streamed(args, w, dev, n_threads) -> int:
     return 0
 
 
+def stream_ceiling(n_elements: int):
+    """Runs the data-movement probe (paper_2608_11919_amd/stream_ceiling, built with
+    the library) in a child process: the step's 8 B read + 6 B write per element and
+    the norm's 2 B read per element, with no arithmetic, at this workload's size."""
+    import subprocess
+    exe = os.path.join(ROOT, "paper_2608_11919_amd", "stream_ceiling")
+    if not os.path.exists(exe):
+        log("stream_ceiling is not built; no ceiling reported")
+        return None
+    r = subprocess.run([exe, str(n_elements), "3"], capture_output=True, text=True, timeout=300)
+    if r.returncode != 0:
+        log(f"stream_ceiling failed ({r.returncode}): {r.stderr.strip()[-200:]}")
+        return None
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
 def copy_probe(dev, nbytes: int, reps: int):
     """A plain copy kernel of known size, for scaling the HBM byte counters."""
     import torch
@@ -413,6 +429,8 @@ def main() -> int:
     ap.add_argument("--host-layers", type=int, default=8,
                     help="streamed workload: distinct pinned host layers the model cycles over")
     ap.add_argument("--ring-slots", type=int, default=3, help="streamed workload: device slots")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the data-movement ceiling probe")
     ap.add_argument("--copy-probe-bytes", type=int, default=0,
                     help="also run a plain copy of this many bytes (counter scaling)")
     args = ap.parse_args()
@@ -578,6 +596,18 @@ def main() -> int:
                      "bytes_per_launch": kbytes},
         "status": st,
     }
+    if not args.no_ceiling and not idx32 and not args.bf16_copy and gb == 2:
+        log("measuring the data-movement ceiling of the same byte pattern")
+        c = stream_ceiling(w.n_params)
+        if c is not None:
+            out["ceiling"] = {
+                "probe": "stream_ceiling: the step's 8 B read + 6 B written and the norm's 2 B "
+                         "read per element, no arithmetic, same array layout and size",
+                "mix_gbps": c["mix_gbps"], "read_gbps": c["read_gbps"],
+                "step_kernel_frac_of_mix": round(achieved / c["mix_gbps"], 4),
+                "norm_pass_frac_of_read": round(nbytes / avg_norm_s / 1e9 / c["read_gbps"], 4),
+                "whole_step_ceiling_ms": round(
+                    (c["mix_ms"] * kbytes / c["mix_bytes"]) + c["read_ms"] * nbytes / c["read_bytes"], 4)}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(w, n_threads, args.cpu_seconds, code_map)

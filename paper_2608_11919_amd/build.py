@@ -27,6 +27,10 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
+CEILING = os.path.join(HERE, "stream_ceiling")
+CEILING_SOURCE = os.path.join(HERE, "csrc", "stream_ceiling.hip")
+
+
 def build(verbose: bool = False, extra_flags=()) -> str:
     cmd = [hipcc()] + HIPCC_FLAGS + list(extra_flags) + [
         "-I", os.path.join(ROOT, "include"), "-o", LIB + ".tmp"] + SOURCES
@@ -34,7 +38,19 @@ def build(verbose: bool = False, extra_flags=()) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(LIB + ".tmp", LIB)
+    build_ceiling_probe(verbose)
     return LIB
+
+
+def build_ceiling_probe(verbose: bool = False) -> str:
+    """The data-movement probe bench.py runs beside the step (an executable)."""
+    flags = [f for f in HIPCC_FLAGS if f not in ("-fPIC", "-shared")]
+    cmd = [hipcc()] + flags + ["-o", CEILING + ".tmp", CEILING_SOURCE]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(CEILING + ".tmp", CEILING)
+    return CEILING
 
 
 if __name__ == "__main__":
