@@ -196,7 +196,7 @@ size_t lt_step_workspace_bytes(int n_tensors);
  *            executor, which moves parameters to the GPU for every layer
  *            (Sec. 3.1; parameter H2D traffic in Sec. 3.4).  After the call it
  *            holds bf16(w1), rounded to nearest even (a NaN becomes a quiet
- *            NaN of the same sign), written by the step kernel from registers
+ *            NaN), written by the step kernel from registers
  *            (+2 B/param); after a skipped step, bf16 of the unchanged weights.
  * The tensors of one call must not overlap.
  */
