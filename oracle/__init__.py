@@ -18,7 +18,9 @@ STATUS_OK, STATUS_NONFINITE = 0, 1
 CHUNK = 8192
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liblazytrain_oracle.so")
+# LTO_LIBRARY names another build of the same source (the tests build copies
+# with one planted mistake each and check that the pins reject them).
+_LIB_PATH = os.environ.get("LTO_LIBRARY") or os.path.join(_HERE, "liblazytrain_oracle.so")
 _lib = None
 
 _i64p = ctypes.POINTER(ctypes.c_int64)
@@ -35,6 +37,8 @@ def _load():
     if _lib is not None:
         return _lib
     if not os.path.exists(_LIB_PATH):
+        if os.environ.get("LTO_LIBRARY"):
+            raise FileNotFoundError(f"LTO_LIBRARY names a missing file: {_LIB_PATH}")
         from . import build as _build  # building the checker is not using the product
 
         _build.build()

@@ -11,15 +11,19 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "liblazytrain_oracle.so")
 
 
-def build(verbose: bool = False) -> str:
-    src = os.path.join(HERE, "lazytrain_oracle.c")
+SOURCE = os.path.join(HERE, "lazytrain_oracle.c")
+
+
+def build(verbose: bool = False, src: str = SOURCE, out: str = LIB) -> str:
+    """Compiles ``src`` (default: the oracle) into the shared library ``out``;
+    the header is taken from this directory."""
     cmd = ["gcc", "-std=c11", "-O2", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
-           "-fopenmp", "-Wall", "-Wextra", "-o", LIB + ".tmp", src, "-lm"]
+           "-fopenmp", "-Wall", "-Wextra", "-I", HERE, "-o", out + ".tmp", src, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    os.replace(out + ".tmp", out)
+    return out
 
 
 if __name__ == "__main__":

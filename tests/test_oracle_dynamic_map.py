@@ -7,13 +7,15 @@ decade tops are the powers of ten, each decade holds 2^p codes at a constant
 spacing 0.9 * 10^-zeros / 2^p starting one spacing above 0.1 * 10^-zeros, the
 magnitudes rise strictly, and the top code is exactly 1.  The quantizer is
 checked against exact rational nearest-code search, the round trip of code
-values, the half-gap error bound, the zero-block rule and sign handling."""
+values, the half-gap error bound, exact ties, the zero-block rule and sign handling."""
+import bisect
 from fractions import Fraction
 
 import numpy as np
 import pytest
 
 import oracle
+from exact_fp import round_to_f32
 
 
 def _decades(bits):
@@ -85,6 +87,74 @@ def test_quantizer_against_exact_nearest(signed):
             d_want = abs(Fraction(float(a[i])) - Fraction(float(t[want])))
             assert abs(int(c[i]) - want) == 1
             assert d_got - d_want <= Fraction(float(np.spacing(np.float32(a[i])))), i
+
+
+@pytest.mark.parametrize("signed", [True, False])
+def test_exact_midpoints_take_the_smaller_code(signed):
+    """Where the midpoint of two neighbouring magnitudes is itself an fp32 value,
+    its two distances are the same real number, so they round alike: an exact
+    tie, resolved to the smaller code (the smaller magnitude)."""
+    t = oracle.dynamic_map(signed)
+    mids, lower = [], []
+    for c in range(t.size - 1):
+        mid = (Fraction(float(t[c])) + Fraction(float(t[c + 1]))) / 2
+        if Fraction(round_to_f32(mid)) == mid:
+            mids.append(float(mid))
+            lower.append(c)
+    assert len(mids) >= 20
+    x = np.array([1.0] + mids, dtype=np.float32)  # absmax 1: normalized value = value
+    if signed:
+        q, A = oracle.quantize_dynamic_signed(-x)
+        assert np.all(q.view(np.uint8)[1:] & 0x80)
+        c = (q.view(np.uint8) & 0x7F)[1:]
+    else:
+        q, A = oracle.quantize_dynamic_unsigned(x)
+        c = q[1:]
+    assert A == 1.0
+    assert c.tolist() == lower
+
+
+def _reading_code(t_exact, A, x):
+    """The code of x in a block of absmax A under the fp32 reading, in exact
+    arithmetic: a = fp32(|x| * fp32(1 / A)), distances fp32(|a - t_c|), the
+    smallest code among the least distances."""
+    inv = Fraction(round_to_f32(1 / Fraction(A)))
+    a = Fraction(round_to_f32(abs(Fraction(x)) * inv))
+    # Rounding is monotone, so a code beyond a's neighbours on either side never
+    # has a smaller rounded distance than the neighbour on that side; the code
+    # gaps exceed an ulp of any distance, so it cannot tie with it either.
+    k = bisect.bisect_left(t_exact, a)
+    lo, hi = max(0, k - 2), min(len(t_exact), k + 2)
+    d = [round_to_f32(abs(a - tc)) for tc in t_exact[lo:hi]]
+    return lo + d.index(min(d))
+
+
+@pytest.mark.parametrize("signed", [True, False])
+def test_codes_follow_the_fp32_reading_exactly(signed):
+    """Blocks whose scale has an inexact reciprocal, with values placed within a
+    few ulps of the midpoints between codes, where the normalization's rounding
+    decides the code: every code equals the exact evaluation of the reading."""
+    rng = np.random.default_rng(41 + signed)
+    t = oracle.dynamic_map(signed)
+    t_exact = [Fraction(float(v)) for v in t]
+    for A in (np.float32(0.7), np.float32(3.0e-3), np.float32(1.9e-7)):
+        FA = Fraction(float(A))
+        c = rng.integers(1, t.size - 1, size=150)
+        mids = [(t_exact[i] + t_exact[i + 1]) / 2 * FA for i in c.tolist()]
+        x = np.array([round_to_f32(m) for m in mids], dtype=np.float32)
+        ulps = rng.integers(-3, 4, size=x.size).astype(np.int32)
+        x = (x.view(np.int32) + ulps).view(np.float32)
+        x = np.concatenate([[A], x, (rng.uniform(0, 1, 100) * A).astype(np.float32)])
+        x = np.minimum(x, A).astype(np.float32)
+        if signed:
+            q, got_A = oracle.quantize_dynamic_signed(-x)
+            codes = (q.view(np.uint8) & 0x7F).tolist()
+        else:
+            q, got_A = oracle.quantize_dynamic_unsigned(x)
+            codes = q.tolist()
+        assert got_A == A
+        want = [_reading_code(t_exact, float(A), float(v)) for v in x.tolist()]
+        assert codes == want, A
 
 
 @pytest.mark.parametrize("signed", [True, False])

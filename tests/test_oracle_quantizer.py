@@ -4,9 +4,10 @@ this implementation's reading).
 
 Pins: the round trip is within half a code step; codes are idempotent; +-A map
 to +-127 and A to 255; zero and non-representable scales give a zero block;
-odd symmetry and monotonicity; and the codes equal the exactly rounded rational
-q = round_half_even(x * 127 / A) except at ties of the rational value, where
-they may differ by one code.
+odd symmetry and monotonicity; exact ties round to even; the code step is the
+once-rounded quotient A/127 (A/255); and the codes equal the exactly rounded
+rational q = round_half_even(x * 127 / A) except near ties of the rational
+value, where the fp32 product may land on the other side.
 """
 from fractions import Fraction
 
@@ -14,6 +15,7 @@ import numpy as np
 import pytest
 
 import oracle
+from exact_fp import round_half_even, round_to_f32
 
 
 def _blocks(rng, n, scale):
@@ -96,12 +98,40 @@ def test_odd_symmetry_and_monotone():
     assert np.all(np.diff(qv.astype(np.int32)) >= 0)
 
 
-def _round_half_even(fr: Fraction) -> int:
-    fl = fr.numerator // fr.denominator
-    rem = fr - fl
-    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
-        return fl + 1
-    return fl
+def test_exact_ties_round_to_even():
+    """With A = 127 (A = 255) the code scale is exactly 1, so x * inv = x and a
+    half-integer x is an exact tie of the rational code value: round half to even."""
+    x = np.array([127.0, 2.5, 0.5, -1.5, 3.5, -0.5, 126.5, -125.5], dtype=np.float32)
+    q, A = oracle.quantize_signed(x)
+    assert A == 127.0
+    assert q.tolist() == [127, 2, 0, -2, 4, 0, 126, -126]
+    v = np.array([255.0, 2.5, 0.5, 1.5, 254.5, 127.5], dtype=np.float32)
+    qv, Av = oracle.quantize_unsigned(v)
+    assert Av == 255.0
+    assert qv.tolist() == [255, 2, 0, 2, 254, 128]
+
+
+def test_code_step_is_the_correctly_rounded_quotient():
+    """Code 1 dequantizes to fp32(A / 127) (fp32(A / 255)), the quotient rounded once,
+    and code q to fp32(q * that step): checked with exact rationals over scales
+    from subnormal to near the top of the fp32 range."""
+    rng = np.random.default_rng(31)
+    scales = np.concatenate([
+        (rng.uniform(1, 2, 400) * 2.0 ** rng.integers(-149, 127, 400)).astype(np.float32),
+        np.array([1.0, 127.0, 255.0, 1e-45, 3.4e38, 1.1754944e-38], np.float32)])
+    one = np.array([1], np.int8)
+    qs = np.array([1, -7, 64, 127], np.int8)
+    for A in scales.tolist():
+        FA = Fraction(A)
+        step_m = round_to_f32(FA / 127)
+        assert float(oracle.dequantize_signed(one, A)[0]) == step_m, A
+        got = oracle.dequantize_signed(qs, A).tolist()
+        assert got == [round_to_f32(int(q) * Fraction(step_m)) for q in qs.tolist()], A
+        step_v = round_to_f32(FA / 255)
+        assert float(oracle.dequantize_unsigned(one.view(np.uint8), A)[0]) == step_v, A
+
+
+_round_half_even = round_half_even
 
 
 def test_codes_match_exact_rational_rounding_except_at_ties():
