@@ -14,7 +14,11 @@
  *    current HIP device, owned by the caller.  The library never frees them
  *    and keeps no reference after the work it enqueued has run.
  *  - Lists (arrays of pointers and numels) are HOST arrays of length
- *    n_tensors, read during the call only.
+ *    n_tensors, read during the call only.  n_tensors may be 0 (the lists may
+ *    then be NULL) and a numel may be 0: an empty tensor contributes nothing
+ *    (its sum of squares is 0, its step writes nothing) and its pointers are
+ *    neither checked nor dereferenced.  The streamed step needs at least one
+ *    tensor per layer; those may be empty too.
  *  - All work is enqueued on `stream` (a hipStream_t; NULL is the default
  *    stream) in call order.  No call synchronizes the host unless its name
  *    says so (lt_read_status).
@@ -42,7 +46,7 @@ extern "C" {
 
 typedef enum lt_err {
     LT_OK = 0,
-    LT_ERR_INVALID_ARG = 1, /* NULL pointer, size < 1, unsupported block size or dtype, bad hyperparameter */
+    LT_ERR_INVALID_ARG = 1, /* NULL pointer, negative size, unsupported block size or dtype, bad hyperparameter */
     LT_ERR_ALIGNMENT = 2,   /* a base pointer is not aligned as stated above */
     LT_ERR_WORKSPACE = 3,   /* workspace NULL, misaligned or smaller than the size query returns */
     LT_ERR_HIP = 4          /* a HIP runtime call failed (device query, copy, launch, sync) */
@@ -65,8 +69,9 @@ typedef enum lt_code_map {
 } lt_code_map;
 
 /* Bytes of device workspace lt_grad_sqnorm needs for this list (descriptors,
- * one fp64 partial per 8192-element chunk, one fp64 per tensor).  Returns 0 if
- * n_tensors < 1, numels is NULL or a numel is < 1. */
+ * one fp64 partial per 8192-element chunk, one fp64 per tensor); never 0 for a
+ * valid list.  Returns 0 if n_tensors < 0, numels is NULL for n_tensors > 0 or
+ * a numel is < 0. */
 size_t lt_grad_sqnorm_workspace_bytes(const int64_t* numels, int n_tensors);
 
 /*
@@ -76,7 +81,8 @@ size_t lt_grad_sqnorm_workspace_bytes(const int64_t* numels, int n_tensors);
  *                  LT_DTYPE_BF16), read only.
  *   sq_per_tensor  device double[n_tensors] or NULL: S_k, the sum of squares
  *                  of tensor k.
- *   sq_total       device double: S = S_0 + S_1 + ... in list order.
+ *   sq_total       device double: S = S_0 + S_1 + ... in list order (0 for
+ *                  an empty list).
  *   status         device int32: LT_STATUS_NONFINITE if S is NaN or
  *                  infinite, else LT_STATUS_OK.
  * Accumulation is fp64 in a fixed order: each tensor is cut into 8192-element
@@ -116,6 +122,7 @@ size_t lt_grad_sqnorm_partials_workspace_bytes(int n_tensors);
  *   partials  device double[lt_grad_chunk_count(numels, n_tensors)]: the slice
  *             of the model-wide partials array that starts at these tensors'
  *             first chunk (the chunk count of the model's earlier tensors).
+ *             Not touched (and may be NULL) when the count is 0.
  * The parts of a model may arrive in any order, on any streams; once all are
  * written, lt_grad_sqnorm_finish gives bitwise the result of lt_grad_sqnorm
  * over the whole list.
@@ -132,7 +139,8 @@ size_t lt_grad_sqnorm_finish_workspace_bytes(int n_tensors);
  * exactly as lt_grad_sqnorm computes them (same accumulators, same trees).
  *   numels    host int64[n_tensors]: the whole model's tensor sizes.
  *   partials  device double[lt_grad_chunk_count(numels, n_tensors)], every
- *             entry written by lt_grad_sqnorm_partials.
+ *             entry written by lt_grad_sqnorm_partials (may be NULL when the
+ *             count is 0).
  *   sq_per_tensor (may be NULL), sq_total, status: as in lt_grad_sqnorm.
  */
 lt_err lt_grad_sqnorm_finish(const int64_t* numels, int n_tensors, const double* partials,
@@ -140,7 +148,7 @@ lt_err lt_grad_sqnorm_finish(const int64_t* numels, int n_tensors, const double*
                              double* sq_total, int32_t* status, void* stream);
 
 /* Bytes of device workspace lt_hybrid8bit_adamw_step needs for n_tensors
- * tensors (the uploaded descriptor table).  0 if n_tensors < 1. */
+ * tensors (the uploaded descriptor table).  0 if n_tensors < 0. */
 size_t lt_step_workspace_bytes(int n_tensors);
 
 /*

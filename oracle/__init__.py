@@ -107,8 +107,8 @@ def _numels(arrays):
 
 def grad_sqnorm(grads, n_threads: int = 1):
     """Returns (S_k as float64 array, S, status) in the fixed reduction order."""
-    gdt = _gdt(grads[0])
-    _contig(grads, grads[0].dtype)
+    gdt = _gdt(grads[0]) if grads else F32
+    _contig(grads, grads[0].dtype if grads else np.float32)
     sk = np.zeros(max(1, len(grads)), dtype=np.float64)
     s = ctypes.c_double()
     st = ctypes.c_int32()
@@ -122,7 +122,7 @@ def grad_sqnorm(grads, n_threads: int = 1):
 
 def grad_sqnorm_naive(grads) -> float:
     return _load().lto_grad_sqnorm_naive(_ptrs(grads), _numels(grads), len(grads),
-                                         _gdt(grads[0]))
+                                         _gdt(grads[0]) if grads else F32)
 
 
 def clip_coef(sq_total: float, max_norm: float):

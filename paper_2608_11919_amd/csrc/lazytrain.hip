@@ -26,6 +26,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -1323,6 +1324,8 @@ lt_err launch_bf16_on_skip(const int64_t* unit_prefix, const Desc* desc, int n_t
                            int64_t n_units, int64_t unit_elems, const int32_t* status,
                            hipStream_t st)
 {
+    if (n_units == 0)
+        return LT_OK;
     const int grid = int(std::min<int64_t>((n_units + 3) / 4, 1024));
     k_bf16_on_skip<Desc><<<grid, kThreads, 0, st>>>(unit_prefix, desc, n_tensors, n_units,
                                                     unit_elems, status);
@@ -1388,12 +1391,26 @@ int64_t sq_chunks_of(const int64_t* numels, int K)
     return C;
 }
 
+// A tensor list: n_tensors >= 0 sizes, each >= 0; numels may be NULL only for
+// an empty list.  A tensor with no elements contributes nothing: its pointers
+// are neither checked nor dereferenced.
 bool valid_list(const int64_t* numels, int K)
 {
-    if (K < 1 || !numels)
+    if (K < 0 || (K > 0 && !numels))
         return false;
     for (int k = 0; k < K; ++k)
-        if (numels[k] < 1)
+        if (numels[k] < 0)
+            return false;
+    return true;
+}
+
+// The host lists of a call: each may be NULL only when the list is empty.
+bool lists_given(int K, std::initializer_list<const void*> lists)
+{
+    if (K == 0)
+        return true;
+    for (const void* l : lists)
+        if (!l)
             return false;
     return true;
 }
@@ -1428,6 +1445,8 @@ StepScalars make_scalars(double lr, double beta1, double beta2, double eps, doub
 lt_err launch_sq_chunks(int gdt, const int64_t* prefix, const uint64_t* ptrs, const int64_t* numels,
                         int K, int64_t C, double* partials, hipStream_t st)
 {
+    if (C == 0)
+        return LT_OK;  // no chunks: every tensor of the list is empty
     const int64_t iters = (C + kSqChunksPerIter - 1) / kSqChunksPerIter;
     int grid;
     if (gdt == LT_DTYPE_BF16) {
@@ -1559,8 +1578,8 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
                       double* sq_per_tensor, double* sq_total, int32_t* status, void* stream)
 {
     g_last_error.clear();
-    if (!grads || !valid_list(numels, n_tensors))
-        return fail(LT_ERR_INVALID_ARG, "grads/numels must hold n_tensors >= 1 entries with numel >= 1");
+    if (!valid_list(numels, n_tensors) || !lists_given(n_tensors, {grads}))
+        return fail(LT_ERR_INVALID_ARG, "grads/numels must hold n_tensors >= 0 entries with numel >= 0");
     if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
     if (!sq_total || !status)
@@ -1568,6 +1587,8 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
     if (!aligned(sq_total, 8) || !aligned(status, 4) || (sq_per_tensor && !aligned(sq_per_tensor, 8)))
         return fail(LT_ERR_ALIGNMENT, "scalar outputs must be naturally aligned");
     for (int k = 0; k < n_tensors; ++k) {
+        if (numels[k] == 0)
+            continue;
         if (!grads[k])
             return fail(LT_ERR_INVALID_ARG, "grads[" + std::to_string(k) + "] is NULL");
         if (!aligned(grads[k], 16))
@@ -1602,8 +1623,10 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
 
     if (lt_err e = launch_sq_chunks(grad_dtype, d_prefix, d_ptrs, d_numels, K, C, d_partials, st))
         return e;
-    k_sqnorm_finish<<<K, kThreads, 0, st>>>(d_prefix, d_partials, d_sk);
-    LT_HIP(hipGetLastError());
+    if (K > 0) {
+        k_sqnorm_finish<<<K, kThreads, 0, st>>>(d_prefix, d_partials, d_sk);
+        LT_HIP(hipGetLastError());
+    }
     k_sqnorm_total<<<1, 256, 0, st>>>(d_sk, K, sq_per_tensor, sq_total, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
@@ -1632,7 +1655,7 @@ int64_t lt_grad_chunk_count(const int64_t* numels, int n_tensors)
 
 size_t lt_grad_sqnorm_partials_workspace_bytes(int n_tensors)
 {
-    return n_tensors < 1 ? 0 : round_up(sq_layout(n_tensors, 0).header_bytes, 256);
+    return n_tensors < 0 ? 0 : round_up(sq_layout(n_tensors, 0).header_bytes, 256);
 }
 
 lt_err lt_grad_sqnorm_partials(const void* const* grads, const int64_t* numels, int n_tensors,
@@ -1640,15 +1663,20 @@ lt_err lt_grad_sqnorm_partials(const void* const* grads, const int64_t* numels, 
                                size_t workspace_bytes, void* stream)
 {
     g_last_error.clear();
-    if (!grads || !valid_list(numels, n_tensors))
-        return fail(LT_ERR_INVALID_ARG, "grads/numels must hold n_tensors >= 1 entries with numel >= 1");
+    if (!valid_list(numels, n_tensors) || !lists_given(n_tensors, {grads}))
+        return fail(LT_ERR_INVALID_ARG, "grads/numels must hold n_tensors >= 0 entries with numel >= 0");
     if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
+    const int64_t n_chunks = sq_chunks_of(numels, n_tensors);
+    if (n_chunks == 0)
+        return LT_OK;  // nothing to sum: partials is not touched
     if (!partials)
         return fail(LT_ERR_INVALID_ARG, "partials must not be NULL");
     if (!aligned(partials, 8))
         return fail(LT_ERR_ALIGNMENT, "partials must be 8-byte aligned");
     for (int k = 0; k < n_tensors; ++k) {
+        if (numels[k] == 0)
+            continue;
         if (!grads[k])
             return fail(LT_ERR_INVALID_ARG, "grads[" + std::to_string(k) + "] is NULL");
         if (!aligned(grads[k], 16))
@@ -1683,7 +1711,7 @@ lt_err lt_grad_sqnorm_partials(const void* const* grads, const int64_t* numels, 
 // Finish workspace: [chunk prefix K+1] | [S_k K]
 size_t lt_grad_sqnorm_finish_workspace_bytes(int n_tensors)
 {
-    return n_tensors < 1 ? 0
+    return n_tensors < 0 ? 0
                          : round_up(sizeof(int64_t) * (n_tensors + 1), 256) +
                                round_up(sizeof(double) * n_tensors, 256);
 }
@@ -1694,8 +1722,9 @@ lt_err lt_grad_sqnorm_finish(const int64_t* numels, int n_tensors, const double*
 {
     g_last_error.clear();
     if (!valid_list(numels, n_tensors))
-        return fail(LT_ERR_INVALID_ARG, "numels must hold n_tensors >= 1 entries >= 1");
-    if (!partials || !sq_total || !status)
+        return fail(LT_ERR_INVALID_ARG, "numels must hold n_tensors >= 0 entries >= 0");
+    const bool no_chunks = sq_chunks_of(numels, n_tensors) == 0;  // partials is then not read
+    if ((!partials && !no_chunks) || !sq_total || !status)
         return fail(LT_ERR_INVALID_ARG, "partials, sq_total and status must not be NULL");
     if (!aligned(partials, 8) || !aligned(sq_total, 8) || !aligned(status, 4) ||
         (sq_per_tensor && !aligned(sq_per_tensor, 8)))
@@ -1713,8 +1742,11 @@ lt_err lt_grad_sqnorm_finish(const int64_t* numels, int n_tensors, const double*
     if (lt_err e = upload(prefix.data(), sizeof(int64_t) * (K + 1), ws, st))
         return e;
     auto* d_sk = reinterpret_cast<double*>(ws + round_up(sizeof(int64_t) * (K + 1), 256));
-    k_sqnorm_finish<<<K, kThreads, 0, st>>>(reinterpret_cast<const int64_t*>(ws), partials, d_sk);
-    LT_HIP(hipGetLastError());
+    if (K > 0) {
+        k_sqnorm_finish<<<K, kThreads, 0, st>>>(reinterpret_cast<const int64_t*>(ws), partials,
+                                                d_sk);
+        LT_HIP(hipGetLastError());
+    }
     k_sqnorm_total<<<1, 256, 0, st>>>(d_sk, K, sq_per_tensor, sq_total, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
@@ -1722,7 +1754,7 @@ lt_err lt_grad_sqnorm_finish(const int64_t* numels, int n_tensors, const double*
 
 size_t lt_step_workspace_bytes(int n_tensors)
 {
-    return n_tensors < 1 ? 0 : step_layout(n_tensors).total;
+    return n_tensors < 0 ? 0 : step_layout(n_tensors).total;
 }
 
 lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int grad_dtype,
@@ -1735,9 +1767,9 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
                                 void* workspace, size_t workspace_bytes, void* stream)
 {
     g_last_error.clear();
-    if (!params || !grads || !m_codes || !m_absmax || !v_codes || !v_absmax ||
-        !valid_list(numels, n_tensors))
-        return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 1 entries with numel >= 1");
+    if (!valid_list(numels, n_tensors) ||
+        !lists_given(n_tensors, {params, grads, m_codes, m_absmax, v_codes, v_absmax}))
+        return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 0 entries with numel >= 0");
     if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
     if (!valid_block_size(block_size))
@@ -1751,6 +1783,8 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
         return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned");
     const int K = n_tensors;
     for (int k = 0; k < K; ++k) {
+        if (numels[k] == 0)
+            continue;
         const std::string at = "[" + std::to_string(k) + "]";
         if (!params[k] || !grads[k] || !m_codes[k] || !m_absmax[k] || !v_codes[k] || !v_absmax[k])
             return fail(LT_ERR_INVALID_ARG, "NULL tensor pointer at index " + at);
@@ -1778,6 +1812,8 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
                              numels[k], params_bf16 ? params_bf16[k] : nullptr};
     }
     const int64_t tiles = prefix[K];
+    if (tiles == 0)
+        return LT_OK;  // every tensor is empty
 
     const StepScalars s = make_scalars(lr, beta1, beta2, eps, weight_decay, step);
 
@@ -1830,9 +1866,9 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
 {
     g_last_error.clear();
     const int K = n_tensors, L = n_layers, S = ring_slots, B = block_size;
-    if (!params || !grads || !m_codes || !m_absmax || !v_codes || !v_absmax ||
-        !valid_list(numels, K))
-        return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 1 entries with numel >= 1");
+    if (K < 1 || !valid_list(numels, K) ||
+        !lists_given(K, {params, grads, m_codes, m_absmax, v_codes, v_absmax}))
+        return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 1 entries with numel >= 0");
     if (!valid_layers(layer_first, L, K))
         return fail(LT_ERR_INVALID_ARG,
                     "layer_first must rise strictly from 0 to n_tensors over n_layers + 1 entries");
@@ -1853,7 +1889,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         (total_norm && !aligned(total_norm, 4)))
         return fail(LT_ERR_ALIGNMENT, "scalar outputs must be naturally aligned");
     for (int k = 0; k < K; ++k)
-        if (!params[k] || !grads[k] || !m_codes[k] || !m_absmax[k] || !v_codes[k] || !v_absmax[k])
+        if (numels[k] > 0 &&
+            (!params[k] || !grads[k] || !m_codes[k] || !m_absmax[k] || !v_codes[k] || !v_absmax[k]))
             return fail(LT_ERR_INVALID_ARG, "NULL host pointer at index " + std::to_string(k));
     const int gbytes = grad_dtype == LT_DTYPE_BF16 ? 2 : 4;
     const bool bf16_copy = params_bf16 != nullptr;
@@ -1937,8 +1974,9 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
             LT_HIP(hipStreamWaitEvent(hs, ev.freed[sl], 0));
         uint8_t* base = slot_base(i);
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j)
-            LT_HIP(hipMemcpyAsync(base + places[i][j].g, grads[k], size_t(numels[k]) * gbytes, H2D,
-                                  hs));
+            if (numels[k] > 0)
+                LT_HIP(hipMemcpyAsync(base + places[i][j].g, grads[k], size_t(numels[k]) * gbytes,
+                                      H2D, hs));
         LT_HIP(hipEventRecord(ev.in[sl], hs));
         LT_HIP(hipStreamWaitEvent(cs, ev.in[sl], 0));
         const int Ki = layer_first[i + 1] - layer_first[i];
@@ -1972,6 +2010,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
             const SlotTensor& t = places[i][j];
             const size_t n = size_t(numels[k]), nb = size_t((numels[k] + B - 1) / B);
+            if (n == 0)
+                continue;
             LT_HIP(hipMemcpyAsync(base + t.w, params[k], n * 4, H2D, hs));
             LT_HIP(hipMemcpyAsync(base + t.g, grads[k], n * gbytes, H2D, hs));
             LT_HIP(hipMemcpyAsync(base + t.mq, m_codes[k], n, H2D, hs));
@@ -1986,7 +2026,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         const auto* dp = reinterpret_cast<const StepTensor*>(ws + lay.st_desc[i]);
         const int64_t units = reinterpret_cast<int64_t*>(header.data() + lay.st_prefix[i])[Ki];
         const bool wb = any_set(params_bf16 ? params_bf16 + layer_first[i] : nullptr, Ki);
-        lt_err e = grad_dtype == LT_DTYPE_BF16
+        lt_err e = units == 0 ? LT_OK
+                   : grad_dtype == LT_DTYPE_BF16
                        ? launch_step<uint16_t>(B, up, dp, Ki, units, sc, coef, status, wb,
                                                code_map, cs)
                        : launch_step<float>(B, up, dp, Ki, units, sc, coef, status, wb, code_map,
@@ -2001,6 +2042,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
             const SlotTensor& t = places[i][j];
             const size_t n = size_t(numels[k]), nb = size_t((numels[k] + B - 1) / B);
+            if (n == 0)
+                continue;
             LT_HIP(hipMemcpyAsync(params[k], base + t.w, n * 4, D2H, ds));
             LT_HIP(hipMemcpyAsync(m_codes[k], base + t.mq, n, D2H, ds));
             LT_HIP(hipMemcpyAsync(v_codes[k], base + t.vq, n, D2H, ds));
@@ -2020,7 +2063,7 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
 
 size_t lt_adamw_fp32_workspace_bytes(int n_tensors)
 {
-    return n_tensors < 1 ? 0 : round_up(round_up(sizeof(int64_t) * (n_tensors + 1), 64) +
+    return n_tensors < 0 ? 0 : round_up(round_up(sizeof(int64_t) * (n_tensors + 1), 64) +
                                             sizeof(Fp32Tensor) * size_t(n_tensors), 256);
 }
 
@@ -2033,8 +2076,8 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
 {
     g_last_error.clear();
     const int K = n_tensors;
-    if (!params || !grads || !exp_avg || !exp_avg_sq || !valid_list(numels, K))
-        return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 1 entries with numel >= 1");
+    if (!valid_list(numels, K) || !lists_given(K, {params, grads, exp_avg, exp_avg_sq}))
+        return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 0 entries with numel >= 0");
     if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
     if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step))
@@ -2043,6 +2086,8 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
     if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)))
         return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned");
     for (int k = 0; k < K; ++k) {
+        if (numels[k] == 0)
+            continue;
         if (!params[k] || !grads[k] || !exp_avg[k] || !exp_avg_sq[k])
             return fail(LT_ERR_INVALID_ARG, "NULL tensor pointer at index " + std::to_string(k));
         if (!aligned(params[k], 16) || !aligned(grads[k], 16) || !aligned(exp_avg[k], 16) ||
@@ -2070,6 +2115,8 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
                              {0, 0}};
     }
     const int64_t units = prefix[K];
+    if (units == 0)
+        return LT_OK;  // every tensor is empty
     const StepScalars sc = make_scalars(lr, beta1, beta2, eps, weight_decay, step);
     auto* ws = static_cast<uint8_t*>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -2095,8 +2142,9 @@ lt_err lt_select_8bit_slice(const int64_t* numels, int n_tensors, double fractio
                             uint8_t* is_8bit, int64_t* n_8bit_params)
 {
     g_last_error.clear();
-    if (!valid_list(numels, n_tensors) || !is_8bit || !(fraction >= 0.0 && fraction <= 1.0))
-        return fail(LT_ERR_INVALID_ARG, "need n_tensors >= 1 numels >= 1, is_8bit and 0 <= fraction <= 1");
+    if (!valid_list(numels, n_tensors) || !lists_given(n_tensors, {is_8bit}) ||
+        !(fraction >= 0.0 && fraction <= 1.0))
+        return fail(LT_ERR_INVALID_ARG, "need n_tensors >= 0 numels >= 0, is_8bit and 0 <= fraction <= 1");
     int64_t total = 0;
     for (int k = 0; k < n_tensors; ++k)
         total += numels[k];

@@ -116,6 +116,8 @@ def _numel_array(tensors) -> ctypes.Array:
 
 
 def _grad_dtype(grads) -> int:
+    if not grads:
+        return LT_DTYPE_F32  # an empty list reads nothing
     dt = grads[0].dtype
     if any(g.dtype != dt for g in grads):
         raise TypeError("all gradients must share one dtype")
@@ -124,6 +126,14 @@ def _grad_dtype(grads) -> int:
     if dt in (torch.bfloat16, torch.int16, torch.uint16):
         return LT_DTYPE_BF16
     raise TypeError(f"gradient dtype must be float32 or bfloat16, got {dt}")
+
+
+def _device_of(tensors, *others):
+    """The device of a tensor list: its first tensor's, else that of the first
+    given scalar tensor, else the current HIP device (an empty list)."""
+    for t in list(tensors) + [o for o in others if o is not None]:
+        return t.device
+    return torch.device("cuda", torch.cuda.current_device())
 
 
 def _check_tensors(tensors, device, dtype=None, what="tensor"):
@@ -204,10 +214,8 @@ def lt_grad_sqnorm(grads: Sequence[torch.Tensor], sq_total: torch.Tensor, status
                    sq_per_tensor: Optional[torch.Tensor] = None,
                    workspace: Optional[torch.Tensor] = None, stream=None) -> None:
     """Steps a1-a2: S_k, S and the non-finite status into device tensors (float64,
-    float64[1], int32[1])."""
-    if not grads:
-        raise ValueError("empty gradient list")
-    device = grads[0].device
+    float64[1], int32[1]).  An empty list, and empty tensors, sum to 0."""
+    device = sq_total.device
     _check_tensors(grads, device, what="grads")
     gdt = _grad_dtype(grads)
     if sq_per_tensor is not None and sq_per_tensor.numel() < len(grads):
@@ -242,9 +250,7 @@ def lt_grad_sqnorm_partials(grads: Sequence[torch.Tensor], partials: torch.Tenso
     """a1 on part of a model as its gradients arrive: chunk partials into
     ``partials``, a float64 device view of the model-wide array starting at these
     tensors' first chunk (see include/lazytrain.h)."""
-    if not grads:
-        raise ValueError("empty gradient list")
-    device = grads[0].device
+    device = partials.device
     _check_tensors(grads, device, what="grads")
     gdt = _grad_dtype(grads)
     need = lt_grad_chunk_count([g.numel() for g in grads])
@@ -316,10 +322,9 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
     params_bf16 (optional, one bf16 tensor or None per parameter) receives the bf16
     copy of the updated weights; code_map selects the linear or dynamic codes."""
     k = len(params)
-    if k == 0 or not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) ==
-                      len(v_absmax) == k):
-        raise ValueError("tensor lists must be non-empty and of equal length")
-    device = params[0].device
+    if not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) == len(v_absmax) == k):
+        raise ValueError("tensor lists must be of equal length")
+    device = _device_of(params, coef, status)
     _check_tensors(params, device, torch.float32, "params")
     _check_tensors(grads, device, what="grads")
     _check_tensors(m_codes, device, torch.int8, "m_codes")
@@ -433,9 +438,9 @@ def lt_adamw_fp32_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Ten
     """fp32-state AdamW, in place on params, exp_avg and exp_avg_sq (device tensors);
     params_bf16 as in lt_hybrid8bit_adamw_step."""
     k = len(params)
-    if k == 0 or not (len(grads) == len(exp_avg) == len(exp_avg_sq) == k):
-        raise ValueError("tensor lists must be non-empty and of equal length")
-    device = params[0].device
+    if not (len(grads) == len(exp_avg) == len(exp_avg_sq) == k):
+        raise ValueError("tensor lists must be of equal length")
+    device = _device_of(params, coef, status)
     _check_tensors(params, device, torch.float32, "params")
     _check_tensors(grads, device, what="grads")
     _check_tensors(exp_avg, device, torch.float32, "exp_avg")

@@ -15,7 +15,8 @@ int main() {
     if (lt_select_8bit_slice(numels.data(), (int)numels.size(), 0.3, is8.data(), &chosen) != LT_OK) ++bad;
     if (lt_select_8bit_slice(numels.data(), (int)numels.size(), 1.5, is8.data(), &chosen) == LT_OK) ++bad;
     if (lt_grad_sqnorm_workspace_bytes(numels.data(), (int)numels.size()) == 0) ++bad;
-    if (lt_step_workspace_bytes(0) != 0 || lt_step_workspace_bytes(7) == 0) ++bad;
+    if (lt_step_workspace_bytes(-1) != 0 || lt_step_workspace_bytes(0) == 0 ||
+        lt_step_workspace_bytes(7) == 0) ++bad;
     if (lt_grad_chunk_count(numels.data(), (int)numels.size()) != 1 + 1 + 1 + 37 + 1 + 8) ++bad;
     int first[3] = {0, 3, 6};
     for (int bf = 0; bf < 2; ++bf)
@@ -37,6 +38,28 @@ int main() {
     if (lt_clip_coef(nullptr, 1.0f, nullptr, nullptr, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_adamw_fp32_step(p, g, LT_DTYPE_F32, p, p, nullptr, n1, 1, NAN, 0.9, 0.999, 1e-8, 0.01, 1,
                            nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    // empty lists and zero-element tensors: validated, then nothing to launch
+    alignas(256) static uint8_t host_ws[4096];
+    if (lt_select_8bit_slice(nullptr, 0, 0.5, nullptr, &chosen) != LT_OK || chosen != 0) ++bad;
+    if (lt_hybrid8bit_adamw_step(nullptr, nullptr, LT_DTYPE_BF16, nullptr, nullptr, nullptr, nullptr,
+                                 nullptr, nullptr, 0, 2048, LT_MAP_LINEAR, 1e-4, 0.9, 0.999, 1e-8,
+                                 0.01, 1, nullptr, nullptr, host_ws, sizeof host_ws, nullptr) != LT_OK) ++bad;
+    int64_t n0[2] = {0, 0};
+    if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n0, 1, 2048, LT_MAP_DYNAMIC,
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, host_ws,
+                                 sizeof host_ws, nullptr) != LT_OK) ++bad;
+    if (lt_adamw_fp32_step(nullptr, nullptr, LT_DTYPE_F32, nullptr, nullptr, nullptr, nullptr, 0, 1e-4,
+                           0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, host_ws, sizeof host_ws,
+                           nullptr) != LT_OK) ++bad;
+    const void* g2[2] = {nullptr, nullptr};  // pointers of empty tensors are not read
+    if (lt_grad_sqnorm_partials(g2, n0, 2, LT_DTYPE_BF16, nullptr, nullptr, 0, nullptr) != LT_OK) ++bad;
+    if (lt_grad_sqnorm_partials(nullptr, n0, 2, LT_DTYPE_BF16, nullptr, nullptr, 0, nullptr) !=
+        LT_ERR_INVALID_ARG) ++bad;  // a NULL list of two tensors
+    int64_t nneg[1] = {-1};
+    if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, nneg, 1, 2048, LT_MAP_LINEAR,
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, host_ws,
+                                 sizeof host_ws, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    if (lt_grad_chunk_count(n0, 2) != 0 || lt_grad_sqnorm_workspace_bytes(nullptr, 0) == 0) ++bad;
     if (lt_last_error() == nullptr || lt_last_error()[0] == 0) ++bad;
     printf("host checks: %d failures; last error: %s\n", bad, lt_last_error());
     return bad != 0;

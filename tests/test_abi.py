@@ -34,9 +34,13 @@ def test_oracle_library_exports_every_declared_symbol():
 
 def test_workspace_size_queries():
     import paper_2608_11919_amd as lt
-    assert lt.lt_step_workspace_bytes(0) == 0
+    assert lt.lt_step_workspace_bytes(-1) == 0  # invalid
+    assert lt.lt_step_workspace_bytes(0) > 0    # an empty list is valid: 0 means invalid
     assert lt.lt_step_workspace_bytes(325) >= 325 * 64
-    assert lt.lt_grad_sqnorm_workspace_bytes([0]) == 0
+    assert lt.lt_grad_sqnorm_workspace_bytes([-1]) == 0
+    assert lt.lt_grad_sqnorm_workspace_bytes([]) > 0
+    assert lt.lt_grad_sqnorm_workspace_bytes([0, 0]) > 0
+    assert lt.lib().lt_grad_sqnorm_workspace_bytes(None, 2) == 0  # numels NULL, n_tensors > 0
     small = lt.lt_grad_sqnorm_workspace_bytes([8192])
     big = lt.lt_grad_sqnorm_workspace_bytes([8192 * 1000 + 1])
     assert big - small >= 1000 * 8 - 256 and big % 256 == 0
@@ -60,7 +64,12 @@ def test_host_side_queries_of_the_next_rows():
     import paper_2608_11919_amd as lt
     assert lt.lt_grad_chunk_count([8192, 8193, 1]) == 4
     L = lt.lib()
-    assert L.lt_grad_sqnorm_partials_workspace_bytes(0) == 0
+    assert L.lt_grad_sqnorm_partials_workspace_bytes(-1) == 0
+    assert L.lt_grad_sqnorm_partials_workspace_bytes(0) > 0
+    assert L.lt_adamw_fp32_workspace_bytes(-1) == 0 and L.lt_adamw_fp32_workspace_bytes(0) > 0
+    assert lt.lt_grad_chunk_count([0, 8193, 0]) == 2
+    assert lt.lt_select_8bit_slice([], 0.5) == ([], 0)
+    assert lt.lt_select_8bit_slice([0, 100, 0, 10], 0.1) == ([True, False, True, True], 10)
     assert L.lt_grad_sqnorm_partials_workspace_bytes(9) % 256 == 0
     assert L.lt_grad_sqnorm_finish_workspace_bytes(325) >= 326 * 8 + 325 * 8
     assert L.lt_adamw_fp32_workspace_bytes(4) >= 4 * 64

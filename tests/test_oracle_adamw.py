@@ -357,3 +357,23 @@ def test_fp32_state_adamw_matches_torch(case):
     terms = step_size * (b1 * np.abs(m0.astype(np.float64)) + (1 - b1) * np.abs(gc)) / denom
     d = np.abs(wo.astype(np.float64) - wt)
     assert np.all(d <= 5e-7 * (terms + np.abs(w) + np.abs(wt)) + 1e-37)
+
+
+def test_empty_tensors_are_not_stepped():
+    # a zero-element tensor has no blocks: the others step exactly as without it
+    block = 256
+    probs = [_random_problem(40 + i, n) for i, n in enumerate((300, 4096))]
+    full = [[p[0].copy() for p in probs], [p[1] for p in probs]] + \
+        [[p[2][j].copy() for p in probs] for j in range(4)]
+    oracle.hybrid8bit_adamw_step(*full, block, coef=0.7, **KW)
+    e32, e8, eu8 = np.zeros(0, np.float32), np.zeros(0, np.int8), np.zeros(0, np.uint8)
+    eg = np.zeros(0, probs[0][1].dtype)
+    mixed = [[e32, probs[0][0].copy(), e32, probs[1][0].copy()],
+             [eg, probs[0][1], eg, probs[1][1]]] + \
+        [[{0: e8, 1: e32, 2: eu8, 3: e32}[j], probs[0][2][j].copy(),
+          {0: e8, 1: e32, 2: eu8, 3: e32}[j], probs[1][2][j].copy()] for j in range(4)]
+    oracle.hybrid8bit_adamw_step(*mixed, block, coef=0.7, **KW)
+    for got, want in zip(mixed, full):
+        assert got[0].size == 0 and got[2].size == 0
+        assert got[1].tobytes() == want[0].tobytes() and got[3].tobytes() == want[1].tobytes()
+    oracle.hybrid8bit_adamw_step([], [], [], [], [], [], block, coef=0.7, **KW)

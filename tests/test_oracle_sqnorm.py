@@ -131,3 +131,20 @@ def test_subnormal_inputs_are_not_flushed():
 def test_all_zero_gradients():
     sk, s, status = oracle.grad_sqnorm([np.zeros(n, np.float32) for n in (1, 8193)])
     assert s == 0.0 and status == oracle.STATUS_OK and sk.tolist() == [0.0, 0.0]
+
+
+def test_empty_list_and_empty_tensors():
+    # an empty sum is 0; an empty tensor adds +0.0 to the list-order total, which is
+    # exact, so S equals that of the list without it (checked against the naive sum)
+    sk, s, status = oracle.grad_sqnorm([])
+    assert s == 0.0 and status == oracle.STATUS_OK and sk.size == 0
+    rng = np.random.default_rng(5)
+    a = f32_to_bf16_bits((rng.standard_normal(9000) * 1e-2).astype(np.float32))
+    b = f32_to_bf16_bits((rng.standard_normal(20000) * 1e-2).astype(np.float32))
+    e = np.zeros(0, np.uint16)
+    sk, s, status = oracle.grad_sqnorm([e, a, e, e, b, e])
+    _, s_ab, _ = oracle.grad_sqnorm([a, b])
+    assert s == s_ab and status == oracle.STATUS_OK
+    assert sk[[0, 2, 3, 5]].tolist() == [0.0] * 4
+    assert abs(s - oracle.grad_sqnorm_naive([a, b])) <= 1e-12 * s
+    assert oracle.grad_sqnorm([e, e])[1] == 0.0
