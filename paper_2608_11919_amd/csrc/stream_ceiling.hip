@@ -3,8 +3,11 @@
 //   mix:  per element read 8 B (4 B weight, 2 B gradient, 1 B + 1 B codes) and
 //         write 6 B back in place (weight, two codes): the fused step's traffic;
 //   read: read 2 B per element (the bf16 gradient): the sum of squares' traffic.
-// Same layout as the step (separate arrays, 16-byte vector accesses, contiguous
-// per-workgroup ranges).  Prints one JSON line.  Usage: stream_ceiling [n] [reps]
+// Same layout as the step (separate arrays, 16-byte vector accesses).  The mix is
+// timed in two shapes and the faster one is reported: one granule per thread per
+// workgroup iteration over contiguous per-workgroup ranges, and wave tiles of 32
+// elements per lane (a lane's granules 64 apart, as the step kernel lays them out)
+// handed to the waves in turn.  Prints one JSON line.  Usage: stream_ceiling [n] [reps]
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -52,6 +55,44 @@ __global__ __launch_bounds__(kThreads) void k_mix(uint4* __restrict__ w, const u
         w[2 * gi + 1] = w1;
         m[gi] = mm;
         v[gi] = vv;
+    }
+}
+
+// Wave tiles: tile t covers granules [256 t, 256 (t + 1)); granule j of lane l is
+// 256 t + l + 64 j (j = 0..3).  Tiles go to the waves in turn.  Every access is
+// inside its array: the largest granule index is 256 * tiles - 1 = n / 8 - 1.
+__global__ __launch_bounds__(kThreads) void k_mix_tiles(uint4* __restrict__ w,
+                                                       const uint4* __restrict__ g,
+                                                       uint2* __restrict__ m,
+                                                       uint2* __restrict__ v, int64_t tiles)
+{
+    constexpr int G = 4;  // granules per lane: 32 elements
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = int64_t(gridDim.x) * 4;
+    for (int64_t t = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6); t < tiles; t += waves) {
+        uint4 a[G], b[G], c[G];
+        uint2 mm[G], vv[G];
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int64_t gi = t * (64 * G) + lane + 64 * j;
+            a[j] = w[2 * gi];
+            b[j] = w[2 * gi + 1];
+            c[j] = g[gi];
+            mm[j] = m[gi];
+            vv[j] = v[gi];
+        }
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int64_t gi = t * (64 * G) + lane + 64 * j;
+            a[j].x ^= c[j].x;
+            b[j].y ^= c[j].y;
+            mm[j].x ^= c[j].z;
+            vv[j].y ^= c[j].w;
+            w[2 * gi] = a[j];
+            w[2 * gi + 1] = b[j];
+            m[gi] = mm[j];
+            v[gi] = vv[j];
+        }
     }
 }
 
@@ -121,6 +162,22 @@ int main(int argc, char** argv)
         CK(hipEventElapsedTime(&ms, a, b));
         if (ms / reps < best_read)
             best_read = ms / reps;
+    }
+    // wave tiles of 2048 elements: n is a multiple of kIter = 2048
+    for (int per_cu : {1, 2, 3}) {
+        const int grid = cus * per_cu;
+        const int64_t tiles = n / 2048;
+        k_mix_tiles<<<grid, kThreads>>>(w, g, m, v, tiles);  // warm
+        CK(hipGetLastError());
+        CK(hipEventRecord(a));
+        for (int r = 0; r < reps; ++r)
+            k_mix_tiles<<<grid, kThreads>>>(w, g, m, v, tiles);
+        CK(hipEventRecord(b));
+        CK(hipEventSynchronize(b));
+        float ms;
+        CK(hipEventElapsedTime(&ms, a, b));
+        if (ms / reps < best_mix)
+            best_mix = ms / reps;
     }
     CK(hipDeviceSynchronize());
     // an iteration of k_read reads 256 x 16 B: 2048 bf16 gradient elements
