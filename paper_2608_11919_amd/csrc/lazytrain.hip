@@ -333,15 +333,6 @@ __device__ inline int find_tensor(const int64_t* __restrict__ prefix, int n_tens
     return lo;
 }
 
-// Contiguous, balanced range of work units for this workgroup.
-__device__ inline void unit_range(int64_t units, int64_t* begin, int64_t* end)
-{
-    const int64_t G = gridDim.x, b = blockIdx.x;
-    const int64_t per = units / G, rem = units % G;
-    *begin = b * per + (b < rem ? b : rem);
-    *end = *begin + per + (b < rem ? 1 : 0);
-}
-
 // ------------------------------------------------------- a1: chunk sums
 
 // One lane's share of a chunk: granules lane + 256*r, r = 0..3.
@@ -389,7 +380,7 @@ __device__ inline double lane_sum(const ChunkLane<GT>& c)
 // next-iteration prefetch and with grid-strided iterations (all within ~5%).
 constexpr int kSqChunksPerIter = 2;
 
-// Each iteration takes U consecutive chunks of the workgroup's contiguous range.
+// Each iteration takes U consecutive chunks.
 template <typename GT>
 __global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __restrict__ chunk_prefix,
                                                             const uint64_t* __restrict__ ptrs,
@@ -402,8 +393,16 @@ __global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __res
     const int lane = threadIdx.x;
     const int wave = lane >> 6;
     const int64_t n_iter = (n_chunks + U - 1) / U;
+    // A contiguous, balanced range of iterations per workgroup: for this
+    // read-only pass it measured 5% faster than handing iterations out in turn
+    // (the opposite of the step kernels).
     int64_t i_begin, i_end;
-    unit_range(n_iter, &i_begin, &i_end);
+    {
+        const int64_t G = gridDim.x, b = blockIdx.x;
+        const int64_t per = n_iter / G, rem = n_iter % G;
+        i_begin = b * per + (b < rem ? b : rem);
+        i_end = i_begin + per + (b < rem ? 1 : 0);
+    }
     if (i_begin >= i_end)
         return;
     int k = find_tensor(chunk_prefix, n_tensors, i_begin * U);
@@ -946,20 +945,17 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
         __syncthreads();
     }
 
-    // Work units: wave spans (W == 1, each wave on its own) or workgroup spans.
-    int64_t u_begin, u_end;
-    {
-        const int64_t workers = W > 1 ? int64_t(gridDim.x) : int64_t(gridDim.x) * 4;
-        const int64_t me = W > 1 ? int64_t(blockIdx.x) : int64_t(blockIdx.x) * 4 + wave;
-        const int64_t per = n_units / workers, rem = n_units % workers;
-        u_begin = me * per + (me < rem ? me : rem);
-        u_end = u_begin + per + (me < rem ? 1 : 0);
-    }
+    // Work units: wave spans (W == 1, each wave on its own) or workgroup spans,
+    // handed to the workers in turn, so that at any moment the chip streams one
+    // contiguous region of every array.  Measured on the 3B-class step: 2%
+    // faster than one contiguous range of units per worker.
+    const int64_t workers = W > 1 ? int64_t(gridDim.x) : int64_t(gridDim.x) * 4;
+    const int64_t me = W > 1 ? int64_t(blockIdx.x) : int64_t(blockIdx.x) * 4 + wave;
     // Offset of this wave's span inside a unit.
     const int64_t span0 = W > 1 ? int64_t(wave) * Geo::WAVE_SPAN : 0;
-    int k = u_begin < u_end ? find_tensor(unit_prefix, n_tensors, u_begin) : 0;
+    int k = me < n_units ? find_tensor(unit_prefix, n_tensors, me) : 0;
     int buf = 0;
-    for (int64_t u = u_begin; u < u_end; ++u, buf ^= 1) {
+    for (int64_t u = me; u < n_units; u += workers, buf ^= 1) {
         while (u >= unit_prefix[k + 1])
             ++k;
         const StepTensor d = desc[k];
@@ -1215,16 +1211,11 @@ __global__ __launch_bounds__(kThreads) void k_adamw32_step(const int64_t* __rest
         return;  // skipped step: nothing is written
     const float coef = coef_ptr ? *coef_ptr : 1.0f;
     const int lane = threadIdx.x & 63;
-    int64_t u_begin, u_end;
-    {
-        const int64_t workers = int64_t(gridDim.x) * 4;
-        const int64_t me = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
-        const int64_t per = n_units / workers, rem = n_units % workers;
-        u_begin = me * per + (me < rem ? me : rem);
-        u_end = u_begin + per + (me < rem ? 1 : 0);
-    }
-    int k = u_begin < u_end ? find_tensor(unit_prefix, n_tensors, u_begin) : 0;
-    for (int64_t u = u_begin; u < u_end; ++u) {
+    // Units go to the waves in turn, as in the 8-bit step.
+    const int64_t workers = int64_t(gridDim.x) * 4;
+    const int64_t me = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    int k = me < n_units ? find_tensor(unit_prefix, n_tensors, me) : 0;
+    for (int64_t u = me; u < n_units; u += workers) {
         while (u >= unit_prefix[k + 1])
             ++k;
         const Fp32Tensor d = desc[k];
