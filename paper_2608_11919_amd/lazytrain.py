@@ -544,6 +544,19 @@ class Hybrid8bitAdamW:
         return torch.cuda.ExternalStream(int(stream), device=dev)
 
     def step(self, grads: Sequence[torch.Tensor], stream=None) -> None:
+        """One clipped step with one gradient per parameter, in the order of the
+        parameters (a zero-element parameter takes a zero-element gradient)."""
+        grads = list(grads)
+        if len(grads) != len(self.params):
+            raise ValueError(f"step() needs one gradient per parameter: got {len(grads)} "
+                             f"for {len(self.params)} parameters")
+        for i, (g, p) in enumerate(zip(grads, self.params)):
+            if g is None:
+                raise ValueError(f"gradient {i} is None (every parameter needs a gradient; "
+                                 "pass zeros for a parameter that received none)")
+            if g.numel() != p.numel():
+                raise ValueError(f"gradient {i} has {g.numel()} elements, its parameter "
+                                 f"{p.numel()}")
         if self._unchecked:
             self.last_status(stream)  # the bias correction needs the true step count
         t = self.step_count + 1

@@ -176,3 +176,20 @@ def test_streamed_layer_with_empty_tensors():
     assert S.item() == S_o and coef.item() == c and status.item() == st_o
     got = State(*[[t.numpy() for t in lst] for lst in (host.w, host.mq, host.ma, host.vq, host.va)])
     assert_state_equal(got, ref, "streamed, empty tensors")
+
+
+def test_optimizer_rejects_mismatched_gradients_before_any_work():
+    params = [torch.zeros(300, dtype=torch.float32, device=DEV),
+              torch.zeros(0, dtype=torch.float32, device=DEV)]
+    opt = lt.Hybrid8bitAdamW(params, block_size=256)
+    g = torch.zeros(300, dtype=torch.bfloat16, device=DEV)
+    e = torch.zeros(0, dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(ValueError, match="one gradient per parameter"):
+        opt.step([g])
+    with pytest.raises(ValueError, match="is None"):
+        opt.step([g, None])
+    with pytest.raises(ValueError, match="elements"):
+        opt.step([g[:299], e])
+    assert opt.step_count == 0
+    opt.step([g, e])
+    assert opt.last_status() == lt.LT_STATUS_OK and opt.step_count == 1
