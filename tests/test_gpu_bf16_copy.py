@@ -62,11 +62,15 @@ def _grads(rng, sizes, as_bf16):
     return [f32_to_bf16_bits(x) for x in g] if as_bf16 else g
 
 
-@pytest.mark.parametrize("block", [256, 2048, 4096])
+@pytest.mark.parametrize("block", [64, 128, 256, 512, 1024, 2048, 4096, 8192])
 @pytest.mark.parametrize("as_bf16", [False, True])
-def test_8bit_step_bf16_copy_matches_oracle(block, as_bf16):
-    rng = np.random.default_rng(block + as_bf16)
+@pytest.mark.parametrize("code_map", [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC])
+def test_8bit_step_bf16_copy_matches_oracle(block, as_bf16, code_map):
+    rng = np.random.default_rng(block + as_bf16 + 10 * code_map)
     base = _random_state(rng, SIZES, block)
+    if code_map == lt.LT_MAP_DYNAMIC:  # every byte is a valid sign-magnitude code
+        for k, n in enumerate(SIZES):
+            base.mq[k][:] = rng.integers(-128, 128, size=n)
     g = _grads(rng, SIZES, as_bf16)
     gdev = [to_dev(x) for x in g]
     _, _, status, _, coef = gpu_norm_and_coef(gdev, 1.0)
@@ -74,15 +78,16 @@ def test_8bit_step_bf16_copy_matches_oracle(block, as_bf16):
     out = _bf16_out(SIZES)
     lt.lt_hybrid8bit_adamw_step(with_copy.w, gdev, with_copy.mq, with_copy.ma, with_copy.vq,
                                 with_copy.va, block, step=3, coef=coef, status=status,
-                                params_bf16=out, **HYPER)
+                                params_bf16=out, code_map=code_map, **HYPER)
     lt.lt_hybrid8bit_adamw_step(without.w, gdev, without.mq, without.ma, without.vq, without.va,
-                                block, step=3, coef=coef, status=status, **HYPER)
+                                block, step=3, coef=coef, status=status, code_map=code_map,
+                                **HYPER)
     torch.cuda.synchronize()
     assert_state_equal(with_copy.to_host(), without.to_host(), "state with vs without copy")
     ref = base.copy()
     _, S, st = oracle.grad_sqnorm(g, n_threads=8)
     _, c = oracle.clip_coef(S, 1.0)
-    oracle_step(ref, g, block, 3, coef=float(c), status=st)
+    oracle_step(ref, g, block, 3, coef=float(c), status=st, code_map=code_map)
     assert_state_equal(with_copy.to_host(), ref, "state vs oracle")
     for k in range(len(SIZES)):
         _assert_bf16_equal(_bits(out[k]), oracle.round_bf16(ref.w[k]), f"copy of tensor {k}")
