@@ -255,19 +255,53 @@ __device__ inline float bf16_lo(uint32_t d) { return __uint_as_float(d << 16); }
 __device__ inline float bf16_hi(uint32_t d) { return __uint_as_float(d & 0xFFFF0000u); }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Every tensor lives in device (global) memory, but the kernels read its address
+// from a descriptor, so the compiler cannot tell and would emit flat memory
+// instructions.  Those count against the LDS/scalar counter as well as the
+// vector-memory one, so each wait for a shuffle or a scalar load would also wait
+// for every load and store the wave has in flight.  Tensor data is therefore
+// accessed through global address-space pointers (global_load/global_store),
+// as the compiler's vector types (HIP's uint4/float4 classes take no such pointer).
+template <typename T>
+__device__ inline __attribute__((address_space(1))) T* gp(T* p)
+{
+    return (__attribute__((address_space(1))) T*)p;
+}
 
 // 16-byte load that asks the memory system not to keep the line (streaming).
 __device__ inline uint4 load16_stream(const void* p)
 {
-    const u32x4 v = __builtin_nontemporal_load(static_cast<const u32x4*>(p));
+    const u32x4 v = __builtin_nontemporal_load(gp(static_cast<const u32x4*>(p)));
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-__device__ inline uint4 load16(const void* p) { return *static_cast<const uint4*>(p); }
+__device__ inline uint4 load16(const void* p)
+{
+    const u32x4 v = *gp(static_cast<const u32x4*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ inline void store16(void* p, uint4 q) { *gp(static_cast<u32x4*>(p)) = u32x4{q.x, q.y, q.z, q.w}; }
+
+__device__ inline void store16f(float* p, float a, float b, float c, float d)
+{
+    *gp(reinterpret_cast<f32x4*>(p)) = f32x4{a, b, c, d};
+}
+
+__device__ inline uint2 load8(const void* p)
+{
+    const u32x2 v = *gp(static_cast<const u32x2*>(p));
+    return make_uint2(v.x, v.y);
+}
+
+__device__ inline void store8(void* p, uint32_t lo, uint32_t hi) { *gp(static_cast<u32x2*>(p)) = u32x2{lo, hi}; }
 
 // Raw bits of one gradient element (bf16: 16 bits, fp32: 32 bits).
-__device__ inline uint32_t grad_bits(const uint16_t* p) { return *p; }
-__device__ inline uint32_t grad_bits(const float* p) { return __float_as_uint(*p); }
+__device__ inline uint32_t grad_bits(const uint16_t* p) { return *gp(p); }
+__device__ inline uint32_t grad_bits(const float* p) { return __float_as_uint(*gp(p)); }
 
 // Packed 16-byte words holding the 8 gradients of one granule: bf16 needs one
 // word, fp32 two.  Unpacking is exact (bf16 is the top half of an fp32).
@@ -690,8 +724,8 @@ __device__ inline void load_step_full(const StepTensor& d, int64_t ei, StepIn<GT
     load_grads<false>(static_cast<const GT*>(d.g) + ei, kGranule, in.g);
     in.w[0] = load16(d.w + ei);
     in.w[1] = load16(d.w + ei + 4);
-    in.m = *reinterpret_cast<const uint2*>(d.mq + ei);
-    in.v = *reinterpret_cast<const uint2*>(d.vq + ei);
+    in.m = load8(d.mq + ei);
+    in.v = load8(d.vq + ei);
 }
 
 // Ragged granule: the first nv (0..8) elements exist, the others read as 0.
@@ -703,9 +737,9 @@ __device__ inline void load_step_ragged(const StepTensor& d, int64_t ei, int nv,
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const bool ok = e < nv;
-        wb[e] = ok ? __float_as_uint(d.w[ei + e]) : 0u;
-        mb[e] = ok ? uint32_t(uint8_t(d.mq[ei + e])) : 0u;
-        vb[e] = ok ? uint32_t(d.vq[ei + e]) : 0u;
+        wb[e] = ok ? __float_as_uint(gp(d.w)[ei + e]) : 0u;
+        mb[e] = ok ? uint32_t(uint8_t(gp(d.mq)[ei + e])) : 0u;
+        vb[e] = ok ? uint32_t(gp(d.vq)[ei + e]) : 0u;
     }
     in.w[0] = make_uint4(wb[0], wb[1], wb[2], wb[3]);
     in.w[1] = make_uint4(wb[4], wb[5], wb[6], wb[7]);
@@ -730,12 +764,12 @@ __device__ inline void store_bf16x8(uint16_t* p, int nv, const float (&w)[8])
     const uint4 q = make_uint4(bf16_pair(w[0], w[1]), bf16_pair(w[2], w[3]),
                                bf16_pair(w[4], w[5]), bf16_pair(w[6], w[7]));
     if (nv >= kGranule) {
-        *reinterpret_cast<uint4*>(p) = q;
+        store16(p, q);
         return;
     }
     const uint32_t word[4] = {q.x, q.y, q.z, q.w};
     for (int e = 0; e < nv; ++e)
-        p[e] = uint16_t(word[e >> 1] >> (16 * (e & 1)));
+        gp(p)[e] = uint16_t(word[e >> 1] >> (16 * (e & 1)));
 }
 
 // Packs four codes held as exact small integers (as floats) into one word.
@@ -969,8 +1003,8 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
         {
             const int64_t blk = (e0 + (B >= 512 ? 0 : kGranule * lane)) / B;
             const bool exists = n_span > (B >= 512 ? 0 : kGranule * lane);
-            a_m = exists ? d.ma[blk] : 0.0f;
-            a_v = exists ? d.va[blk] : 0.0f;
+            a_m = exists ? gp(d.ma)[blk] : 0.0f;
+            a_v = exists ? gp(d.va)[blk] : 0.0f;
         }
         // linear map: the code steps A/127 and A/255
         const float step_m = MAP == kMapLinear ? div_by_const<127>(a_m) : 0.0f;
@@ -1049,13 +1083,13 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                 }
                 const int64_t ei = e0 + kGranule * (lane + 64 * j);
                 if (full) {
-                    *reinterpret_cast<float4*>(d.w + ei) = make_float4(w[0], w[1], w[2], w[3]);
-                    *reinterpret_cast<float4*>(d.w + ei + 4) = make_float4(w[4], w[5], w[6], w[7]);
+                    store16f(d.w + ei, w[0], w[1], w[2], w[3]);
+                    store16f(d.w + ei + 4, w[4], w[5], w[6], w[7]);
                 } else {
                     const int nv =
                         int(i64min(i64max(n_span - kGranule * (lane + 64 * j), 0), kGranule));
                     for (int e = 0; e < nv; ++e)
-                        d.w[ei + e] = w[e];
+                        gp(d.w)[ei + e] = w[e];
                 }
                 if (WB && d.wb) {
                     const int nv = full ? kGranule
@@ -1126,14 +1160,14 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
                 pv0 = pv1 = 0u;
             const int64_t ei = e0 + kGranule * (lane + 64 * j);
             if (full) {
-                *reinterpret_cast<uint2*>(d.mq + ei) = make_uint2(pm0, pm1);
-                *reinterpret_cast<uint2*>(d.vq + ei) = make_uint2(pv0, pv1);
+                store8(d.mq + ei, pm0, pm1);
+                store8(d.vq + ei, pv0, pv1);
             } else {
                 const int nv = int(i64min(i64max(n_span - kGranule * (lane + 64 * j), 0), kGranule));
                 for (int e = 0; e < nv; ++e) {
                     const uint32_t wm = e < 4 ? pm0 : pm1, wv = e < 4 ? pv0 : pv1;
-                    d.mq[ei + e] = int8_t((wm >> (8 * (e & 3))) & 0xFFu);
-                    d.vq[ei + e] = uint8_t((wv >> (8 * (e & 3))) & 0xFFu);
+                    gp(d.mq)[ei + e] = int8_t((wm >> (8 * (e & 3))) & 0xFFu);
+                    gp(d.vq)[ei + e] = uint8_t((wv >> (8 * (e & 3))) & 0xFFu);
                 }
             }
         }
@@ -1144,8 +1178,8 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
             const bool first_wave = W > 1 ? (wave % W) == 0 : true;
             if (first_lane && first_wave && n_span > o) {
                 const int64_t blk = (e0 + o) / B;
-                d.ma[blk] = ok_m ? amax_m : 0.0f;
-                d.va[blk] = ok_v ? amax_v : 0.0f;
+                gp(d.ma)[blk] = ok_m ? amax_m : 0.0f;
+                gp(d.va)[blk] = ok_v ? amax_v : 0.0f;
             }
         }
     }
@@ -1184,18 +1218,18 @@ __device__ inline void load8f(const float* p, int nv, float (&x)[8])
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e)
-        x[e] = e < nv ? p[e] : 0.0f;
+        x[e] = e < nv ? gp(p)[e] : 0.0f;
 }
 
 __device__ inline void store8f(float* p, int nv, const float (&x)[8])
 {
     if (nv >= kGranule) {
-        *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
-        *reinterpret_cast<float4*>(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
+        store16f(p, x[0], x[1], x[2], x[3]);
+        store16f(p + 4, x[4], x[5], x[6], x[7]);
         return;
     }
     for (int e = 0; e < nv; ++e)
-        p[e] = x[e];
+        gp(p)[e] = x[e];
 }
 
 template <typename GT, bool WB>
