@@ -9,6 +9,20 @@
  * training-configuration table (beta1, beta2, eps, learning rate, weight
  * decay, max grad norm; non-finite gradients skip the step).
  *
+ * Steps, as named in this header and in the sources:
+ *   a1  sum of squares of the gradients: one fp64 partial per 8192-element chunk;
+ *   a2  the fixed-order finish: per-tensor sums S_k, the total S, the status;
+ *   a3  the norm and the clip coefficient;
+ *   a4  dequantizing the stored 8-bit moments;   a5  the clipped gradient;
+ *   a6  the moment update;   a7  the AdamW weight update;
+ *   a8  the new block absmax of each moment;   a9  requantizing and storing;
+ *   a10 skipping a step whose gradients are not finite;
+ *   a11 the same step over host-resident state streamed layer by layer;
+ *   f1  fp32-state AdamW for tensors outside the 8-bit slice, and the slice;
+ *   f2  the dynamic (non-linear) 8-bit code map;
+ *   f3  the bf16 copy of the updated weights;
+ *   f4  the gradient norm accumulated as gradients arrive.
+ *
  * Conventions for every entry point:
  *  - Tensor data, workspace and scalar outputs are DEVICE pointers on the
  *    current HIP device, owned by the caller.  The library never frees them

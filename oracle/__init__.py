@@ -39,7 +39,7 @@ def _load():
     if not os.path.exists(_LIB_PATH):
         if os.environ.get("LTO_LIBRARY"):
             raise FileNotFoundError(f"LTO_LIBRARY names a missing file: {_LIB_PATH}")
-        from . import build as _build  # building the checker is not using the product
+        from . import build as _build  # builds the oracle's own C library
 
         _build.build()
     lib = ctypes.CDLL(_LIB_PATH)

@@ -23,6 +23,12 @@
  * caller beyond transient scratch and never keep pointers after returning.
  * n_threads <= 1 runs single-threaded; any thread count gives bitwise the same
  * results because every partial has a fixed index.
+ *
+ * Step labels in the section titles of the source: a1-a2 the sum of squares
+ * and its fixed-order finish, a3 the clip coefficient, a4-a10 the step
+ * (dequantize, clip, moments, weight update, block absmax, requantize, skip),
+ * a8-a9 the block quantizer on its own, f1 fp32-state AdamW, f2 the dynamic
+ * code map, f3 the bf16 weight copy.
  */
 #ifndef LAZYTRAIN_ORACLE_H
 #define LAZYTRAIN_ORACLE_H

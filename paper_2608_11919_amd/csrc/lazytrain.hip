@@ -17,7 +17,8 @@
 // Host side: the C ABI, descriptor uploads through a pinned staging ring, and
 // the layer-streamed step (a ring of device slots on three streams).
 // The reduction order and the fp32 operation order are fixed (see
-// include/lazytrain.h); every kernel's result is independent of its grid.
+// include/lazytrain.h, which also names the steps a1..a11 and f1..f4 used in
+// the section titles below); every kernel's result is independent of its grid.
 
 #include <hip/hip_runtime.h>
 

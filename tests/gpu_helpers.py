@@ -90,7 +90,7 @@ def assert_state_equal(gpu: State, ref: State, what=""):
                                      f"first {i}: gpu {a[i]!r} oracle {b[i]!r}")
 
 
-def check_north_star_tolerance(gpu: State, ref: State, lr: float):
+def check_stated_tolerance(gpu: State, ref: State, lr: float):
     """The stated bar, as a second check: weights within 1e-6 relative (floor lr),
     codes equal except +-1 at a rate <= 1e-6."""
     n_codes = mism = 0

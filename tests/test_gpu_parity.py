@@ -13,7 +13,7 @@ import oracle
 import paper_2608_11919_amd as lt
 import synth
 from golden_io import adamw_examples, dense, f32_to_bf16_bits, sqnorm_cases
-from gpu_helpers import (DEV, HYPER, State, assert_state_equal, check_north_star_tolerance,
+from gpu_helpers import (DEV, HYPER, State, assert_state_equal, check_stated_tolerance,
                          gpu_norm_and_coef, gpu_step, oracle_step, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
@@ -161,7 +161,7 @@ def test_workload_step_parity(wid):
     assert to_host(S)[0].hex() == rS.hex()
     assert to_host(coef)[0].tobytes() == rcoef.tobytes()
     assert_state_equal(got, ref, w.name)
-    check_north_star_tolerance(got, ref, HYPER["lr"])
+    check_stated_tolerance(got, ref, HYPER["lr"])
 
 
 def _random_state(sizes, block, rng, zero_frac=0.1):
