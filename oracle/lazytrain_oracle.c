@@ -33,7 +33,9 @@ static float grad_value(const void* g, int gdt, int64_t i)
 
 /* ------------------------------------------------- sum of squares (a1-a2) */
 
-/* Sum of squares of chunk c of one tensor (n elements), fixed order. */
+/* Sum of squares of chunk c of one tensor (n elements), fixed order.  Part of
+ * the per-tensor norm of Sec. 3.5's clipping path; the chunk and lane order is
+ * this implementation's reading, since the paper fixes no order. */
 static double chunk_sum_of_squares(const void* g, int gdt, int64_t n, int64_t c)
 {
     const int64_t base = c * LTO_CHUNK;
@@ -68,6 +70,8 @@ static double chunk_sum_of_squares(const void* g, int gdt, int64_t n, int64_t c)
     return (W[0] + W[2]) + (W[1] + W[3]);
 }
 
+/* The per-tensor norm of Sec. 3.5, as its square: chunk partials combined in a
+ * fixed order. */
 static double tensor_sum_of_squares(const void* g, int gdt, int64_t n, int n_threads)
 {
     const int64_t n_chunks = (n + LTO_CHUNK - 1) / LTO_CHUNK;
@@ -91,6 +95,8 @@ static double tensor_sum_of_squares(const void* g, int gdt, int64_t n, int n_thr
     return b[0];
 }
 
+/* Sec. 3.5: one global norm aggregated from the per-tensor norms; App. C
+ * safety-checks row: non-finite gradients are detected (here, as the status). */
 int lto_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_tensors, int gdt,
                     double* sq_per_tensor, double* sq_total, int32_t* status, int n_threads)
 {
@@ -110,6 +116,7 @@ int lto_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_tenso
     return LTO_OK;
 }
 
+/* Not from the paper: the plain definition of the sum of squares, used as a pin. */
 double lto_grad_sqnorm_naive(const void* const* grads, const int64_t* numels, int n_tensors,
                              int gdt)
 {
@@ -124,6 +131,8 @@ double lto_grad_sqnorm_naive(const void* const* grads, const int64_t* numels, in
 
 /* ----------------------------------------------------- clip coefficient (a3) */
 
+/* Sec. 3.5: one scale applied to all gradients; App. C: max grad norm.  The
+ * formula is the usual clip-by-global-norm rule with a 1e-6 guard. */
 void lto_clip_coef(double sq_total, float max_norm, float* total_norm, float* coef)
 {
     float norm = (float)sqrt(sq_total);
@@ -139,6 +148,8 @@ static float clampf(float x, float lo, float hi)
     return fminf(fmaxf(x, lo), hi);
 }
 
+/* Sec. 3.5: block-wise 8-bit states with a scale per block.  The linear absmax
+ * code is a reading (the paper names no code map); this is the first moment's. */
 void lto_quantize_signed(const float* x, int64_t n, int8_t* q, float* absmax)
 {
     float A = 0.0f;
@@ -151,6 +162,7 @@ void lto_quantize_signed(const float* x, int64_t n, int8_t* q, float* absmax)
     *absmax = ok ? A : 0.0f;
 }
 
+/* As above, for the second moment (non-negative): 255 levels. */
 void lto_quantize_unsigned(const float* x, int64_t n, uint8_t* q, float* absmax)
 {
     float A = 0.0f;
@@ -163,6 +175,7 @@ void lto_quantize_unsigned(const float* x, int64_t n, uint8_t* q, float* absmax)
     *absmax = ok ? A : 0.0f;
 }
 
+/* The inverse maps of the two linear codes (Sec. 3.5: dequantization). */
 void lto_dequantize_signed(const int8_t* q, int64_t n, float absmax, float* x)
 {
     float step = absmax / 127.0f;
@@ -182,6 +195,8 @@ void lto_dequantize_unsigned(const uint8_t* q, int64_t n, float absmax, float* x
 /* Powers of ten of the map's decades, as correctly rounded double literals. */
 static const double pow10_neg[8] = {1.0, 1e-1, 1e-2, 1e-3, 1e-4, 1e-5, 1e-6, 1e-7};
 
+/* The dynamic tree code map (a second reading of Sec. 3.5's 8-bit states,
+ * after Dettmers et al.'s block-wise 8-bit optimizers): magnitudes by decade. */
 void lto_dynamic_map(int is_signed, float* table)
 {
     const int bits = is_signed ? 7 : 8; /* magnitude bits of a code */
@@ -267,6 +282,9 @@ void lto_dequantize_dynamic_unsigned(const uint8_t* q, int64_t n, float absmax, 
 
 /* --------------------------------------------------------- AdamW step (a4-a10) */
 
+/* App. C optimizer-hyperparameters row (beta1, beta2, eps, learning rate,
+ * weight decay): the per-step scalars of Adam with bias correction and
+ * decoupled weight decay (AdamW), each rounded once to fp32. */
 void lto_step_scalars(double lr, double beta1, double beta2, double eps, double weight_decay,
                       int64_t step, lto_scalars* out)
 {
@@ -304,7 +322,8 @@ static void adamw_element(const adamw_scalars* s, float m0, float v0, float grad
 }
 
 /* One quantization block: elements [off, off + len) of a tensor; *am, *av are
- * this block's stored scales. */
+ * this block's stored scales.  Sec. 3.5: dequantize the 8-bit states, update
+ * them and the fp32 master weights, requantize with new block scales. */
 static void step_block(const adamw_scalars* s, int code_map, float* w, const void* g, int gdt,
                        int64_t off, int64_t len, int8_t* qm, float* am, uint8_t* qv, float* av,
                        float* m1, float* v1)
@@ -325,6 +344,8 @@ static void step_block(const adamw_scalars* s, int code_map, float* w, const voi
     (dyn ? lto_quantize_dynamic_unsigned : lto_quantize_unsigned)(v1, len, qv + off, av);
 }
 
+/* Sec. 3.5's Hybrid 8-bit operator, optimizer side: the clipped AdamW step over
+ * 8-bit block-wise states; App. C: a non-finite step is skipped. */
 int lto_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int gdt,
                               int8_t* const* m_codes, float* const* m_absmax,
                               uint8_t* const* v_codes, float* const* v_absmax,
@@ -367,6 +388,8 @@ int lto_hybrid8bit_adamw_step(float* const* params, const void* const* grads, in
     return LTO_OK;
 }
 
+/* Sec. 3.5: the parameters outside the 8-bit slice keep full-precision Adam
+ * states (DeepSpeed CPUAdam in the paper's run); same operation order. */
 void lto_adamw_fp32_step(float* w, const void* grad, int gdt, float* m, float* v, int64_t n,
                          double lr, double beta1, double beta2, double eps, double weight_decay,
                          int64_t step, float coef)
@@ -378,6 +401,8 @@ void lto_adamw_fp32_step(float* w, const void* grad, int gdt, float* m, float* v
         adamw_element(&s, m[i], v[i], grad_value(grad, gdt, i), w[i], &m[i], &v[i], &w[i]);
 }
 
+/* Sec. 3.1 and 3.4: parameters travel to the GPU for each layer; this is the
+ * bf16 copy of the updated weights that such a transfer carries. */
 void lto_round_bf16(const float* x, int64_t n, uint16_t* y)
 {
     for (int64_t i = 0; i < n; ++i) {

@@ -75,7 +75,8 @@ double lto_grad_sqnorm_naive(const void* const* grads, const int64_t* numels, in
 void lto_clip_coef(double sq_total, float max_norm, float* total_norm, float* coef);
 
 /*
- * The fp32 scalars of one AdamW step.  Hyperparameters arrive as doubles (as a
+ * The fp32 scalars of one AdamW step (App. C optimizer-hyperparameters row;
+ * Adam with bias correction and decoupled weight decay).  Hyperparameters arrive as doubles (as a
  * Python or C caller holds them); each scalar is computed in fp64 and rounded
  * once to fp32: decay = 1 - lr*wd, step_size = lr / (1 - beta1^t),
  * rbc2 = 1 / sqrt(1 - beta2^t), c1 = 1 - beta1, c2 = 1 - beta2, and beta1,
@@ -88,7 +89,8 @@ void lto_step_scalars(double lr, double beta1, double beta2, double eps, double 
                       int64_t step, lto_scalars* out);
 
 /*
- * One Hybrid 8-bit AdamW step over a list of tensors.  For tensor k:
+ * One Hybrid 8-bit AdamW step over a list of tensors (Sec. 3.5, the Hybrid
+ * 8-bit operator; App. C hyperparameters and safety checks).  For tensor k:
  * params[k] fp32[n], grads[k] gdt[n] (read only), m_codes[k] int8[n],
  * v_codes[k] uint8[n], m_absmax[k] / v_absmax[k] fp32[ceil(n / block_size)].
  * coef may be NULL (no clipping, 1.0f).  status may be NULL (never skip);
@@ -113,7 +115,8 @@ int lto_hybrid8bit_adamw_step(float* const* params, const void* const* grads, in
                               double weight_decay, int64_t step, const float* coef,
                               const int32_t* status, int n_threads);
 
-/* Block quantizers used by the step (exported for the quantizer tests).
+/* Block quantizers used by the step (Sec. 3.5 block-wise scales; the linear map
+ * is a reading), exported for the quantizer tests.
  * Signed (first moment): A = max|x|, q = clamp(rint(x * (127/A)), -127, 127).
  * Unsigned (second moment, x >= 0): A = max x, q = clamp(rint(x * (255/A)), 0, 255).
  * A block whose A or reciprocal is not finite gets q = 0 and A = 0. */
@@ -148,7 +151,8 @@ void lto_quantize_dynamic_unsigned(const float* x, int64_t n, uint8_t* q, float*
 void lto_dequantize_dynamic_signed(const int8_t* q, int64_t n, float absmax, float* x);
 void lto_dequantize_dynamic_unsigned(const uint8_t* q, int64_t n, float absmax, float* x);
 
-/* fp32-state AdamW with the same operation order as the 8-bit step (states
+/* fp32-state AdamW (Sec. 3.5: the parameters outside the 8-bit slice) with the
+ * same operation order as the 8-bit step (states
  * m, v stay fp32 and are updated in place).  Used to check that the 8-bit
  * step reduces to plain AdamW when its states are exactly representable. */
 void lto_adamw_fp32_step(float* w, const void* grad, int gdt, float* m, float* v, int64_t n,
