@@ -24,6 +24,12 @@
  * n_threads <= 1 runs single-threaded; any thread count gives bitwise the same
  * results because every partial has a fixed index.
  *
+ * Parity unpinned, in part: two choices here are readings that the paper does
+ * not fix, the fixed reduction order of the sum of squares and the 8-bit code
+ * maps.  Their values are pinned (the sum within the order's rounding bound and
+ * exactly on exactly representable inputs; the codes by round-trip, rounding
+ * and map-structure properties), but their exact bits are this definition's.
+ *
  * Step labels in the section titles of the source: a1-a2 the sum of squares
  * and its fixed-order finish, a3 the clip coefficient, a4-a10 the step
  * (dequantize, clip, moments, weight update, block absmax, requantize, skip),
