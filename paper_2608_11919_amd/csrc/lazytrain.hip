@@ -719,10 +719,14 @@ struct StepIn {
     uint2 m, v;
 };
 
+// The gradients are read once and never written back, so their loads carry the
+// streaming (non-temporal) hint: measured 0.4% faster on the whole 3B-class step
+// (16 alternating rounds).  Loads of data that the step writes back keep the
+// default policy: streaming those costs 4% in a probe of the same byte mix.
 template <typename GT>
 __device__ inline void load_step_full(const StepTensor& d, int64_t ei, StepIn<GT>& in)
 {
-    load_grads<false>(static_cast<const GT*>(d.g) + ei, kGranule, in.g);
+    load_grads<true>(static_cast<const GT*>(d.g) + ei, kGranule, in.g);
     in.w[0] = load16(d.w + ei);
     in.w[1] = load16(d.w + ei + 4);
     in.m = load8(d.mq + ei);
@@ -733,7 +737,7 @@ __device__ inline void load_step_full(const StepTensor& d, int64_t ei, StepIn<GT
 template <typename GT>
 __device__ inline void load_step_ragged(const StepTensor& d, int64_t ei, int nv, StepIn<GT>& in)
 {
-    load_grads<false>(static_cast<const GT*>(d.g) + ei, nv, in.g);
+    load_grads<true>(static_cast<const GT*>(d.g) + ei, nv, in.g);
     uint32_t wb[8], mb[8], vb[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -1264,7 +1268,7 @@ __global__ __launch_bounds__(kThreads) void k_adamw32_step(const int64_t* __rest
             nv[j] = int(i64min(i64max(n_span - o, 0), kGranule));
             const int64_t ei = e0 + o;
             GradWords<GT> gw;
-            load_grads<false>(static_cast<const GT*>(d.g) + ei, nv[j], gw);
+            load_grads<true>(static_cast<const GT*>(d.g) + ei, nv[j], gw);
             float gg[8], ww[8], mm[8], vv[8];
             unpack8(gw, gg);
             load8f(d.w + ei, nv[j], ww);
