@@ -222,22 +222,24 @@ def lt_grad_sqnorm(grads: Sequence[torch.Tensor], sq_total: torch.Tensor, status
         raise ValueError("sq_per_tensor needs one float64 per tensor")
     nbytes = lt_grad_sqnorm_workspace_bytes([g.numel() for g in grads])
     ws = _workspace(device, nbytes, workspace, stream)
-    _check(lib().lt_grad_sqnorm(
-        _ptr_array(grads), _numel_array(grads), len(grads), gdt, ws.data_ptr(),
-        ws.numel() * ws.element_size(), _scalar(sq_per_tensor, device, torch.float64, "sq_per_tensor"),
-        _scalar(sq_total, device, torch.float64, "sq_total"),
-        _scalar(status, device, torch.int32, "status"), _stream_handle(stream, device)))
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_grad_sqnorm(
+            _ptr_array(grads), _numel_array(grads), len(grads), gdt, ws.data_ptr(),
+            ws.numel() * ws.element_size(), _scalar(sq_per_tensor, device, torch.float64, "sq_per_tensor"),
+            _scalar(sq_total, device, torch.float64, "sq_total"),
+            _scalar(status, device, torch.int32, "status"), _stream_handle(stream, device)))
 
 
 def lt_clip_coef(sq_total: torch.Tensor, max_norm: float, coef: torch.Tensor,
                  total_norm: Optional[torch.Tensor] = None, stream=None) -> None:
     """Step a3: norm and clip coefficient into device float32 tensors."""
     device = sq_total.device
-    _check(lib().lt_clip_coef(_scalar(sq_total, device, torch.float64, "sq_total"),
-                              float(max_norm),
-                              _scalar(total_norm, device, torch.float32, "total_norm"),
-                              _scalar(coef, device, torch.float32, "coef"),
-                              _stream_handle(stream, device)))
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_clip_coef(_scalar(sq_total, device, torch.float64, "sq_total"),
+                                  float(max_norm),
+                                  _scalar(total_norm, device, torch.float32, "total_norm"),
+                                  _scalar(coef, device, torch.float32, "coef"),
+                                  _stream_handle(stream, device)))
 
 
 def lt_grad_chunk_count(numels: Sequence[int]) -> int:
@@ -259,9 +261,10 @@ def lt_grad_sqnorm_partials(grads: Sequence[torch.Tensor], partials: torch.Tenso
         raise ValueError(f"partials must be a contiguous float64 device view of >= {need} entries")
     ws = _workspace(device, int(lib().lt_grad_sqnorm_partials_workspace_bytes(len(grads))),
                     workspace, stream)
-    _check(lib().lt_grad_sqnorm_partials(
-        _ptr_array(grads), _numel_array(grads), len(grads), gdt, partials.data_ptr(),
-        ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_grad_sqnorm_partials(
+            _ptr_array(grads), _numel_array(grads), len(grads), gdt, partials.data_ptr(),
+            ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
 
 
 def lt_grad_sqnorm_finish(numels: Sequence[int], partials: torch.Tensor, sq_total: torch.Tensor,
@@ -277,11 +280,12 @@ def lt_grad_sqnorm_finish(numels: Sequence[int], partials: torch.Tensor, sq_tota
     ws = _workspace(device, int(lib().lt_grad_sqnorm_finish_workspace_bytes(len(numels))),
                     workspace, stream)
     arr = (ctypes.c_int64 * len(numels))(*numels)
-    _check(lib().lt_grad_sqnorm_finish(
-        arr, len(numels), partials.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
-        _scalar(sq_per_tensor, device, torch.float64, "sq_per_tensor"),
-        _scalar(sq_total, device, torch.float64, "sq_total"),
-        _scalar(status, device, torch.int32, "status"), _stream_handle(stream, device)))
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_grad_sqnorm_finish(
+            arr, len(numels), partials.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
+            _scalar(sq_per_tensor, device, torch.float64, "sq_per_tensor"),
+            _scalar(sq_total, device, torch.float64, "sq_total"),
+            _scalar(status, device, torch.int32, "status"), _stream_handle(stream, device)))
 
 
 class GradNormAccumulator:
@@ -341,13 +345,14 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
             raise ValueError(f"tensor {i}: absmax arrays need ceil({n}/{block_size}) = {nb} entries")
     wb = _bf16_list(params_bf16, params, device)
     ws = _workspace(device, lt_step_workspace_bytes(k), workspace, stream)
-    _check(lib().lt_hybrid8bit_adamw_step(
-        _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
-        _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, int(block_size),
-        int(code_map),
-        float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
-        _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
-        ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_hybrid8bit_adamw_step(
+            _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
+            _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, int(block_size),
+            int(code_map),
+            float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
+            _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
+            ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
 
 
 def lt_streamed_workspace_bytes(numels: Sequence[int], layer_first: Sequence[int],
@@ -410,18 +415,19 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
     first = (ctypes.c_int * len(layer_first))(*layer_first)
     hs = _stream_handle(h2d_stream, device) if h2d_stream is not None else cs
     ds = _stream_handle(d2h_stream, device) if d2h_stream is not None else cs
-    _check(lib().lt_streamed_hybrid8bit_adamw_step(
-        _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
-        _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, first,
-        len(layer_first) - 1, int(block_size), int(code_map), float(lr), float(beta1),
-        float(beta2), float(eps),
-        float(weight_decay), int(step), float(max_norm), int(bool(norm_ready)), int(ring_slots),
-        workspace.data_ptr(),
-        workspace.numel() * workspace.element_size(),
-        _scalar(sq_total, device, torch.float64, "sq_total"),
-        _scalar(total_norm, device, torch.float32, "total_norm"),
-        _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
-        cs, hs, ds))
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_streamed_hybrid8bit_adamw_step(
+            _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
+            _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, first,
+            len(layer_first) - 1, int(block_size), int(code_map), float(lr), float(beta1),
+            float(beta2), float(eps),
+            float(weight_decay), int(step), float(max_norm), int(bool(norm_ready)), int(ring_slots),
+            workspace.data_ptr(),
+            workspace.numel() * workspace.element_size(),
+            _scalar(sq_total, device, torch.float64, "sq_total"),
+            _scalar(total_norm, device, torch.float32, "total_norm"),
+            _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
+            cs, hs, ds))
 
 
 def lt_adamw_fp32_workspace_bytes(n_tensors: int) -> int:
@@ -452,12 +458,13 @@ def lt_adamw_fp32_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Ten
             raise ValueError(f"tensor {i}: params, grads and states must have {n} elements")
     wb = _bf16_list(params_bf16, params, device)
     ws = _workspace(device, lt_adamw_fp32_workspace_bytes(k), workspace, stream)
-    _check(lib().lt_adamw_fp32_step(
-        _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(exp_avg), _ptr_array(exp_avg_sq),
-        wb, _numel_array(params), k, float(lr), float(beta1), float(beta2), float(eps),
-        float(weight_decay), int(step), _scalar(coef, device, torch.float32, "coef"),
-        _scalar(status, device, torch.int32, "status"), ws.data_ptr(),
-        ws.numel() * ws.element_size(), _stream_handle(stream, device)))
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_adamw_fp32_step(
+            _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(exp_avg), _ptr_array(exp_avg_sq),
+            wb, _numel_array(params), k, float(lr), float(beta1), float(beta2), float(eps),
+            float(weight_decay), int(step), _scalar(coef, device, torch.float32, "coef"),
+            _scalar(status, device, torch.int32, "status"), ws.data_ptr(),
+            ws.numel() * ws.element_size(), _stream_handle(stream, device)))
 
 
 def lt_select_8bit_slice(numels: Sequence[int], fraction: float):
@@ -473,8 +480,9 @@ def lt_read_status(status: torch.Tensor, stream=None) -> int:
     """Reads the device status word (synchronizes the stream)."""
     out = ctypes.c_int32()
     device = status.device
-    _check(lib().lt_read_status(_scalar(status, device, torch.int32, "status"),
-                                _stream_handle(stream, device), ctypes.byref(out)))
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_read_status(_scalar(status, device, torch.int32, "status"),
+                                    _stream_handle(stream, device), ctypes.byref(out)))
     return out.value
 
 
