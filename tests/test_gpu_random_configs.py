@@ -101,3 +101,71 @@ def test_random_configuration_matches_oracle(seed):
         both = np.isnan(a) & np.isnan(b)
         a[both] = b[both] = 0.0
     assert_state_equal(got, ref, what)
+
+
+@pytest.mark.parametrize("seed", range(100, 115))
+def test_random_configuration_fp32_state_step(seed):
+    c = _config(seed)
+    rng, sizes = c["rng"], c["sizes"]
+    w = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
+    g32 = [(rng.standard_t(3, size=n) * c["grad_scale"]).astype(np.float32) for n in sizes]
+    g = [f32_to_bf16_bits(x) for x in g32] if c["bf16"] else g32
+    m = [(rng.standard_normal(n) * c["grad_scale"]).astype(np.float32) for n in sizes]
+    v = [(rng.uniform(0, 1, n) * c["grad_scale"] ** 2).astype(np.float32) for n in sizes]
+    dw, dm, dv = [to_dev(x) for x in w], [to_dev(x) for x in m], [to_dev(x) for x in v]
+    coef = torch.tensor([0.37], dtype=torch.float32, device=DEV)
+    lt.lt_adamw_fp32_step(dw, [to_dev(x) for x in g], dm, dv, step=c["step"], coef=coef,
+                          **c["hyper"])
+    torch.cuda.synchronize()
+    for k in range(len(sizes)):
+        oracle.adamw_fp32_step(w[k], g[k], m[k], v[k], step=c["step"], coef=0.37, **c["hyper"])
+        for a, b, name in ((dw[k], w[k], "w"), (dm[k], m[k], "m"), (dv[k], v[k], "v")):
+            assert to_host(a).tobytes() == b.tobytes(), f"seed {seed}: {name}[{k}]"
+
+
+@pytest.mark.parametrize("seed", range(200, 208))
+def test_random_configuration_streamed_step(seed):
+    c = _config(seed)
+    rng, sizes, B = c["rng"], c["sizes"], c["block"]
+    # random layer split of the list, ring of 2..4 slots, separate or shared streams
+    cuts = sorted(set(rng.choice(np.arange(1, len(sizes)), size=min(len(sizes) - 1, 2),
+                                 replace=False).tolist())) if len(sizes) > 1 else []
+    first = [0] + cuts + [len(sizes)]
+    slots = int(rng.integers(2, 5))
+    separate = bool(rng.integers(0, 2))
+    w = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
+    g = [f32_to_bf16_bits((rng.standard_t(3, size=n) * c["grad_scale"]).astype(np.float32))
+         for n in sizes]
+    base = State.zero_host(w, B)
+    for k, n in enumerate(sizes):
+        lo = -128 if c["code_map"] == lt.LT_MAP_DYNAMIC else -127
+        base.mq[k][:] = rng.integers(lo, 128, size=n)
+        base.vq[k][:] = rng.integers(0, 256, size=n)
+        base.ma[k][:] = rng.uniform(0.1, 5.0, size=base.ma[k].size) * c["grad_scale"]
+        base.va[k][:] = rng.uniform(0.1, 5.0, size=base.va[k].size) * c["grad_scale"] ** 2
+    ref = base.copy()
+    _, S_o, st_o = oracle.grad_sqnorm(g, n_threads=8)
+    _, c_o = oracle.clip_coef(S_o, c["max_norm"])
+    oracle.hybrid8bit_adamw_step(ref.w, g, ref.mq, ref.ma, ref.vq, ref.va, B, step=c["step"],
+                                 coef=float(c_o), status=st_o, code_map=c["code_map"],
+                                 n_threads=8, **c["hyper"])
+    pin = lambda a: torch.from_numpy(a).pin_memory()
+    host = State(*[[pin(a.copy()) for a in lst] for lst in
+                   (base.w, base.mq, base.ma, base.vq, base.va)])
+    S = torch.zeros(1, dtype=torch.float64, device=DEV)
+    coef = torch.zeros(1, dtype=torch.float32, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    streams = [torch.cuda.Stream(DEV) for _ in range(3)] if separate else [None] * 3
+    if separate:
+        streams[0].wait_stream(torch.cuda.current_stream())
+    lt.lt_streamed_hybrid8bit_adamw_step(host.w, [pin(x.view(np.int16)) for x in g], host.mq,
+                                         host.ma, host.vq, host.va, first, B, step=c["step"],
+                                         max_norm=c["max_norm"], ring_slots=slots, sq_total=S,
+                                         coef=coef, status=status, compute_stream=streams[0],
+                                         h2d_stream=streams[1], d2h_stream=streams[2],
+                                         code_map=c["code_map"], **c["hyper"])
+    (streams[0] or torch.cuda.current_stream()).synchronize()
+    what = f"seed {seed}: sizes {sizes}, layers {first}, block {B}, slots {slots}"
+    assert to_host(S)[0].hex() == S_o.hex() and to_host(coef)[0] == c_o, what
+    got = State(*[[t.numpy() for t in lst] for lst in (host.w, host.mq, host.ma, host.vq, host.va)])
+    assert_state_equal(got, ref, what)
