@@ -45,6 +45,10 @@
  *  - The workspace holds the tensor-list descriptors the call uploads (and,
  *    for the norm, its partial sums).  Calls that overlap on the device must
  *    use different workspaces.
+ *  - Each list call copies its descriptors from a library-owned pinned host
+ *    buffer that later calls reuse, so the calls must not be captured into a
+ *    HIP graph: a replay would copy whatever that buffer holds by then.
+ *    lt_clip_coef and lt_read_status stage nothing.
  *  - Results are bitwise reproducible: they do not depend on the grid size,
  *    the device occupancy or the stream.
  */
