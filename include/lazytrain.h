@@ -48,7 +48,7 @@
  *  - Each list call copies its descriptors from a library-owned pinned host
  *    buffer that later calls reuse, so the calls must not be captured into a
  *    HIP graph: a replay would copy whatever that buffer holds by then.
- *    lt_clip_coef and lt_read_status stage nothing.
+ *    lt_clip_coef stages nothing and may be captured.
  *  - Results are bitwise reproducible: they do not depend on the grid size,
  *    the device occupancy or the stream.
  */
