@@ -195,7 +195,8 @@ def test_full_3b_model_step_parity(code_map):
     _check_code_properties(dev, code_map)
 
 
-def test_clip_stress_three_steps():
+@pytest.mark.parametrize("code_map", [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC])
+def test_clip_stress_three_steps(code_map):
     w = synth.clip_stress()
     n_threads = synth.default_threads()
     B = w.block_size
@@ -215,7 +216,7 @@ def test_clip_stress_three_steps():
             free = [tuple(a.copy() for a in blk) for blk in before]
         dev.load_grads(stream)
         _say(f"step t = {t}: GPU")
-        dev.step(t)
+        dev.step(t, code_map=code_map)
         assert lt.lt_read_status(dev.status) == lt.LT_STATUS_OK
         host_g = _full_grads(w, stream, n_threads)
         rsk, rS, rst = oracle.grad_sqnorm(host_g, n_threads=n_threads)
@@ -230,18 +231,18 @@ def test_clip_stress_three_steps():
         oracle.hybrid8bit_adamw_step([x[0] for x in lock], gs, [x[1] for x in lock],
                                      [x[2] for x in lock], [x[3] for x in lock],
                                      [x[4] for x in lock], B, step=t, coef=float(rcoef),
-                                     status=rst, n_threads=n_threads, **h)
+                                     status=rst, n_threads=n_threads, code_map=code_map, **h)
         after = dev.read_blocks(blocks)
         _compare_blocks(after, lock, f"lockstep t = {t}")
         oracle.hybrid8bit_adamw_step([x[0] for x in free], gs, [x[1] for x in free],
                                      [x[2] for x in free], [x[3] for x in free],
                                      [x[4] for x in free], B, step=t, coef=float(rcoef),
-                                     status=rst, n_threads=n_threads, **h)
+                                     status=rst, n_threads=n_threads, code_map=code_map, **h)
         _compare_blocks(after, free, f"free-running t = {t}")
         for (k, b), blk in zip(blocks, after):
             if (k, b) in zero_blocks:
                 assert not blk[1].any() and not blk[3].any() and blk[2][0] == 0 and blk[4][0] == 0
         _say(f"  {len(blocks)} sampled blocks bitwise equal (lockstep and free-running)")
-    _check_code_properties(dev)
+    _check_code_properties(dev, code_map)
     # the reading of this workload: norm ~ 1.76e7 from the +-9984 outliers
     assert 1.5e7 < float(rnorm) < 2.0e7
