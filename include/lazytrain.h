@@ -224,7 +224,8 @@ size_t lt_step_workspace_bytes(int n_tensors);
  *            holds bf16(w1), rounded to nearest even (a NaN becomes a quiet
  *            NaN), written by the step kernel from registers
  *            (+2 B/param); after a skipped step, bf16 of the unchanged weights.
- * The tensors of one call must not overlap.
+ * No array the call writes may share a byte with another array of the call
+ * (gradients may alias one another): otherwise LT_ERR_INVALID_ARG.
  */
 lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, int grad_dtype,
                                 int8_t* const* m_codes, float* const* m_absmax,
@@ -284,6 +285,9 @@ size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const i
  *                       compute_stream (synchronize it before reading results).
  *                       The three may be the same stream.  Streamed calls on one
  *                       device are serialized by the library.
+ * Host arrays of different tensors should not overlap: the call does not check it
+ * (a caller may stream one host buffer for several layers to measure transfer
+ * rates), and the results of tensors that share bytes are then undefined.
  * Pass 1 copies each layer's gradients in (2 or 4 B/param) and sums them; pass 2
  * copies weights, gradients, codes and scales in (8 or 10 B/param + 8 B/block)
  * and weights, codes and scales out (6 B/param + 8 B/block).
@@ -315,7 +319,8 @@ size_t lt_adamw_fp32_workspace_bytes(int n_tensors);
  * lt_hybrid8bit_adamw_step with m0, v0 taken from and m1, v1 stored to these
  * arrays.  coef, status and params_bf16 (NULL or a list of device bf16 copies,
  * entries may be NULL) as there.  Pointers 16-byte aligned; workspace
- * 256-byte aligned.
+ * 256-byte aligned.  As there, written arrays may not overlap any other array of
+ * the call (LT_ERR_INVALID_ARG).
  */
 lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int grad_dtype,
                           float* const* exp_avg, float* const* exp_avg_sq,

@@ -1455,6 +1455,38 @@ bool valid_hyper(double lr, double beta1, double beta2, double eps, double weigh
 
 bool valid_block_size(int B) { return B >= 64 && B <= 8192 && (B & (B - 1)) == 0; }
 
+// Byte ranges a call reads or writes, for the no-overlap rule: no array the call
+// writes may share a byte with any other array of the call (gradients, which are
+// only read, may alias one another).
+struct ByteRange {
+    uintptr_t lo, hi;  // [lo, hi)
+    bool written;
+};
+
+void add_range(std::vector<ByteRange>& v, const void* p, size_t bytes, bool written)
+{
+    if (p && bytes)
+        v.push_back({reinterpret_cast<uintptr_t>(p), reinterpret_cast<uintptr_t>(p) + bytes, written});
+}
+
+// The first pair of ranges that overlap with at least one of them written, as a
+// message; empty when there is none.
+std::string overlap_error(std::vector<ByteRange> v)
+{
+    std::sort(v.begin(), v.end(), [](const ByteRange& a, const ByteRange& b) { return a.lo < b.lo; });
+    // sweep: the furthest-reaching written range and any range seen so far
+    uintptr_t end_any = 0, end_written = 0;
+    for (const ByteRange& r : v) {
+        if (r.lo < end_written || (r.written && r.lo < end_any))
+            return "tensors of one call overlap in memory (at address " +
+                   std::to_string(static_cast<unsigned long long>(r.lo)) + ")";
+        end_any = std::max(end_any, r.hi);
+        if (r.written)
+            end_written = std::max(end_written, r.hi);
+    }
+    return std::string();
+}
+
 // The fp32 scalars of one step, each computed in fp64 and rounded once.
 StepScalars make_scalars(double lr, double beta1, double beta2, double eps, double weight_decay,
                          int64_t step)
@@ -1826,6 +1858,25 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
         if (params_bf16 && !aligned(params_bf16[k], 16))
             return fail(LT_ERR_ALIGNMENT, "params_bf16" + at + " must be 16-byte aligned");
     }
+    {
+        std::vector<ByteRange> r;
+        r.reserve(size_t(K) * 7);
+        const size_t gbytes = grad_dtype == LT_DTYPE_BF16 ? 2 : 4;
+        for (int k = 0; k < K; ++k) {
+            const size_t n = size_t(numels[k]), nb = size_t((numels[k] + block_size - 1) / block_size);
+            add_range(r, params[k], n * 4, true);
+            add_range(r, grads[k], n * gbytes, false);
+            add_range(r, m_codes[k], n, true);
+            add_range(r, v_codes[k], n, true);
+            add_range(r, m_absmax[k], nb * 4, true);
+            add_range(r, v_absmax[k], nb * 4, true);
+            if (params_bf16)
+                add_range(r, params_bf16[k], n * 2, true);
+        }
+        const std::string e = overlap_error(std::move(r));
+        if (!e.empty())
+            return fail(LT_ERR_INVALID_ARG, e);
+    }
     const StepLayout lay = step_layout(K);
     if (!workspace || !aligned(workspace, 256) || workspace_bytes < lay.total)
         return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
@@ -2126,6 +2177,23 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
         if (params_bf16 && !aligned(params_bf16[k], 16))
             return fail(LT_ERR_ALIGNMENT,
                         "params_bf16[" + std::to_string(k) + "] must be 16-byte aligned");
+    }
+    {
+        std::vector<ByteRange> r;
+        r.reserve(size_t(K) * 5);
+        const size_t gbytes = grad_dtype == LT_DTYPE_BF16 ? 2 : 4;
+        for (int k = 0; k < K; ++k) {
+            const size_t n = size_t(numels[k]);
+            add_range(r, params[k], n * 4, true);
+            add_range(r, grads[k], n * gbytes, false);
+            add_range(r, exp_avg[k], n * 4, true);
+            add_range(r, exp_avg_sq[k], n * 4, true);
+            if (params_bf16)
+                add_range(r, params_bf16[k], n * 2, true);
+        }
+        const std::string e = overlap_error(std::move(r));
+        if (!e.empty())
+            return fail(LT_ERR_INVALID_ARG, e);
     }
     const size_t desc_at = round_up(sizeof(int64_t) * (K + 1), 64);
     const size_t total = lt_adamw_fp32_workspace_bytes(K);

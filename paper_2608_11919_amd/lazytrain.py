@@ -35,6 +35,16 @@ class LazyTrainError(RuntimeError):
         self.code = code
 
 
+class NonFiniteAbort(RuntimeError):
+    """Raised by Hybrid8bitAdamW once it has seen its limit of consecutive steps
+    skipped for a non-finite gradient norm (App. C safety checks: non-finite steps
+    are skipped, and training stops after three of them in a row)."""
+
+    def __init__(self, skips: int):
+        super().__init__(f"{skips} consecutive steps skipped for non-finite gradients")
+        self.skips = skips
+
+
 def lib() -> ctypes.CDLL:
     """Loads liblazytrain.so, raising if it has not been built."""
     global _lib
@@ -498,8 +508,11 @@ class Hybrid8bitAdamW:
     without a host synchronization.  With ``slice_fraction`` None every tensor keeps
     8-bit states; otherwise lt_select_8bit_slice picks the tensors that do (the
     paper's 2% slice) and the others keep fp32 states (lt_adamw_fp32_step), all under
-    one global norm.  The caller owns the skip/abort policy: ``last_status()`` reads
-    the status word of the last step.  With ``bf16_copy`` the steps also keep
+    one global norm.  A step whose norm is not finite writes nothing (the kernels
+    skip it on the device); the object counts such skips in a row when it reads a
+    step's status (at the next ``step()`` or ``last_status()``) and raises
+    NonFiniteAbort once ``max_consecutive_skips`` of them follow one another (App. C:
+    three; None never aborts).  With ``bf16_copy`` the steps also keep
     ``params_bf16``, a bf16 copy of every parameter for the next forward pass,
     written by the step kernels (valid after the first step)."""
 
@@ -507,10 +520,14 @@ class Hybrid8bitAdamW:
                  betas=(0.9, 0.999), eps: float = 1e-8, weight_decay: float = 0.01,
                  max_norm: float = 1.0, block_size: int = 4096,
                  slice_fraction: Optional[float] = None, bf16_copy: bool = False,
-                 code_map: int = LT_MAP_LINEAR):
+                 code_map: int = LT_MAP_LINEAR, max_consecutive_skips: Optional[int] = 3):
         self.params = list(params)
         if not self.params:
             raise ValueError("no parameters")
+        if max_consecutive_skips is not None and max_consecutive_skips < 1:
+            raise ValueError("max_consecutive_skips must be >= 1 or None")
+        self.max_consecutive_skips = max_consecutive_skips
+        self.consecutive_skips = 0
         dev = self.params[0].device
         self.lr, self.betas, self.eps, self.weight_decay = lr, betas, eps, weight_decay
         self.max_norm, self.block_size, self.code_map = max_norm, block_size, code_map
@@ -567,6 +584,7 @@ class Hybrid8bitAdamW:
                                  f"{p.numel()}")
         if self._unchecked:
             self.last_status(stream)  # the bias correction needs the true step count
+        self._raise_if_aborted()
         t = self.step_count + 1
         lt_grad_sqnorm(grads, self.sq_total, self.status, stream=stream)
         clip = self.max_norm if self.max_norm is not None else math.inf
@@ -596,16 +614,29 @@ class Hybrid8bitAdamW:
 
     def last_status(self, stream=None) -> int:
         """Reads the status of the last step, waiting for that step only (not for work
-        enqueued after it); a skipped step is taken off the step count once."""
+        enqueued after it); a skipped step is taken off the step count once and
+        counted towards the consecutive-skip limit, which raises NonFiniteAbort."""
         if self._status_pending:
             self._status_event.synchronize()
             st = int(self._status_host[0])
         else:
             st = lt_read_status(self.status, stream)
-        if self._unchecked and st == LT_STATUS_NONFINITE:
-            self.step_count -= 1
+        if self._unchecked:
+            if st == LT_STATUS_NONFINITE:
+                self.step_count -= 1
+                self.consecutive_skips += 1
+            else:
+                self.consecutive_skips = 0
         self._unchecked = False
+        self._raise_if_aborted()
         return st
+
+    def _raise_if_aborted(self) -> None:
+        """Once the limit is reached every step() and last_status() raises, until the
+        caller sets consecutive_skips back (or loads a checkpoint)."""
+        if (self.max_consecutive_skips is not None and
+                self.consecutive_skips >= self.max_consecutive_skips):
+            raise NonFiniteAbort(self.consecutive_skips)
 
     def state_dict(self, stream=None) -> dict:
         """The optimizer state for a checkpoint: the step count, the hyperparameters,
@@ -617,6 +648,7 @@ class Hybrid8bitAdamW:
         host = lambda ts: [t.detach().cpu().clone() for t in ts]
         return {
             "step_count": self.step_count,
+            "consecutive_skips": self.consecutive_skips,
             "hyper": {"lr": self.lr, "betas": tuple(self.betas), "eps": self.eps,
                       "weight_decay": self.weight_decay, "max_norm": self.max_norm,
                       "block_size": self.block_size, "code_map": self.code_map},
@@ -647,4 +679,5 @@ class Hybrid8bitAdamW:
                     raise ValueError(f"{name}: shape or dtype differs from the checkpoint")
                 a.copy_(b)
         self.step_count = int(state["step_count"])
+        self.consecutive_skips = int(state.get("consecutive_skips", 0))
         self._unchecked = False

@@ -60,6 +60,42 @@ int main() {
                                  1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, host_ws,
                                  sizeof host_ws, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_grad_chunk_count(n0, 2) != 0 || lt_grad_sqnorm_workspace_bytes(nullptr, 0) == 0) ++bad;
+    // overlap rule: the addresses are compared before anything is read or launched
+    // (a host buffer stands in for device memory; no workspace, so a call that
+    // passes the overlap check stops at the workspace check)
+    alignas(256) static uint8_t mem[1 << 16];
+    int64_t n2[2] = {1024, 1024};
+    float* pw[2] = {(float*)(mem), (float*)(mem + 4096)};
+    const void* gw[2] = {mem + 8192, mem + 8192};  // one gradient for both: only read
+    int8_t* mqw[2] = {(int8_t*)(mem + 12288), (int8_t*)(mem + 13312)};
+    uint8_t* vqw[2] = {mem + 14336, mem + 15360};
+    float* maw[2] = {(float*)(mem + 16384), (float*)(mem + 16388)};
+    float* vaw[2] = {(float*)(mem + 16392), (float*)(mem + 16396)};
+    auto step8 = [&]() {
+        return lt_hybrid8bit_adamw_step(pw, gw, LT_DTYPE_BF16, mqw, maw, vqw, vaw, nullptr, n2, 2,
+                                        2048, LT_MAP_LINEAR, 1e-4, 0.9, 0.999, 1e-8, 0.01, 1,
+                                        nullptr, nullptr, nullptr, 0, nullptr);
+    };
+    if (step8() != LT_ERR_WORKSPACE) ++bad;       // disjoint, shared gradient
+    pw[1] = (float*)(mem + 4080);                 // params[1] shares the last 16 bytes of params[0]
+    if (step8() != LT_ERR_INVALID_ARG) ++bad;
+    pw[1] = (float*)(mem + 4096);
+    vaw[1] = (float*)(mem + 8192 + 2044);         // a v scale inside the gradient
+    if (step8() != LT_ERR_INVALID_ARG) ++bad;
+    vaw[1] = (float*)(mem + 16396);
+    mqw[1] = (int8_t*)(mem + 12288);              // m codes of both tensors at one address
+    if (step8() != LT_ERR_INVALID_ARG) ++bad;
+    mqw[1] = (int8_t*)(mem + 13312);
+    if (step8() != LT_ERR_WORKSPACE) ++bad;
+    float* ea[2] = {(float*)(mem + 20480), (float*)(mem + 24576)};
+    float* es[2] = {(float*)(mem + 28672), (float*)(mem + 32768)};
+    auto step32 = [&]() {
+        return lt_adamw_fp32_step(pw, gw, LT_DTYPE_BF16, ea, es, nullptr, n2, 2, 1e-4, 0.9, 0.999,
+                                  1e-8, 0.01, 1, nullptr, nullptr, nullptr, 0, nullptr);
+    };
+    if (step32() != LT_ERR_WORKSPACE) ++bad;
+    es[0] = (float*)(mem + 24576 + 4080);         // exp_avg_sq[0] shares 16 bytes with exp_avg[1]
+    if (step32() != LT_ERR_INVALID_ARG) ++bad;
     if (lt_last_error() == nullptr || lt_last_error()[0] == 0) ++bad;
     printf("host checks: %d failures; last error: %s\n", bad, lt_last_error());
     return bad != 0;

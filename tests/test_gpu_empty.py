@@ -193,3 +193,33 @@ def test_optimizer_rejects_mismatched_gradients_before_any_work():
     assert opt.step_count == 0
     opt.step([g, e])
     assert opt.last_status() == lt.LT_STATUS_OK and opt.step_count == 1
+
+
+def test_overlapping_tensors_are_rejected_before_launch():
+    buf = torch.zeros(3 * 4096, dtype=torch.float32, device=DEV)
+    g = torch.zeros(4096, dtype=torch.bfloat16, device=DEV)
+    mq = torch.zeros(2 * 4096, dtype=torch.int8, device=DEV)
+    vq = torch.zeros(4096, dtype=torch.uint8, device=DEV)
+    ma = torch.zeros(4, dtype=torch.float32, device=DEV)
+    va = torch.zeros(4, dtype=torch.float32, device=DEV)
+    # two parameters sharing 4 KB
+    with pytest.raises(lt.LazyTrainError, match="overlap") as e:
+        lt.lt_hybrid8bit_adamw_step([buf[:4096], buf[3072:3072 + 4096]], [g, g],
+                                    [mq[:4096], mq[4096:]], [ma[:2], ma[2:]],
+                                    [vq, torch.zeros(4096, dtype=torch.uint8, device=DEV)],
+                                    [va[:2], va[2:]], 2048, step=1, **HYPER)
+    assert e.value.code == 1  # LT_ERR_INVALID_ARG
+    # a written array inside a gradient
+    with pytest.raises(lt.LazyTrainError, match="overlap"):
+        lt.lt_hybrid8bit_adamw_step([buf[:4096]], [buf[4096:8192]], [mq[:4096]], [ma[:2]], [vq],
+                                    [buf[4096:4098]], 2048, step=1, **HYPER)
+    # the same gradient for two tensors is fine (only read)
+    lt.lt_hybrid8bit_adamw_step([buf[:4096], buf[4096:8192]], [g, g], [mq[:4096], mq[4096:]],
+                                [ma[:2], ma[2:]],
+                                [vq, torch.zeros(4096, dtype=torch.uint8, device=DEV)],
+                                [va[:2], va[2:]], 2048, step=1, **HYPER)
+    # fp32-state step: exp_avg sharing bytes with exp_avg_sq
+    m = torch.zeros(8192, dtype=torch.float32, device=DEV)
+    with pytest.raises(lt.LazyTrainError, match="overlap"):
+        lt.lt_adamw_fp32_step([buf[:4096]], [g], [m[:4096]], [m[2048:6144]], step=1, **HYPER)
+    torch.cuda.synchronize()

@@ -158,3 +158,53 @@ def test_checkpoint_resume_is_bitwise_uninterrupted(code_map, tmp_path):
     assert opt.last_status() == lt.LT_STATUS_OK and opt.step_count == 4
     for a, b in zip((to_host(p) for p in params), want):
         assert a.tobytes() == b.tobytes()
+
+
+def test_optimizer_aborts_after_three_consecutive_skips():
+    """App. C safety checks: a non-finite gradient skips the step; skips in a row are
+    counted when the status is read, a finite step resets the count, and the third
+    consecutive skip raises NonFiniteAbort with the weights untouched since the last
+    applied step.  max_consecutive_skips=None never aborts."""
+    rng = np.random.default_rng(46)
+    sizes = [3000, 4096]
+    w0 = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
+
+    def grads(bad):
+        g = [f32_to_bf16_bits((rng.standard_normal(n) * 1e-2).astype(np.float32)) for n in sizes]
+        if bad:
+            g[1][7] = 0x7F80  # +inf
+        return [to_dev(x) for x in g]
+
+    params = [to_dev(x) for x in w0]
+    opt = lt.Hybrid8bitAdamW(params, lr=1e-4, block_size=2048)
+    for bad in (False, True, True, False, True, True):
+        opt.step(grads(bad))
+        st = opt.last_status()
+        assert st == (lt.LT_STATUS_NONFINITE if bad else lt.LT_STATUS_OK)
+    assert opt.step_count == 2 and opt.consecutive_skips == 2
+    applied = [to_host(p).copy() for p in params]
+    opt.step(grads(True))
+    with pytest.raises(lt.NonFiniteAbort) as e:
+        opt.last_status()
+    assert e.value.skips == 3 and opt.step_count == 2
+    for a, p in zip(applied, params):
+        assert to_host(p).tobytes() == a.tobytes()
+    with pytest.raises(lt.NonFiniteAbort):  # and so does every later call
+        opt.step(grads(False))
+    opt.consecutive_skips = 0  # the caller may go on explicitly
+    opt.step(grads(False))
+    assert opt.last_status() == lt.LT_STATUS_OK and opt.step_count == 3
+
+    # the abort also comes from step() when the status was not read in between
+    opt = lt.Hybrid8bitAdamW([to_dev(x) for x in w0], lr=1e-4, block_size=2048)
+    for _ in range(3):
+        opt.step(grads(True))
+    with pytest.raises(lt.NonFiniteAbort):
+        opt.step(grads(False))
+
+    opt = lt.Hybrid8bitAdamW([to_dev(x) for x in w0], lr=1e-4, block_size=2048,
+                             max_consecutive_skips=None)
+    for _ in range(5):
+        opt.step(grads(True))
+    assert opt.last_status() == lt.LT_STATUS_NONFINITE
+    assert opt.step_count == 0 and opt.consecutive_skips == 5
