@@ -377,16 +377,19 @@ def run_streamed(args, w, dev, n_threads) -> int:
     return 0
 
 
-def stream_ceiling(n_elements: int):
+def stream_ceiling(n_elements: int, pattern: str = "step8"):
     """Runs the data-movement probe (paper_2608_11919_amd/stream_ceiling, built with
-    the library) in a child process: the step's 8 B read + 6 B write per element and
-    the norm's 2 B read per element, with no arithmetic, at this workload's size."""
+    the library) in a child process, with no arithmetic, at this workload's size: the
+    norm's 2 B read per element, and the step's byte pattern per element (step8: 8 B
+    read + 6 B written in place; step8_copy: the same + 2 B written to the bf16 copy;
+    adamw32: 14 B read + 12 B written, the fp32-state step)."""
     import subprocess
     exe = os.path.join(ROOT, "paper_2608_11919_amd", "stream_ceiling")
     if not os.path.exists(exe):
         log("stream_ceiling is not built; no ceiling reported")
         return None
-    r = subprocess.run([exe, str(n_elements), "3"], capture_output=True, text=True, timeout=300)
+    r = subprocess.run([exe, str(n_elements), "5", pattern], capture_output=True, text=True,
+                       timeout=300)
     if r.returncode != 0:
         log(f"stream_ceiling failed ({r.returncode}): {r.stderr.strip()[-200:]}")
         return None
@@ -596,18 +599,36 @@ def main() -> int:
                      "bytes_per_launch": kbytes},
         "status": st,
     }
-    if not args.no_ceiling and not idx32 and not args.bf16_copy and gb == 2:
-        log("measuring the data-movement ceiling of the same byte pattern")
-        c = stream_ceiling(w.n_params)
-        if c is not None:
+    if not args.no_ceiling and gb == 2:
+        # the probe pattern of each step kernel, at the whole model's size; the hybrid
+        # step's two kernels are priced at their own patterns' rates
+        n8 = sum(w.numels[k] for k in idx8)
+        b8 = step_kernel_bytes([w.numels[k] for k in idx8], B, gb) + (2 * n8 if args.bf16_copy else 0)
+        parts = []  # (pattern, algorithmic bytes of that kernel's launch)
+        if idx8:
+            parts.append(("step8_copy" if args.bf16_copy else "step8", b8))
+        if idx32:
+            # no probe pattern for the fp32-state step with the copy
+            parts = parts + [("adamw32", kbytes - b8)] if not args.bf16_copy else []
+        log(f"measuring the data-movement ceiling of the same byte patterns: "
+            f"{[p for p, _ in parts]}")
+        probes = [(p, nb, stream_ceiling(w.n_params, p)) for p, nb in parts]
+        if probes and all(c is not None for _, _, c in probes):
+            mix_ms = sum(c["mix_ms"] * nb / c["mix_bytes"] for _, nb, c in probes)
+            read = min((c for _, _, c in probes), key=lambda c: c["read_ms"])
+            mix_gbps = kbytes / (mix_ms * 1e-3) / 1e9
             out["ceiling"] = {
-                "probe": "stream_ceiling: the step's 8 B read + 6 B written and the norm's 2 B "
-                         "read per element, no arithmetic, same array layout and size",
-                "mix_gbps": c["mix_gbps"], "read_gbps": c["read_gbps"],
-                "step_kernel_frac_of_mix": round(achieved / c["mix_gbps"], 4),
-                "norm_pass_frac_of_read": round(nbytes / avg_norm_s / 1e9 / c["read_gbps"], 4),
-                "whole_step_ceiling_ms": round(
-                    (c["mix_ms"] * kbytes / c["mix_bytes"]) + c["read_ms"] * nbytes / c["read_bytes"], 4)}
+                "probe": "stream_ceiling: each step kernel's bytes per element (" +
+                         " + ".join(f"{p} for {nb} B" for p, nb, _ in probes) +
+                         ") and the norm's 2 B read per element, no arithmetic, same array "
+                         "layout, at the whole model's size",
+                "mix_gbps": round(mix_gbps, 1), "read_gbps": read["read_gbps"],
+                "step_kernel_frac_of_mix": round(achieved / mix_gbps, 4),
+                "norm_pass_frac_of_read": round(nbytes / avg_norm_s / 1e9 / read["read_gbps"], 4),
+                "whole_step_ceiling_ms": round(mix_ms + read["read_ms"] * nbytes /
+                                               read["read_bytes"], 4)}
+            if len(probes) > 1:
+                out["ceiling"]["patterns"] = {p: c["mix_gbps"] for p, _, c in probes}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(w, n_threads, args.cpu_seconds, code_map)

@@ -1,18 +1,26 @@
-// stream_ceiling.hip -- measures the data-movement ceiling of this GPU for the two
-// access patterns of the optimizer step, with no arithmetic:
-//   mix:  per element read 8 B (4 B weight, 2 B gradient, 1 B + 1 B codes) and
-//         write 6 B back in place (weight, two codes): the fused step's traffic;
+// stream_ceiling.hip -- measures the data-movement ceiling of this GPU for the
+// access patterns of the optimizer steps, with no arithmetic:
+//   mix (pattern "step8", the default): per element read 8 B (4 B weight, 2 B
+//         gradient, 1 B + 1 B codes) and write 6 B back in place (weight, two
+//         codes): the fused 8-bit step's traffic;
+//   mix (pattern "step8_copy"): the same plus 2 B written to a separate array (the
+//         bf16 weight copy): 8 B read, 8 B written;
+//   mix (pattern "adamw32"): read 4 B weight, 2 B gradient, 4 B + 4 B moments and
+//         write weight and moments back: 14 B read, 12 B written (the fp32-state step);
 //   read: read 2 B per element (the bf16 gradient): the sum of squares' traffic.
-// Same layout as the step (separate arrays, 16-byte vector accesses).  The mix is
-// timed in two shapes and the faster one is reported: one granule per thread per
-// workgroup iteration over contiguous per-workgroup ranges, and wave tiles of 32
+// Same layout as the steps (separate arrays, 16-byte vector accesses).  The step8
+// mix is timed in two shapes and the faster one is reported: one granule per thread
+// per workgroup iteration over contiguous per-workgroup ranges, and wave tiles of 32
 // elements per lane (a lane's granules 64 apart, as the step kernel lays them out)
-// handed to the waves in turn.  Prints one JSON line.  Usage: stream_ceiling [n] [reps]
+// handed to the waves in turn.  The other two patterns are timed as wave tiles of 16
+// and 32 elements per lane.  Prints one JSON line.
+// Usage: stream_ceiling [n] [reps] [step8 | step8_copy | adamw32]
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
 
 #define CK(x)                                                                       \
     do {                                                                            \
@@ -35,6 +43,27 @@ __device__ inline void range(int64_t iters, int64_t* b, int64_t* e)
     *e = *b + per + (i < rem ? 1 : 0);
 }
 
+// Trivial integer work that changes every word the probes store.  A word stored
+// unchanged lets the compiler (the pointers are restrict) drop it from the store and
+// the load, which would leave partial lines and fewer bytes than the steps move.
+__device__ inline void xor_words(uint4& x, const uint4& k)
+{
+    x.x ^= k.x | 1u;
+    x.y ^= k.y | 1u;
+    x.z ^= k.z | 1u;
+    x.w ^= k.w | 1u;
+}
+
+__device__ inline void mix_words(uint4& w0, uint4& w1, uint2& m, uint2& v, const uint4& g)
+{
+    xor_words(w0, g);
+    xor_words(w1, make_uint4(g.y, g.z, g.w, g.x));
+    m.x ^= g.x | 1u;
+    m.y ^= g.z | 1u;
+    v.x ^= g.y | 1u;
+    v.y ^= g.w | 1u;
+}
+
 // Elements [0, iters * 2048): granule gi (8 elements) is w[2gi..2gi+1], g[gi],
 // m[gi], v[gi]; every access is inside its array.
 __global__ __launch_bounds__(kThreads) void k_mix(uint4* __restrict__ w, const uint4* __restrict__ g,
@@ -49,8 +78,8 @@ __global__ __launch_bounds__(kThreads) void k_mix(uint4* __restrict__ w, const u
         uint4 w0 = w[2 * gi], w1 = w[2 * gi + 1];
         const uint4 gg = g[gi];
         uint2 mm = m[gi], vv = v[gi];
-        // keep the loads live with trivial integer work
-        w0.x ^= gg.x; w1.y ^= gg.y; mm.x ^= gg.z; vv.y ^= gg.w;
+        // every stored word changes, so no load or store can be narrowed
+        mix_words(w0, w1, mm, vv, gg);
         w[2 * gi] = w0;
         w[2 * gi + 1] = w1;
         m[gi] = mm;
@@ -84,16 +113,96 @@ __global__ __launch_bounds__(kThreads) void k_mix_tiles(uint4* __restrict__ w,
 #pragma unroll
         for (int j = 0; j < G; ++j) {
             const int64_t gi = t * (64 * G) + lane + 64 * j;
-            a[j].x ^= c[j].x;
-            b[j].y ^= c[j].y;
-            mm[j].x ^= c[j].z;
-            vv[j].y ^= c[j].w;
+            mix_words(a[j], b[j], mm[j], vv[j], c[j]);
             w[2 * gi] = a[j];
             w[2 * gi + 1] = b[j];
             m[gi] = mm[j];
             v[gi] = vv[j];
         }
     }
+}
+
+enum Pattern { kStep8 = 0, kStep8Copy = 1, kAdamW32 = 2 };
+
+// Wave tiles of G granules per lane for the other two patterns, laid out as in
+// k_mix_tiles: granule j of lane l in tile t is 64 G t + l + 64 j, and every stored
+// vector differs from the one loaded, so no store can be dropped.  Every access is
+// inside its array: the largest granule index is 64 G * tiles - 1 = n / 8 - 1.
+// step8_copy: w[2gi..2gi+1], g[gi], m2[gi], v2[gi] read and written back (g read
+// only), c[gi] written.  adamw32: w, m4, v4 [2gi..2gi+1] and g[gi] read, w, m4, v4
+// written back.
+template <int P, int G>
+__global__ __launch_bounds__(kThreads) void k_pattern_tiles(uint4* __restrict__ w,
+                                                           const uint4* __restrict__ g,
+                                                           uint2* __restrict__ m2,
+                                                           uint2* __restrict__ v2,
+                                                           uint4* __restrict__ m4,
+                                                           uint4* __restrict__ v4,
+                                                           uint4* __restrict__ c, int64_t tiles)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = int64_t(gridDim.x) * 4;
+    for (int64_t t = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6); t < tiles; t += waves) {
+        uint4 a[G], b[G], gg[G], ma[G], mb[G], va[G], vb[G];
+        uint2 mm[G], vv[G];
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int64_t gi = t * (64 * G) + lane + 64 * j;
+            a[j] = w[2 * gi];
+            b[j] = w[2 * gi + 1];
+            gg[j] = g[gi];
+            if (P == kAdamW32) {
+                ma[j] = m4[2 * gi];
+                mb[j] = m4[2 * gi + 1];
+                va[j] = v4[2 * gi];
+                vb[j] = v4[2 * gi + 1];
+            } else {
+                mm[j] = m2[gi];
+                vv[j] = v2[gi];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int64_t gi = t * (64 * G) + lane + 64 * j;
+            if (P == kAdamW32) {
+                xor_words(a[j], gg[j]);
+                xor_words(b[j], gg[j]);
+                xor_words(ma[j], gg[j]);
+                xor_words(mb[j], gg[j]);
+                xor_words(va[j], gg[j]);
+                xor_words(vb[j], gg[j]);
+                m4[2 * gi] = ma[j];
+                m4[2 * gi + 1] = mb[j];
+                v4[2 * gi] = va[j];
+                v4[2 * gi + 1] = vb[j];
+            } else {
+                mix_words(a[j], b[j], mm[j], vv[j], gg[j]);
+                m2[gi] = mm[j];
+                v2[gi] = vv[j];
+            }
+            w[2 * gi] = a[j];
+            w[2 * gi + 1] = b[j];
+            if (P == kStep8Copy)
+                c[gi] = make_uint4(a[j].x ^ b[j].w, a[j].y ^ b[j].z, a[j].z ^ b[j].y, a[j].w ^ b[j].x);
+        }
+    }
+}
+
+template <int P, int G>
+float time_pattern(int grid, int reps, uint4* w, const uint4* g, uint2* m2, uint2* v2, uint4* m4,
+                   uint4* v4, uint4* c, int64_t n, hipEvent_t a, hipEvent_t b)
+{
+    const int64_t tiles = n / (8 * 64 * G);
+    k_pattern_tiles<P, G><<<grid, kThreads>>>(w, g, m2, v2, m4, v4, c, tiles);  // warm
+    if (hipGetLastError() != hipSuccess || hipEventRecord(a) != hipSuccess)
+        return -1.f;
+    for (int r = 0; r < reps; ++r)
+        k_pattern_tiles<P, G><<<grid, kThreads>>>(w, g, m2, v2, m4, v4, c, tiles);
+    float ms;
+    if (hipEventRecord(b) != hipSuccess || hipEventSynchronize(b) != hipSuccess ||
+        hipEventElapsedTime(&ms, a, b) != hipSuccess)
+        return -1.f;
+    return ms / reps;
 }
 
 __global__ __launch_bounds__(kThreads) void k_read(const u32x4* __restrict__ g, int64_t iters,
@@ -115,43 +224,62 @@ int main(int argc, char** argv)
 {
     const int64_t n_req = argc > 1 ? atoll(argv[1]) : 3085844480LL;
     const int reps = argc > 2 ? atoi(argv[2]) : 3;
+    const char* pname = argc > 3 ? argv[3] : "step8";
+    const int pattern = !strcmp(pname, "step8")        ? kStep8
+                        : !strcmp(pname, "step8_copy") ? kStep8Copy
+                        : !strcmp(pname, "adamw32")    ? kAdamW32
+                                                       : -1;
     const int64_t iters = n_req / kIter;
-    const int64_t n = iters * kIter;
-    if (iters < 1 || reps < 1) {
-        fprintf(stderr, "need n >= %lld and reps >= 1\n", (long long)kIter);
+    const int64_t n = iters * kIter;  // a multiple of 2048: whole tiles for G = 2 and 4
+    if (iters < 1 || reps < 1 || pattern < 0) {
+        fprintf(stderr, "need n >= %lld, reps >= 1 and pattern step8, step8_copy or adamw32\n",
+                (long long)kIter);
         return 2;
     }
     int cus;
     CK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0));
-    uint4 *w, *g;
-    uint2 *m, *v;
+    uint4 *w, *g, *m4 = nullptr, *v4 = nullptr, *c = nullptr;
+    uint2 *m = nullptr, *v = nullptr;
     uint32_t* sink;
     CK(hipMalloc(&w, n * 4));
     CK(hipMalloc(&g, n * 2));
-    CK(hipMalloc(&m, n));
-    CK(hipMalloc(&v, n));
     CK(hipMalloc(&sink, 4));
     CK(hipMemset(w, 1, n * 4));
     CK(hipMemset(g, 2, n * 2));
-    CK(hipMemset(m, 3, n));
-    CK(hipMemset(v, 4, n));
+    if (pattern == kAdamW32) {
+        CK(hipMalloc(&m4, n * 4));
+        CK(hipMalloc(&v4, n * 4));
+        CK(hipMemset(m4, 3, n * 4));
+        CK(hipMemset(v4, 4, n * 4));
+    } else {
+        CK(hipMalloc(&m, n));
+        CK(hipMalloc(&v, n));
+        CK(hipMemset(m, 3, n));
+        CK(hipMemset(v, 4, n));
+    }
+    if (pattern == kStep8Copy) {
+        CK(hipMalloc(&c, n * 2));
+        CK(hipMemset(c, 5, n * 2));
+    }
     hipEvent_t a, b;
     CK(hipEventCreate(&a));
     CK(hipEventCreate(&b));
     float best_mix = 1e30f, best_read = 1e30f;
     for (int per_cu : {2, 4, 8}) {
         const int grid = cus * per_cu;
-        k_mix<<<grid, kThreads>>>(w, g, m, v, iters);  // warm
-        CK(hipGetLastError());
-        CK(hipEventRecord(a));
-        for (int r = 0; r < reps; ++r)
-            k_mix<<<grid, kThreads>>>(w, g, m, v, iters);
-        CK(hipEventRecord(b));
-        CK(hipEventSynchronize(b));
         float ms;
-        CK(hipEventElapsedTime(&ms, a, b));
-        if (ms / reps < best_mix)
-            best_mix = ms / reps;
+        if (pattern == kStep8) {
+            k_mix<<<grid, kThreads>>>(w, g, m, v, iters);  // warm
+            CK(hipGetLastError());
+            CK(hipEventRecord(a));
+            for (int r = 0; r < reps; ++r)
+                k_mix<<<grid, kThreads>>>(w, g, m, v, iters);
+            CK(hipEventRecord(b));
+            CK(hipEventSynchronize(b));
+            CK(hipEventElapsedTime(&ms, a, b));
+            if (ms / reps < best_mix)
+                best_mix = ms / reps;
+        }
         k_read<<<grid, kThreads>>>(reinterpret_cast<const u32x4*>(g), iters, sink);  // warm
         CK(hipGetLastError());
         CK(hipEventRecord(a));
@@ -163,8 +291,28 @@ int main(int argc, char** argv)
         if (ms / reps < best_read)
             best_read = ms / reps;
     }
+    for (int per_cu : {1, 2, 3}) {
+        if (pattern == kStep8)
+            break;
+        const int grid = cus * per_cu;
+        const float t2 = pattern == kStep8Copy
+                             ? time_pattern<kStep8Copy, 2>(grid, reps, w, g, m, v, m4, v4, c, n, a, b)
+                             : time_pattern<kAdamW32, 2>(grid, reps, w, g, m, v, m4, v4, c, n, a, b);
+        const float t4 = pattern == kStep8Copy
+                             ? time_pattern<kStep8Copy, 4>(grid, reps, w, g, m, v, m4, v4, c, n, a, b)
+                             : time_pattern<kAdamW32, 4>(grid, reps, w, g, m, v, m4, v4, c, n, a, b);
+        if (t2 < 0.f || t4 < 0.f) {
+            fprintf(stderr, "pattern kernel launch or timing failed\n");
+            return 1;
+        }
+        fprintf(stderr, "%s: %d workgroups per CU: %.4f ms (16 per lane), %.4f ms (32 per lane)\n",
+                pname, per_cu, t2, t4);
+        best_mix = fminf(best_mix, fminf(t2, t4));
+    }
     // wave tiles of 2048 elements: n is a multiple of kIter = 2048
     for (int per_cu : {1, 2, 3}) {
+        if (pattern != kStep8)
+            break;
         const int grid = cus * per_cu;
         const int64_t tiles = n / 2048;
         k_mix_tiles<<<grid, kThreads>>>(w, g, m, v, tiles);  // warm
@@ -181,15 +329,17 @@ int main(int argc, char** argv)
     }
     CK(hipDeviceSynchronize());
     // an iteration of k_read reads 256 x 16 B: 2048 bf16 gradient elements
-    const double mix_bytes = double(n) * 14.0, read_bytes = double(n) * 2.0;
-    printf("{\"n\": %lld, \"mix_bytes\": %.0f, \"mix_ms\": %.4f, \"mix_gbps\": %.1f, "
-           "\"read_bytes\": %.0f, \"read_ms\": %.4f, \"read_gbps\": %.1f}\n",
-           (long long)n, mix_bytes, best_mix, mix_bytes / best_mix / 1e6, read_bytes, best_read,
-           read_bytes / best_read / 1e6);
+    const double per_elem = pattern == kStep8 ? 14.0 : pattern == kStep8Copy ? 16.0 : 26.0;
+    const double mix_bytes = double(n) * per_elem, read_bytes = double(n) * 2.0;
+    printf("{\"n\": %lld, \"pattern\": \"%s\", \"mix_bytes\": %.0f, \"mix_ms\": %.4f, "
+           "\"mix_gbps\": %.1f, \"read_bytes\": %.0f, \"read_ms\": %.4f, \"read_gbps\": %.1f}\n",
+           (long long)n, pname, mix_bytes, best_mix, mix_bytes / best_mix / 1e6, read_bytes,
+           best_read, read_bytes / best_read / 1e6);
     CK(hipFree(w));
     CK(hipFree(g));
-    CK(hipFree(m));
-    CK(hipFree(v));
+    for (void* p : {(void*)m, (void*)v, (void*)m4, (void*)v4, (void*)c})
+        if (p)
+            CK(hipFree(p));
     CK(hipFree(sink));
     return 0;
 }
