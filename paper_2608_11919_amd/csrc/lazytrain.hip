@@ -114,9 +114,10 @@ StepLayout step_layout(int K)
 // ---------------------------------------------------- descriptor uploads
 //
 // The tensor-list descriptors are packed on the host into a pinned staging
-// slot and copied into the caller's workspace on the caller's stream, so the
-// call never blocks.  A slot is reused only after the event recorded behind
-// its copy has completed.
+// slot and copied into the caller's workspace on the caller's stream.  A slot
+// is reused only after the event recorded behind its copy has completed, so a
+// call waits on the host only when the copy of the call eight uploads earlier
+// on the device has not run yet (a caller far ahead of the GPU).
 
 struct StagingSlot {
     void* host = nullptr;
