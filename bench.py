@@ -300,7 +300,7 @@ def run_streamed(args, w, dev, n_threads) -> int:
     cs, hs, ds = torch.cuda.Stream(dev), torch.cuda.Stream(dev), torch.cuda.Stream(dev)
     slots = args.ring_slots
     nbytes = lt.lt_streamed_workspace_bytes(w.numels, first, lt.LT_DTYPE_BF16, B, slots,
-                                            args.bf16_copy)
+                                            args.bf16_copy, args.keep_grads)
     workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     acc = dev_grads = None
     if args.norm_on_arrival:
@@ -322,6 +322,7 @@ def run_streamed(args, w, dev, n_threads) -> int:
             step=t, max_norm=w.max_norm, ring_slots=slots, sq_total=S, coef=coef, status=status,
             total_norm=norm, workspace=workspace, compute_stream=cs, h2d_stream=hs,
             d2h_stream=ds, params_bf16=lists.get("wb"), norm_ready=acc is not None,
+            keep_grads=args.keep_grads,
             code_map=lt.LT_MAP_DYNAMIC if args.code_map == "dynamic" else lt.LT_MAP_LINEAR,
             **hyper)
 
@@ -343,9 +344,10 @@ def run_streamed(args, w, dev, n_threads) -> int:
     per = elapsed / args.steps
     n = w.n_params
     nb = sum(-(-x // B) for x in w.numels)
-    # pass 1 gradients (not with the norm summed on arrival); pass 2 weights, gradients,
-    # codes, scales
-    h2d = (0 if args.norm_on_arrival else n * 2) + n * 8 + nb * 8
+    # pass 1 gradients (not with the norm summed on arrival); pass 2 weights, gradients
+    # (not when pass 1 left them in HBM), codes, scales
+    once = args.keep_grads and not args.norm_on_arrival
+    h2d = (0 if args.norm_on_arrival else n * 2) + n * (6 if once else 8) + nb * 8
     d2h = n * (8 if args.bf16_copy else 6) + nb * 8  # weights, codes, scales (bf16 copy) back
     bound = max(h2d / (rates["h2d_gbps"] * 1e9), d2h / (rates["d2h_gbps"] * 1e9))
     out = {
@@ -355,6 +357,7 @@ def run_streamed(args, w, dev, n_threads) -> int:
         "data": "synthetic",
         "config": {"workload": w.name + ("+bf16-copy" if args.bf16_copy else "") +
                    ("+norm-on-arrival" if args.norm_on_arrival else "") +
+                   ("+grads-kept-in-hbm" if args.keep_grads else "") +
                    ("+dynamic-map" if args.code_map == "dynamic" else ""), "params": n,
                    "tensors": len(w.shapes), "layers": L,
                    "block_size": B, "grad_dtype": "bf16", "ring_slots": slots,
@@ -425,6 +428,9 @@ def main() -> int:
                     help="code map of the 8-bit moments")
     ap.add_argument("--bf16-copy", action="store_true",
                     help="the steps also write a bf16 copy of the updated weights (+2 B/param)")
+    ap.add_argument("--keep-grads", action="store_true",
+                    help="streamed workload: the gradients stay in HBM from the first pass to "
+                         "the second and cross the link once")
     ap.add_argument("--norm-on-arrival", action="store_true",
                     help="streamed workload: the norm is summed layer by layer from gradients "
                          "already in HBM (as they arrive in backward) and the step skips its "

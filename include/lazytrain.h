@@ -240,11 +240,12 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
  * descriptors of every layer, one fp64 partial per 8192-element chunk of the
  * whole model, and ring_slots slots each large enough for the largest layer's
  * weights, gradients, codes and scales (and its bf16 weight copy when
- * bf16_copy is nonzero: the call passes a params_bf16 list).  0 if an argument
- * is invalid. */
+ * bf16_copy is nonzero: the call passes a params_bf16 list).  With keep_grads
+ * nonzero the slots hold no gradients and every gradient gets a region of its
+ * own instead (the call passes keep_grads).  0 if an argument is invalid. */
 size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const int* layer_first,
                                    int n_layers, int grad_dtype, int block_size, int ring_slots,
-                                   int bf16_copy);
+                                   int bf16_copy, int keep_grads);
 
 /*
  * Step a11: one clipped Hybrid 8-bit AdamW step over a model whose fp32
@@ -273,6 +274,12 @@ size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const i
  *                       status (from lt_grad_sqnorm_finish over gradients summed
  *                       as they arrived); pass 1 and the finish are skipped and
  *                       the gradients are copied in once.
+ *   keep_grads          nonzero: every gradient keeps its own region of the
+ *                       workspace (sized with keep_grads = 1: 2 or 4 B/param more,
+ *                       and the slots then hold no gradient), so a gradient copied
+ *                       in by pass 1 stays in HBM for pass 2 and crosses the link
+ *                       once.  Results are bitwise those without it.  With
+ *                       norm_ready, pass 2 copies the gradients into those regions.
  *   ring_slots          device slots in the ring, 2..16 (3 lets one layer copy in
  *                       while one computes and one copies out).
  *   sq_total, total_norm (may be NULL), coef, status: device outputs as in
@@ -289,8 +296,9 @@ size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const i
  * (a caller may stream one host buffer for several layers to measure transfer
  * rates), and the results of tensors that share bytes are then undefined.
  * Pass 1 copies each layer's gradients in (2 or 4 B/param) and sums them; pass 2
- * copies weights, gradients, codes and scales in (8 or 10 B/param + 8 B/block)
- * and weights, codes and scales out (6 B/param + 8 B/block).
+ * copies weights, gradients, codes and scales in (8 or 10 B/param + 8 B/block;
+ * 6 B/param + 8 B/block with keep_grads) and weights, codes and scales out
+ * (6 B/param + 8 B/block).
  */
 lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const* grads,
                                          int grad_dtype, int8_t* const* m_codes,
@@ -301,8 +309,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                          int block_size, int code_map, double lr, double beta1,
                                          double beta2,
                                          double eps, double weight_decay, int64_t step,
-                                         float max_norm, int norm_ready, int ring_slots,
-                                         void* workspace,
+                                         float max_norm, int norm_ready, int keep_grads,
+                                         int ring_slots, void* workspace,
                                          size_t workspace_bytes, double* sq_total,
                                          float* total_norm, float* coef, int32_t* status,
                                          void* compute_stream, void* h2d_stream, void* d2h_stream);

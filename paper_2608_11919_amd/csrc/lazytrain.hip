@@ -1573,11 +1573,15 @@ struct StreamLayout {
     size_t gprefix = 0;                 // global chunk prefix, K + 1
     std::vector<size_t> sq_prefix, sq_ptrs, sq_numels, st_prefix, st_desc;  // per layer
     size_t partials = 0, sk = 0, slots = 0, slot_bytes = 0, total = 0;
+    size_t resident = 0;        // resident gradients (keep_grads), after the slots
+    std::vector<size_t> roff;   // per tensor, from `resident`
     int64_t C = 0;
 };
 
+// With keep_grads every gradient gets its own region after the slots, and the
+// slots hold no gradient.
 StreamLayout stream_layout(const int64_t* numels, int K, const int* first, int L, int gbytes, int B,
-                           int S, bool bf16_copy)
+                           int S, bool bf16_copy, bool keep_grads)
 {
     StreamLayout l;
     size_t at = 0;
@@ -1605,11 +1609,17 @@ StreamLayout stream_layout(const int64_t* numels, int K, const int* first, int L
     for (int i = 0; i < L; ++i) {
         size_t b = 0;
         for (int k = first[i]; k < first[i + 1]; ++k)
-            b = slot_tensor(b, numels[k], gbytes, B, bf16_copy).end;
+            b = slot_tensor(b, numels[k], keep_grads ? 0 : gbytes, B, bf16_copy).end;
         biggest = std::max(biggest, b);
     }
     l.slot_bytes = biggest;
-    l.total = l.slots + l.slot_bytes * size_t(S);
+    l.resident = l.slots + l.slot_bytes * size_t(S);
+    size_t r = 0;
+    for (int k = 0; keep_grads && k < K; ++k) {
+        l.roff.push_back(r);
+        r += align256(size_t(numels[k]) * gbytes);
+    }
+    l.total = l.resident + r;
     return l;
 }
 
@@ -1919,7 +1929,7 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
 
 size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const int* layer_first,
                                    int n_layers, int grad_dtype, int block_size, int ring_slots,
-                                   int bf16_copy)
+                                   int bf16_copy, int keep_grads)
 {
     if (!valid_list(numels, n_tensors) || !valid_layers(layer_first, n_layers, n_tensors) ||
         (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16) ||
@@ -1927,7 +1937,7 @@ size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const i
         return 0;
     return stream_layout(numels, n_tensors, layer_first, n_layers,
                          grad_dtype == LT_DTYPE_BF16 ? 2 : 4, block_size, ring_slots,
-                         bf16_copy != 0)
+                         bf16_copy != 0, keep_grads != 0)
         .total;
 }
 
@@ -1940,8 +1950,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                          int block_size, int code_map, double lr, double beta1,
                                          double beta2,
                                          double eps, double weight_decay, int64_t step,
-                                         float max_norm, int norm_ready, int ring_slots,
-                                         void* workspace,
+                                         float max_norm, int norm_ready, int keep_grads,
+                                         int ring_slots, void* workspace,
                                          size_t workspace_bytes, double* sq_total,
                                          float* total_norm, float* coef, int32_t* status,
                                          void* compute_stream, void* h2d_stream, void* d2h_stream)
@@ -1976,13 +1986,20 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
             return fail(LT_ERR_INVALID_ARG, "NULL host pointer at index " + std::to_string(k));
     const int gbytes = grad_dtype == LT_DTYPE_BF16 ? 2 : 4;
     const bool bf16_copy = params_bf16 != nullptr;
-    const StreamLayout lay = stream_layout(numels, K, layer_first, L, gbytes, B, S, bf16_copy);
+    const bool resident = keep_grads != 0;
+    const StreamLayout lay =
+        stream_layout(numels, K, layer_first, L, gbytes, B, S, bf16_copy, resident);
     if (!workspace || !aligned(workspace, 256) || workspace_bytes < lay.total)
         return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
                                           std::to_string(lay.total) + " bytes");
 
     auto* ws = static_cast<uint8_t*>(workspace);
     auto slot_base = [&](int layer) { return ws + lay.slots + lay.slot_bytes * size_t(layer % S); };
+    // Where tensor k's gradient sits on the device: its resident region, or the
+    // layer's slot (place = the tensor's offsets in that slot).
+    auto grad_at = [&](int k, uint8_t* base, const SlotTensor& place) {
+        return resident ? ws + lay.resident + lay.roff[k] : base + place.g;
+    };
     const int64_t unit = step_unit_elems(B, code_map);
 
     // Descriptors of every layer, each pointing into the slot the layer will use.
@@ -2003,14 +2020,14 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         sp[0] = 0;
         up[0] = 0;
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
-            const SlotTensor t = slot_tensor(at, numels[k], gbytes, B, bf16_copy);
+            const SlotTensor t = slot_tensor(at, numels[k], resident ? 0 : gbytes, B, bf16_copy);
             places[i].push_back(t);
             at = t.end;
             sp[j + 1] = sp[j] + (numels[k] + kChunk - 1) / kChunk;
-            pp[j] = reinterpret_cast<uint64_t>(base + t.g);
+            pp[j] = reinterpret_cast<uint64_t>(grad_at(k, base, t));
             np[j] = numels[k];
             up[j + 1] = up[j] + (numels[k] + unit - 1) / unit;
-            dp[j] = StepTensor{reinterpret_cast<float*>(base + t.w), base + t.g,
+            dp[j] = StepTensor{reinterpret_cast<float*>(base + t.w), grad_at(k, base, t),
                                reinterpret_cast<int8_t*>(base + t.mq),
                                reinterpret_cast<float*>(base + t.ma),
                                reinterpret_cast<uint8_t*>(base + t.vq),
@@ -2050,15 +2067,17 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
 
     // Pass 1: gradients in, chunk sums at their global indices.  Skipped when the
     // caller summed the gradients as they arrived (sq_total and status are given).
+    // Resident gradients each have their own region, so their copies wait for no
+    // slot and pass 2 does not copy them again.
     for (int i = 0; i < (norm_ready ? 0 : L); ++i) {
         const int sl = i % S;
-        if (used[sl])
+        if (used[sl] && !resident)
             LT_HIP(hipStreamWaitEvent(hs, ev.freed[sl], 0));
         uint8_t* base = slot_base(i);
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j)
             if (numels[k] > 0)
-                LT_HIP(hipMemcpyAsync(base + places[i][j].g, grads[k], size_t(numels[k]) * gbytes,
-                                      H2D, hs));
+                LT_HIP(hipMemcpyAsync(grad_at(k, base, places[i][j]), grads[k],
+                                      size_t(numels[k]) * gbytes, H2D, hs));
         LT_HIP(hipEventRecord(ev.in[sl], hs));
         LT_HIP(hipStreamWaitEvent(cs, ev.in[sl], 0));
         const int Ki = layer_first[i + 1] - layer_first[i];
@@ -2070,7 +2089,7 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                 d_partials + gprefix[layer_first[i]], cs))
             return e;
         LT_HIP(hipEventRecord(ev.freed[sl], cs));
-        used[sl] = true;
+        used[sl] = used[sl] || !resident;
     }
     if (!norm_ready) {
         const auto* d_gprefix = reinterpret_cast<const int64_t*>(ws + lay.gprefix);
@@ -2095,7 +2114,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
             if (n == 0)
                 continue;
             LT_HIP(hipMemcpyAsync(base + t.w, params[k], n * 4, H2D, hs));
-            LT_HIP(hipMemcpyAsync(base + t.g, grads[k], n * gbytes, H2D, hs));
+            if (!resident || norm_ready)  // resident gradients came in during pass 1
+                LT_HIP(hipMemcpyAsync(grad_at(k, base, t), grads[k], n * gbytes, H2D, hs));
             LT_HIP(hipMemcpyAsync(base + t.mq, m_codes[k], n, H2D, hs));
             LT_HIP(hipMemcpyAsync(base + t.vq, v_codes[k], n, H2D, hs));
             LT_HIP(hipMemcpyAsync(base + t.ma, m_absmax[k], nb * 4, H2D, hs));

@@ -79,13 +79,14 @@ def lib() -> ctypes.CDLL:
                                                ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp]
     ip = ctypes.POINTER(ctypes.c_int)
     L.lt_streamed_workspace_bytes.argtypes = [i64p, ctypes.c_int, ip, ctypes.c_int, ctypes.c_int,
-                                              ctypes.c_int, ctypes.c_int, ctypes.c_int]
+                                              ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                              ctypes.c_int]
     L.lt_streamed_workspace_bytes.restype = ctypes.c_size_t
     L.lt_streamed_hybrid8bit_adamw_step.argtypes = [
         vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, vpp, i64p, ctypes.c_int, ip, ctypes.c_int,
         ctypes.c_int, ctypes.c_int] + [ctypes.c_double] * 5 + [ctypes.c_int64, ctypes.c_float, ctypes.c_int,
-                                                 ctypes.c_int, vp, ctypes.c_size_t, vp, vp, vp,
-                                                 vp, vp, vp, vp]
+                                                 ctypes.c_int, ctypes.c_int, vp, ctypes.c_size_t,
+                                                 vp, vp, vp, vp, vp, vp, vp]
     L.lt_adamw_fp32_workspace_bytes.argtypes = [ctypes.c_int]
     L.lt_adamw_fp32_workspace_bytes.restype = ctypes.c_size_t
     L.lt_adamw_fp32_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, i64p, ctypes.c_int] + [
@@ -367,12 +368,12 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
 
 def lt_streamed_workspace_bytes(numels: Sequence[int], layer_first: Sequence[int],
                                 grad_dtype: int, block_size: int, ring_slots: int,
-                                bf16_copy: bool = False) -> int:
+                                bf16_copy: bool = False, keep_grads: bool = False) -> int:
     n = (ctypes.c_int64 * len(numels))(*numels)
     f = (ctypes.c_int * len(layer_first))(*layer_first)
     return int(lib().lt_streamed_workspace_bytes(n, len(numels), f, len(layer_first) - 1,
                                                  grad_dtype, block_size, ring_slots,
-                                                 int(bool(bf16_copy))))
+                                                 int(bool(bf16_copy)), int(bool(keep_grads))))
 
 
 def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes, v_absmax,
@@ -386,12 +387,15 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
                                       compute_stream=None, h2d_stream=None,
                                       d2h_stream=None, params_bf16=None,
                                       norm_ready: bool = False,
-                                      code_map: int = LT_MAP_LINEAR) -> None:
+                                      code_map: int = LT_MAP_LINEAR,
+                                      keep_grads: bool = False) -> None:
     """Step a11: host-resident tensors (CPU, ideally pinned) streamed layer by layer
     through HBM; scalar outputs are device tensors (see include/lazytrain.h).
     params_bf16 (optional, host bf16 tensors or None) receives the bf16 weight copy.
     With norm_ready, sq_total and status already hold S and its status (summed as the
-    gradients arrived) and the first streamed pass is skipped."""
+    gradients arrived) and the first streamed pass is skipped.  With keep_grads every
+    gradient stays in HBM from the first pass to the second (2 or 4 B/param of
+    workspace), so it crosses the link once."""
     k = len(params)
     if k == 0 or not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) ==
                       len(v_absmax) == k):
@@ -415,7 +419,7 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
     wb = _bf16_list(params_bf16, params, cpu)
     numels = [p.numel() for p in params]
     nbytes = lt_streamed_workspace_bytes(numels, layer_first, gdt, block_size, ring_slots,
-                                         wb is not None)
+                                         wb is not None, keep_grads)
     if nbytes == 0:
         raise ValueError("invalid layer_first, block_size or ring_slots")
     cs = _stream_handle(compute_stream, device)
@@ -431,7 +435,8 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
             _ptr_array(v_codes), _ptr_array(v_absmax), wb, _numel_array(params), k, first,
             len(layer_first) - 1, int(block_size), int(code_map), float(lr), float(beta1),
             float(beta2), float(eps),
-            float(weight_decay), int(step), float(max_norm), int(bool(norm_ready)), int(ring_slots),
+            float(weight_decay), int(step), float(max_norm), int(bool(norm_ready)),
+            int(bool(keep_grads)), int(ring_slots),
             workspace.data_ptr(),
             workspace.numel() * workspace.element_size(),
             _scalar(sq_total, device, torch.float64, "sq_total"),

@@ -20,7 +20,8 @@ int main() {
     if (lt_grad_chunk_count(numels.data(), (int)numels.size()) != 1 + 1 + 1 + 37 + 1 + 8) ++bad;
     int first[3] = {0, 3, 6};
     for (int bf = 0; bf < 2; ++bf)
-        if (lt_streamed_workspace_bytes(numels.data(), 6, first, 2, LT_DTYPE_BF16, 2048, 3, bf) == 0) ++bad;
+        for (int kg = 0; kg < 2; ++kg)
+            if (lt_streamed_workspace_bytes(numels.data(), 6, first, 2, LT_DTYPE_BF16, 2048, 3, bf, kg) == 0) ++bad;
     if (lt_adamw_fp32_workspace_bytes(6) == 0 || lt_grad_sqnorm_partials_workspace_bytes(6) == 0 ||
         lt_grad_sqnorm_finish_workspace_bytes(6) == 0) ++bad;
     // argument errors are reported before any device call

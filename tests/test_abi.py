@@ -77,5 +77,11 @@ def test_host_side_queries_of_the_next_rows():
     plain = lt.lt_streamed_workspace_bytes(numels, first, lt.LT_DTYPE_BF16, 2048, 3)
     copy = lt.lt_streamed_workspace_bytes(numels, first, lt.LT_DTYPE_BF16, 2048, 3, True)
     assert plain > 0 and copy > plain  # the bf16 copy needs room in every slot
+    # resident gradients: the 3 slots (sized by layer 0) lose their gradient regions,
+    # and every tensor gets one of its own, each rounded up to 256 bytes
+    keep = lt.lt_streamed_workspace_bytes(numels, first, lt.LT_DTYPE_BF16, 2048, 3,
+                                          keep_grads=True)
+    up = lambda x: -(-x // 256) * 256
+    assert keep == plain - 3 * (up(2 * 4096) + up(2 * 300001)) + sum(up(2 * n) for n in numels)
     assert lt.lt_streamed_workspace_bytes(numels, [0, 5], lt.LT_DTYPE_BF16, 2048, 3) == 0
     assert lt.lt_streamed_workspace_bytes(numels, first, lt.LT_DTYPE_BF16, 2048, 1) == 0

@@ -70,7 +70,10 @@ def test_nonfinite_part_sets_status():
     assert st == lt.LT_STATUS_NONFINITE
 
 
-def test_streamed_step_with_norm_ready():
+@pytest.mark.parametrize("keep", [False, True])
+def test_streamed_step_with_norm_ready(keep):
+    """norm_ready against the two-pass streamed step and the oracle; with keep_grads
+    pass 2 copies the gradients into their resident regions instead of the slots."""
     rng = np.random.default_rng(73)
     block = 2048
     w = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in SIZES]
@@ -104,7 +107,7 @@ def test_streamed_step_with_norm_ready():
         lt.lt_streamed_hybrid8bit_adamw_step(host.w, g_pin, host.mq, host.ma, host.vq, host.va,
                                              LAYERS, block, step=2, max_norm=1.0, ring_slots=3,
                                              sq_total=S, coef=coef, status=status,
-                                             norm_ready=ready, **HYPER)
+                                             norm_ready=ready, keep_grads=keep, **HYPER)
         torch.cuda.synchronize()
         results.append((host, to_host(S)[0], to_host(coef)[0]))
     (h0, S0, c0), (h1, S1, c1) = results

@@ -133,6 +133,7 @@ def test_random_configuration_streamed_step(seed):
     first = [0] + cuts + [len(sizes)]
     slots = int(rng.integers(2, 5))
     separate = bool(rng.integers(0, 2))
+    keep = bool(rng.integers(0, 2))
     w = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
     g = [f32_to_bf16_bits((rng.standard_t(3, size=n) * c["grad_scale"]).astype(np.float32))
          for n in sizes]
@@ -163,9 +164,9 @@ def test_random_configuration_streamed_step(seed):
                                          max_norm=c["max_norm"], ring_slots=slots, sq_total=S,
                                          coef=coef, status=status, compute_stream=streams[0],
                                          h2d_stream=streams[1], d2h_stream=streams[2],
-                                         code_map=c["code_map"], **c["hyper"])
+                                         code_map=c["code_map"], keep_grads=keep, **c["hyper"])
     (streams[0] or torch.cuda.current_stream()).synchronize()
-    what = f"seed {seed}: sizes {sizes}, layers {first}, block {B}, slots {slots}"
+    what = f"seed {seed}: sizes {sizes}, layers {first}, block {B}, slots {slots}, keep {keep}"
     assert to_host(S)[0].hex() == S_o.hex() and to_host(coef)[0] == c_o, what
     got = State(*[[t.numpy() for t in lst] for lst in (host.w, host.mq, host.ma, host.vq, host.va)])
     assert_state_equal(got, ref, what)

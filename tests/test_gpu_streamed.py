@@ -1,7 +1,8 @@
 """The layer-streamed step (host-resident state passing through a ring of device
 slots) against the resident HIP path and the oracle on the same data: norm,
 coefficient, weights, codes and scales bitwise, for 2 and 3 slots, separate and
-shared streams, two consecutive steps, ragged layers and the non-finite skip."""
+shared streams, gradients kept in HBM between the passes or copied in twice, two
+consecutive steps, ragged layers and the non-finite skip."""
 import math
 
 import numpy as np
@@ -47,7 +48,8 @@ def _host_np(st: State):
     return State(*[[t.numpy().copy() for t in lst] for lst in (st.w, st.mq, st.ma, st.vq, st.va)])
 
 
-def _streamed(host: State, grads_pinned, first, block, t, slots, streams, max_norm=1.0):
+def _streamed(host: State, grads_pinned, first, block, t, slots, streams, max_norm=1.0,
+              keep_grads=False):
     S = torch.zeros(1, dtype=torch.float64, device=DEV)
     coef = torch.zeros(1, dtype=torch.float32, device=DEV)
     norm = torch.zeros(1, dtype=torch.float32, device=DEV)
@@ -59,15 +61,17 @@ def _streamed(host: State, grads_pinned, first, block, t, slots, streams, max_no
                                          first, block, step=t, max_norm=max_norm,
                                          ring_slots=slots, sq_total=S, coef=coef, status=status,
                                          total_norm=norm, compute_stream=cs, h2d_stream=hs,
-                                         d2h_stream=ds, **HYPER)
+                                         d2h_stream=ds, keep_grads=keep_grads, **HYPER)
     (cs or torch.cuda.current_stream()).synchronize()
     return to_host(S)[0], to_host(coef)[0], int(to_host(status)[0])
 
 
-@pytest.mark.parametrize("slots,separate", [(3, True), (2, True), (3, False)])
+@pytest.mark.parametrize("slots,separate,keep", [(3, True, False), (2, True, False),
+                                                  (3, False, False), (3, True, True),
+                                                  (2, False, True)])
 @pytest.mark.parametrize("block", [2048, 256])
-def test_streamed_equals_resident_and_oracle(slots, separate, block):
-    rng, numels, first = _model(slots * 10 + block)
+def test_streamed_equals_resident_and_oracle(slots, separate, keep, block):
+    rng, numels, first = _model(slots * 10 + block + keep)
     base = _random_state(rng, numels, block)
     streams = (torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()) if separate else \
         (None, None, None)
@@ -78,7 +82,8 @@ def test_streamed_equals_resident_and_oracle(slots, separate, block):
         g = [f32_to_bf16_bits((rng.standard_t(3, size=n) * 1e-3).astype(np.float32))
              for n in numels]
         g_pin = [torch.from_numpy(x.view(np.int16)).pin_memory().view(torch.bfloat16) for x in g]
-        S_s, coef_s, st_s = _streamed(host, g_pin, first, block, t, slots, streams)
+        S_s, coef_s, st_s = _streamed(host, g_pin, first, block, t, slots, streams,
+                                      keep_grads=keep)
         # resident path on the same data
         gdev = [to_dev(x) for x in g]
         _, S_r, status_r, _, coef_r = gpu_norm_and_coef(gdev, 1.0)
@@ -96,20 +101,22 @@ def test_streamed_equals_resident_and_oracle(slots, separate, block):
         assert_state_equal(got, ref, f"streamed vs oracle, t={t}")
 
 
-def test_streamed_skips_nonfinite_and_no_clip():
+@pytest.mark.parametrize("keep", [False, True])
+def test_streamed_skips_nonfinite_and_no_clip(keep):
     rng, numels, first = _model(5)
     base = _random_state(rng, numels, 2048)
     host = _pinned(base)
     g = [f32_to_bf16_bits((rng.standard_normal(n) * 1e-3).astype(np.float32)) for n in numels]
     g[20][3] = 0x7FC0  # NaN in bf16
     g_pin = [torch.from_numpy(x.view(np.int16)).pin_memory().view(torch.bfloat16) for x in g]
-    _, _, st = _streamed(host, g_pin, first, 2048, 2, 3, (None, None, None))
+    _, _, st = _streamed(host, g_pin, first, 2048, 2, 3, (None, None, None), keep_grads=keep)
     assert st == lt.LT_STATUS_NONFINITE
     assert_state_equal(_host_np(host), base, "skipped streamed step")
     # max_norm = inf: no clipping, equal to the oracle step without a coefficient
     g[20][3] = 0
     g_pin = [torch.from_numpy(x.view(np.int16)).pin_memory().view(torch.bfloat16) for x in g]
-    _, coef, st = _streamed(host, g_pin, first, 2048, 2, 3, (None, None, None), max_norm=math.inf)
+    _, coef, st = _streamed(host, g_pin, first, 2048, 2, 3, (None, None, None), max_norm=math.inf,
+                            keep_grads=keep)
     assert st == lt.LT_STATUS_OK and coef == np.float32(1.0)
     ref = base.copy()
     oracle_step(ref, g, 2048, 2)

@@ -9,7 +9,7 @@ configuration bench.py times (27B-class decoder layers of hidden 5120, FFN 17408
   the oracle's.  (Pass 2 writes the shared host state of several layers, so its
   results are not checked here.)
 * Eight distinct layers (2.6e9 parameters, every tensor at its full size) from zero
-  state: S and the coefficient bitwise, and the updated weights, codes and scales of
+  state, with the gradients copied in twice and kept in HBM between the passes: S and the coefficient bitwise, and the updated weights, codes and scales of
   sampled blocks (the first and last block of every tensor and random ones),
   which the oracle recomputes block by block from the generator."""
 import time
@@ -102,7 +102,8 @@ def test_whole_model_norm_and_coefficient_as_benchmarked(host_model):
     _say(f"S = {S_o!r}, norm {float(n_o):.6g}, coef {float(c_o):.6g}: bitwise equal")
 
 
-def test_eight_full_size_layers_against_oracle_blocks(host_model):
+@pytest.mark.parametrize("keep", [False, True])
+def test_eight_full_size_layers_against_oracle_blocks(host_model, keep):
     w8, h = host_model
     B = w8.block_size
     # fresh state: the weights from the generator, zero codes and scales
@@ -116,12 +117,13 @@ def test_eight_full_size_layers_against_oracle_blocks(host_model):
     S, coef, norm, status = _outputs()
     cs, hs, ds = torch.cuda.Stream(DEV), torch.cuda.Stream(DEV), torch.cuda.Stream(DEV)
     cs.wait_stream(torch.cuda.current_stream())
-    _say("streamed step over 8 distinct full-size layers from zero state, t = 1")
+    _say(f"streamed step over 8 distinct full-size layers from zero state, t = 1, "
+         f"gradients kept in HBM: {keep}")
     lt.lt_streamed_hybrid8bit_adamw_step(h["w"], h["g"], h["mq"], h["ma"], h["vq"], h["va"],
                                          first, B, step=1, max_norm=w8.max_norm, ring_slots=3,
                                          sq_total=S, coef=coef, status=status, total_norm=norm,
                                          compute_stream=cs, h2d_stream=hs, d2h_stream=ds,
-                                         **_hyper(w8))
+                                         keep_grads=keep, **_hyper(w8))
     cs.synchronize()
     _, S_o, st_o = oracle.grad_sqnorm([_grad_bits(g) for g in h["g"]], n_threads=n_threads)
     _, c_o = oracle.clip_coef(S_o, w8.max_norm)
