@@ -123,7 +123,7 @@ def test_random_configuration_fp32_state_step(seed):
             assert to_host(a).tobytes() == b.tobytes(), f"seed {seed}: {name}[{k}]"
 
 
-@pytest.mark.parametrize("seed", range(200, 208))
+@pytest.mark.parametrize("seed", range(200, 212))
 def test_random_configuration_streamed_step(seed):
     c = _config(seed)
     rng, sizes, B = c["rng"], c["sizes"], c["block"]
@@ -135,8 +135,8 @@ def test_random_configuration_streamed_step(seed):
     separate = bool(rng.integers(0, 2))
     keep = bool(rng.integers(0, 2))
     w = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
-    g = [f32_to_bf16_bits((rng.standard_t(3, size=n) * c["grad_scale"]).astype(np.float32))
-         for n in sizes]
+    g32 = [(rng.standard_t(3, size=n) * c["grad_scale"]).astype(np.float32) for n in sizes]
+    g = [f32_to_bf16_bits(x) for x in g32] if c["bf16"] else g32
     base = State.zero_host(w, B)
     for k, n in enumerate(sizes):
         lo = -128 if c["code_map"] == lt.LT_MAP_DYNAMIC else -127
@@ -159,14 +159,16 @@ def test_random_configuration_streamed_step(seed):
     streams = [torch.cuda.Stream(DEV) for _ in range(3)] if separate else [None] * 3
     if separate:
         streams[0].wait_stream(torch.cuda.current_stream())
-    lt.lt_streamed_hybrid8bit_adamw_step(host.w, [pin(x.view(np.int16)) for x in g], host.mq,
+    g_host = [pin(x.view(np.int16)).view(torch.bfloat16) if c["bf16"] else pin(x) for x in g]
+    lt.lt_streamed_hybrid8bit_adamw_step(host.w, g_host, host.mq,
                                          host.ma, host.vq, host.va, first, B, step=c["step"],
                                          max_norm=c["max_norm"], ring_slots=slots, sq_total=S,
                                          coef=coef, status=status, compute_stream=streams[0],
                                          h2d_stream=streams[1], d2h_stream=streams[2],
                                          code_map=c["code_map"], keep_grads=keep, **c["hyper"])
     (streams[0] or torch.cuda.current_stream()).synchronize()
-    what = f"seed {seed}: sizes {sizes}, layers {first}, block {B}, slots {slots}, keep {keep}"
+    what = (f"seed {seed}: sizes {sizes}, layers {first}, block {B}, slots {slots}, "
+            f"keep {keep}, bf16 {c['bf16']}")
     assert to_host(S)[0].hex() == S_o.hex() and to_host(coef)[0] == c_o, what
     got = State(*[[t.numpy() for t in lst] for lst in (host.w, host.mq, host.ma, host.vq, host.va)])
     assert_state_equal(got, ref, what)
