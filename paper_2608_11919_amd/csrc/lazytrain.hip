@@ -1210,7 +1210,10 @@ struct Fp32Tensor {
 };
 static_assert(sizeof(Fp32Tensor) == 64, "descriptor is one 64-byte line");
 
-constexpr int kFp32ElemsPerLane = 16;
+// 32 elements per lane (224-230 VGPRs, 2 waves per SIMD): measured on the 3B-class
+// model with fp32 states, 1.2% faster than 16 per lane (4 waves) and 2.7% faster
+// than 8 per lane (8 waves), bitwise identical.
+constexpr int kFp32ElemsPerLane = 32;
 
 __device__ inline void load8f(const float* p, int nv, float (&x)[8])
 {
