@@ -97,6 +97,24 @@ int main() {
     if (step32() != LT_ERR_WORKSPACE) ++bad;
     es[0] = (float*)(mem + 24576 + 4080);         // exp_avg_sq[0] shares 16 bytes with exp_avg[1]
     if (step32() != LT_ERR_INVALID_ARG) ++bad;
+    // streamed step: a workspace sized for resident gradients is too small for the
+    // ring that carries them (3 slots of a 2-tensor layer), which the call reports
+    // before it touches anything
+    {
+        int64_t sn[2] = {1024, 1024};
+        int lf[2] = {0, 2};
+        const size_t kept = lt_streamed_workspace_bytes(sn, 2, lf, 1, LT_DTYPE_BF16, 2048, 3, 0, 1);
+        const size_t twice = lt_streamed_workspace_bytes(sn, 2, lf, 1, LT_DTYPE_BF16, 2048, 3, 0, 0);
+        if (!(kept > 0 && twice > kept)) ++bad;
+        static double dS; static float dc, dn; static int32_t dst;
+        for (int keep = 0; keep < 2; ++keep) {
+            const lt_err e = lt_streamed_hybrid8bit_adamw_step(
+                pw, gw, LT_DTYPE_BF16, mqw, maw, vqw, vaw, nullptr, sn, 2, lf, 1, 2048,
+                LT_MAP_LINEAR, 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, 1.0f, 0, keep, 3, mem,
+                keep ? kept - 256 : kept, &dS, &dn, &dc, &dst, nullptr, nullptr, nullptr);
+            if (e != LT_ERR_WORKSPACE) ++bad;
+        }
+    }
     if (lt_last_error() == nullptr || lt_last_error()[0] == 0) ++bad;
     printf("host checks: %d failures; last error: %s\n", bad, lt_last_error());
     return bad != 0;
