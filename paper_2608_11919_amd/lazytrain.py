@@ -686,3 +686,120 @@ class Hybrid8bitAdamW:
         self.step_count = int(state["step_count"])
         self.consecutive_skips = int(state.get("consecutive_skips", 0))
         self._unchecked = False
+
+
+class StreamedHybrid8bitAdamW:
+    """The optimizer object of the layer-streamed step (lt_streamed_hybrid8bit_adamw_step):
+    the fp32 master weights (the caller's CPU tensors, pinned for overlapped copies) and
+    the 8-bit states (pinned host memory allocated here) stay in host memory and pass
+    through HBM layer by layer, as the paper keeps parameters and optimizer states in
+    CPU memory (Sec. 3.5).  ``layer_first`` splits the parameter list into layers
+    (layer i is parameters [layer_first[i], layer_first[i + 1])).  The workspace, the
+    device scalars and three streams are allocated once.  With ``keep_grads`` (the
+    default) the gradients stay in HBM between the two passes and cross the link once.
+    ``step()`` returns when the host state is updated and gives the step's status; a
+    skipped step (non-finite norm) changes nothing and counts towards
+    ``max_consecutive_skips`` as in Hybrid8bitAdamW (NonFiniteAbort)."""
+
+    def __init__(self, params: Sequence[torch.Tensor], layer_first: Sequence[int], device,
+                 lr: float = 1e-5, betas=(0.9, 0.999), eps: float = 1e-8,
+                 weight_decay: float = 0.01, max_norm: float = 1.0, block_size: int = 4096,
+                 ring_slots: int = 3, keep_grads: bool = True, code_map: int = LT_MAP_LINEAR,
+                 max_consecutive_skips: Optional[int] = 3, grad_dtype=torch.bfloat16):
+        self.params = list(params)
+        if not self.params:
+            raise ValueError("no parameters")
+        cpu = torch.device("cpu")
+        _check_tensors(self.params, cpu, torch.float32, "params")
+        if max_consecutive_skips is not None and max_consecutive_skips < 1:
+            raise ValueError("max_consecutive_skips must be >= 1 or None")
+        if grad_dtype not in (torch.bfloat16, torch.float32):
+            raise ValueError("grad_dtype must be torch.bfloat16 or torch.float32")
+        self.device = torch.device(device)
+        self.layer_first = list(layer_first)
+        self.lr, self.betas, self.eps, self.weight_decay = lr, betas, eps, weight_decay
+        self.max_norm, self.block_size, self.code_map = max_norm, block_size, code_map
+        self.ring_slots, self.keep_grads = ring_slots, keep_grads
+        self.max_consecutive_skips = max_consecutive_skips
+        numels = [p.numel() for p in self.params]
+        gdt = LT_DTYPE_BF16 if grad_dtype == torch.bfloat16 else LT_DTYPE_F32
+        nbytes = lt_streamed_workspace_bytes(numels, self.layer_first, gdt, block_size,
+                                             ring_slots, False, keep_grads)
+        if nbytes == 0:
+            raise ValueError("invalid layer_first, block_size or ring_slots")
+        pinned = lambda n, dt: torch.zeros(n, dtype=dt, pin_memory=True)
+        nb = [-(-n // block_size) for n in numels]
+        self.m_codes = [pinned(n, torch.int8) for n in numels]
+        self.v_codes = [pinned(n, torch.uint8) for n in numels]
+        self.m_absmax = [pinned(n, torch.float32) for n in nb]
+        self.v_absmax = [pinned(n, torch.float32) for n in nb]
+        dev = self.device
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        self.sq_total = torch.zeros(1, dtype=torch.float64, device=dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.coef = torch.ones(1, dtype=torch.float32, device=dev)
+        self.total_norm = torch.zeros(1, dtype=torch.float32, device=dev)
+        self.streams = [torch.cuda.Stream(dev) for _ in range(3)]  # compute, in, out
+        self.step_count = 0  # steps applied (skipped steps do not count)
+        self.consecutive_skips = 0
+
+    def step(self, grads: Sequence[torch.Tensor]) -> int:
+        """One clipped step with one host gradient per parameter (CPU tensors, pinned
+        for overlapped copies).  Returns LT_STATUS_OK or LT_STATUS_NONFINITE once the
+        updated weights, codes and scales are in host memory."""
+        if (self.max_consecutive_skips is not None and
+                self.consecutive_skips >= self.max_consecutive_skips):
+            raise NonFiniteAbort(self.consecutive_skips)
+        grads = list(grads)
+        if len(grads) != len(self.params):
+            raise ValueError(f"step() needs one gradient per parameter: got {len(grads)} "
+                             f"for {len(self.params)} parameters")
+        cs, hs, ds = self.streams
+        cs.wait_stream(torch.cuda.current_stream(self.device))
+        t = self.step_count + 1
+        lt_streamed_hybrid8bit_adamw_step(
+            self.params, grads, self.m_codes, self.m_absmax, self.v_codes, self.v_absmax,
+            self.layer_first, self.block_size, lr=self.lr, beta1=self.betas[0],
+            beta2=self.betas[1], eps=self.eps, weight_decay=self.weight_decay, step=t,
+            max_norm=self.max_norm if self.max_norm is not None else math.inf,
+            ring_slots=self.ring_slots, sq_total=self.sq_total, coef=self.coef,
+            status=self.status, total_norm=self.total_norm, workspace=self.workspace,
+            compute_stream=cs, h2d_stream=hs, d2h_stream=ds, code_map=self.code_map,
+            keep_grads=self.keep_grads)
+        st = lt_read_status(self.status, cs)  # waits for the call's work, copies out included
+        if st == LT_STATUS_NONFINITE:
+            self.consecutive_skips += 1
+        else:
+            self.consecutive_skips = 0
+            self.step_count = t
+        if (self.max_consecutive_skips is not None and
+                self.consecutive_skips >= self.max_consecutive_skips):
+            raise NonFiniteAbort(self.consecutive_skips)
+        return st
+
+    def state_dict(self) -> dict:
+        """The step count, hyperparameters and copies of the 8-bit states (the master
+        weights are the caller's parameters)."""
+        copy = lambda ts: [t.clone() for t in ts]
+        return {"step_count": self.step_count, "consecutive_skips": self.consecutive_skips,
+                "hyper": {"lr": self.lr, "betas": tuple(self.betas), "eps": self.eps,
+                          "weight_decay": self.weight_decay, "max_norm": self.max_norm,
+                          "block_size": self.block_size, "code_map": self.code_map},
+                "m_codes": copy(self.m_codes), "m_absmax": copy(self.m_absmax),
+                "v_codes": copy(self.v_codes), "v_absmax": copy(self.v_absmax)}
+
+    def load_state_dict(self, state: dict) -> None:
+        h = state["hyper"]
+        if h["block_size"] != self.block_size or h["code_map"] != self.code_map:
+            raise ValueError("the checkpoint's block size or code map differs")
+        for name in ("m_codes", "m_absmax", "v_codes", "v_absmax"):
+            mine, saved = getattr(self, name), state[name]
+            if len(mine) != len(saved) or any(a.shape != b.shape or a.dtype != b.dtype
+                                               for a, b in zip(mine, saved)):
+                raise ValueError(f"{name}: the checkpoint's tensors differ from this optimizer's")
+            for a, b in zip(mine, saved):
+                a.copy_(b)
+        self.lr, self.betas, self.eps = h["lr"], tuple(h["betas"]), h["eps"]
+        self.weight_decay, self.max_norm = h["weight_decay"], h["max_norm"]
+        self.step_count = int(state["step_count"])
+        self.consecutive_skips = int(state.get("consecutive_skips", 0))
