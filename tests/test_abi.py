@@ -85,3 +85,21 @@ def test_host_side_queries_of_the_next_rows():
     assert keep == plain - 3 * (up(2 * 4096) + up(2 * 300001)) + sum(up(2 * n) for n in numels)
     assert lt.lt_streamed_workspace_bytes(numels, [0, 5], lt.LT_DTYPE_BF16, 2048, 3) == 0
     assert lt.lt_streamed_workspace_bytes(numels, first, lt.LT_DTYPE_BF16, 2048, 1) == 0
+
+
+def test_streamed_optimizer_rejects_bad_arguments_before_any_device_work():
+    import torch
+    import paper_2608_11919_amd as lt
+    w = [torch.zeros(4096), torch.zeros(10)]
+    with pytest.raises(ValueError):
+        lt.StreamedHybrid8bitAdamW([], [0], "cuda:0")
+    with pytest.raises(ValueError):
+        lt.StreamedHybrid8bitAdamW(w, [0, 2], "cuda:0", max_consecutive_skips=0)
+    with pytest.raises(ValueError):
+        lt.StreamedHybrid8bitAdamW(w, [0, 3], "cuda:0")  # layer_first past the list
+    with pytest.raises(ValueError):
+        lt.StreamedHybrid8bitAdamW(w, [0, 2], "cuda:0", ring_slots=1)
+    with pytest.raises(ValueError):
+        lt.StreamedHybrid8bitAdamW(w, [0, 2], "cuda:0", grad_dtype=torch.float16)
+    with pytest.raises(TypeError):
+        lt.StreamedHybrid8bitAdamW([torch.zeros(8, dtype=torch.float64)], [0, 1], "cuda:0")
