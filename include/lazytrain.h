@@ -34,21 +34,33 @@
  *    neither checked nor dereferenced.  The streamed step needs at least one
  *    tensor per layer; those may be empty too.
  *  - All work is enqueued on `stream` (a hipStream_t; NULL is the default
- *    stream) in call order.  No call synchronizes the host unless its name
- *    says so (lt_read_status).
+ *    stream) in call order.  No call waits for the device; lt_read_status is
+ *    the one entry point that synchronizes (a stream).
  *  - The return value reports argument and launch problems synchronously.
  *    Data problems (a non-finite gradient) are reported on the device through
  *    a status word.  lt_last_error() gives a message for the calling thread.
  *  - Every tensor is dense and contiguous.  Base pointers of weights,
  *    gradients and codes must be 16-byte aligned, absmax arrays 4-byte
  *    aligned, the workspace 256-byte aligned.
- *  - The workspace holds the tensor-list descriptors the call uploads (and,
+ *  - The workspace holds the tensor-list descriptors the call builds (and,
  *    for the norm, its partial sums).  Calls that overlap on the device must
- *    use different workspaces.
- *  - Each list call copies its descriptors from a library-owned pinned host
- *    buffer that later calls reuse, so the calls must not be captured into a
- *    HIP graph: a replay would copy whatever that buffer holds by then.
- *    lt_clip_coef stages nothing and may be captured.
+ *    use different workspaces.  The library remembers what it last wrote into
+ *    each workspace (by address) and copies descriptors in only when they
+ *    differ, from a library-owned pinned staging buffer (the ring of buffers
+ *    grows rather than wait for a copy still in flight).  Between calls the
+ *    caller therefore must not write into a workspace; before freeing it or
+ *    using its memory for anything else, call lt_workspace_release.  A kernel
+ *    whose workspace no longer holds the descriptors it was launched for
+ *    (checked through a per-copy tag in the workspace's first word) returns
+ *    without reading or writing any tensor; lt_grad_sqnorm and
+ *    lt_grad_sqnorm_finish then report LT_STATUS_BAD_WORKSPACE.
+ *  - HIP graph capture: a list call whose descriptors are already in its
+ *    workspace enqueues kernels only, and may be captured (also on another
+ *    stream than the one the descriptors were copied on).  It must come after
+ *    one uncaptured call with the same workspace and tensor list whose work has
+ *    completed; a captured call that would have to copy descriptors returns
+ *    LT_ERR_INVALID_ARG.  lt_clip_coef copies nothing and may always be
+ *    captured.  The streamed step (host copies) is not capturable.
  *  - Results are bitwise reproducible: they do not depend on the grid size,
  *    the device occupancy or the stream.
  */
@@ -66,13 +78,16 @@ typedef enum lt_err {
     LT_OK = 0,
     LT_ERR_INVALID_ARG = 1, /* NULL pointer, negative size, unsupported block size or dtype, bad hyperparameter */
     LT_ERR_ALIGNMENT = 2,   /* a base pointer is not aligned as stated above */
-    LT_ERR_WORKSPACE = 3,   /* workspace NULL, misaligned or smaller than the size query returns */
-    LT_ERR_HIP = 4          /* a HIP runtime call failed (device query, copy, launch, sync) */
+    LT_ERR_HIP = 3,         /* a HIP runtime call failed (device query, copy, launch, sync) */
+    LT_ERR_WORKSPACE = 4    /* workspace NULL, misaligned or smaller than the size query returns */
 } lt_err;
 
+/* The status word written on the device by the norm (and lt_clip_coef).  The
+ * steps skip, writing nothing, unless it holds LT_STATUS_OK. */
 typedef enum lt_status {
     LT_STATUS_OK = 0,
-    LT_STATUS_NONFINITE = 1 /* the global sum of squares is NaN or infinite */
+    LT_STATUS_NONFINITE = 1,    /* the global sum of squares is NaN or infinite */
+    LT_STATUS_BAD_WORKSPACE = 2 /* the workspace did not hold the call's descriptors (see above) */
 } lt_status;
 
 typedef enum lt_dtype {
@@ -83,7 +98,7 @@ typedef enum lt_dtype {
 /* Code map of the 8-bit moments (see lt_hybrid8bit_adamw_step). */
 typedef enum lt_code_map {
     LT_MAP_LINEAR = 0, /* linear absmax codes: m = q * A / 127 (int8), v = q * A / 255 (uint8) */
-    LT_MAP_DYNAMIC = 1 /* dynamic tree codes: sign-magnitude m, unsigned v, magnitudes 1e-7 .. 1 */
+    LT_MAP_DYNAMIC = 1 /* this library's decade-tree codes: sign-magnitude m, unsigned v, 1e-7 .. 1 */
 } lt_code_map;
 
 /* Bytes of device workspace lt_grad_sqnorm needs for this list (descriptors,
@@ -102,7 +117,8 @@ size_t lt_grad_sqnorm_workspace_bytes(const int64_t* numels, int n_tensors);
  *   sq_total       device double: S = S_0 + S_1 + ... in list order (0 for
  *                  an empty list).
  *   status         device int32: LT_STATUS_NONFINITE if S is NaN or
- *                  infinite, else LT_STATUS_OK.
+ *                  infinite, else LT_STATUS_OK (LT_STATUS_BAD_WORKSPACE, with
+ *                  S = NaN, if the workspace lost its descriptors; see above).
  * Accumulation is fp64 in a fixed order: each tensor is cut into 8192-element
  * chunks; in a chunk, lane l of 256 adds the squares of elements
  * 8*(l + 256*r) + e (r = 0..3, e = 0..7) in that order, a 64-lane halving
@@ -120,9 +136,14 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
  * rounded, then rounded to fp32 (ties to even);
  * coef = fminf(1, max_norm / (total_norm + 1e-6f)) in fp32.  max_norm must be
  * > 0; +INFINITY gives coef = 1 exactly.  total_norm may be NULL.
+ *   status  device int32 or NULL.  When given, it is set to LT_STATUS_OK or
+ *           LT_STATUS_NONFINITE from *sq_total, unless it already holds another
+ *           value (a library error such as LT_STATUS_BAD_WORKSPACE), which it
+ *           keeps; so a sum of squares obtained elsewhere (for example reduced
+ *           across devices) yields the status the steps read.
  */
 lt_err lt_clip_coef(const double* sq_total, float max_norm, float* total_norm, float* coef,
-                    void* stream);
+                    int32_t* status, void* stream);
 
 /* Number of 8192-element chunks of a tensor list: the number of fp64 partials
  * the sum of squares keeps for it.  0 if an argument is invalid. */
@@ -181,7 +202,10 @@ size_t lt_step_workspace_bytes(int n_tensors);
  *   v_codes[k]  device uint8[n] and v_absmax[k] device float[nb]: second
  *               moment, value = code * absmax / 255.
  * Blocks are contiguous runs of block_size elements of one tensor (the last
- * may be partial).  block_size is a power of two in [64, 8192].
+ * may be partial).  block_size is a multiple of 64 in [64, 65536] (the paper's
+ * run uses 4096, App. C variant table).  Powers of two up to 8192 take the
+ * fast kernel; other sizes a kernel that owns one block per workgroup, with
+ * the same results.
  * Per element, in fp32 with one rounding per operation (fma rounds once,
  * division and sqrt are correctly rounded):
  *   m0 = q_m * (A_m / 127), v0 = q_v * (A_v / 255), g = grad * coef,
@@ -196,11 +220,17 @@ size_t lt_step_workspace_bytes(int n_tensors);
  * clamped to [0, 255] (round half to even); a block whose new absmax or its
  * reciprocal is not finite stores zero codes and absmax 0.  These are the
  * codes of code_map = LT_MAP_LINEAR.
- *   code_map LT_MAP_DYNAMIC: both moments use dynamic tree codes instead (the
- *            paper names block-wise 8-bit AdamW states without a code map;
- *            this is the non-linear map of Dettmers et al.'s block-wise 8-bit
- *            optimizers).  A code's magnitude bits are leading zeros z (decade
- *            10^-z), an indicator one and p fraction bits f: magnitude
+ *   code_map LT_MAP_DYNAMIC: both moments use non-linear decade-tree codes
+ *            instead (the paper names block-wise 8-bit AdamW states without a
+ *            code map).  This map is this library's own, after the dynamic tree
+ *            quantization of Dettmers et al.'s block-wise 8-bit optimizers, and
+ *            differs from that construction: each code sits at the upper end
+ *            of its linear sub-interval (not its midpoint), so the top code is
+ *            exactly 1 with no separate code for it; m codes are sign-magnitude
+ *            bytes with a -0; v spans 8 decades.  Codes are therefore not
+ *            interchangeable with that map's.  A code's magnitude bits are
+ *            leading zeros z (decade 10^-z), an indicator one and p fraction
+ *            bits f: magnitude
  *            fp32((0.1 + 0.9 * ((f + 1) / 2^p)) * 10^-z), computed in fp64 in
  *            that order, 0 for the zero code.  m codes are sign-magnitude
  *            bytes (sign bit 0x80 set for m1 < 0, 7 magnitude bits, 1e-6 .. 1),
@@ -211,10 +241,12 @@ size_t lt_step_workspace_bytes(int n_tensors);
  *            same absmax and zero-block rule.  A second moment down to 5e-8 of its
  *            block's absmax keeps a nonzero code (2e-3 with the linear map).
  *   step     1-based index t of the step being applied (>= 1).
- *   lr, weight_decay >= 0; 0 <= beta1, beta2 < 1; eps >= 0; all finite.
+ *   lr, weight_decay >= 0; 0 <= beta1, beta2 < 1; eps > 0, also after its
+ *            rounding to fp32 (with eps = 0 a zero gradient on a zero second
+ *            moment divides 0 by 0); all finite.  Otherwise LT_ERR_INVALID_ARG.
  *   coef     device float or NULL (no clipping, 1.0f).
- *   status   device int32 or NULL (never skip).  When it holds
- *            LT_STATUS_NONFINITE the kernel writes nothing: weights, codes and
+ *   status   device int32 or NULL (never skip).  When it holds anything but
+ *            LT_STATUS_OK the kernel writes nothing: weights, codes and
  *            absmax stay bitwise unchanged.
  *   params_bf16  NULL, or a host list of device uint16[n] arrays (entries may
  *            be NULL: no copy of that tensor), 16-byte aligned: a bf16 copy of
@@ -352,6 +384,13 @@ lt_err lt_select_8bit_slice(const int64_t* numels, int n_tensors, double fractio
  * entry point that blocks the host).  An asynchronous device fault from
  * earlier work on the stream surfaces here as LT_ERR_HIP. */
 lt_err lt_read_status(const int32_t* status, void* stream, int32_t* out);
+
+/* Forgets what the library last wrote into `workspace` (a device pointer
+ * passed as the workspace of earlier calls; NULL or an unknown pointer is a
+ * no-op).  Call it before freeing a workspace, reusing its memory, or writing
+ * into it; the next call with it copies its descriptors in again.  Host only:
+ * it enqueues nothing and waits for nothing. */
+lt_err lt_workspace_release(const void* workspace);
 
 /* Caps the number of workgroups of the persistent kernels (0 = size the grid
  * from the device's compute units and occupancy).  Results do not depend on

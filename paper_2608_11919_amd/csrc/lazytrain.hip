@@ -28,6 +28,8 @@
 #include <cstdint>
 #include <cstring>
 #include <initializer_list>
+#include <chrono>
+#include <map>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -79,7 +81,11 @@ struct StepScalars {
 
 constexpr size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Sum-of-squares workspace: [chunk_prefix K+1][ptr K][numel K] | [partials C][S_k K]
+// Every workspace starts with kTagBytes that hold the tag of the descriptors it
+// holds (see put_descriptors); the descriptors follow.
+constexpr size_t kTagBytes = 64;
+
+// Sum-of-squares workspace: [tag][chunk_prefix K+1][ptr K][numel K] | [partials C][S_k K]
 struct SqLayout {
     size_t prefix, ptrs, numels, header_bytes, partials, sk, total;
 };
@@ -87,8 +93,8 @@ struct SqLayout {
 SqLayout sq_layout(int K, int64_t C)
 {
     SqLayout l;
-    l.prefix = 0;
-    l.ptrs = round_up(sizeof(int64_t) * (K + 1), 64);
+    l.prefix = kTagBytes;
+    l.ptrs = l.prefix + round_up(sizeof(int64_t) * (K + 1), 64);
     l.numels = l.ptrs + round_up(sizeof(uint64_t) * K, 64);
     l.header_bytes = l.numels + round_up(sizeof(int64_t) * K, 64);
     l.partials = round_up(l.header_bytes, 256);
@@ -97,7 +103,7 @@ SqLayout sq_layout(int K, int64_t C)
     return l;
 }
 
-// Step workspace: [tile_prefix K+1][StepTensor K]
+// Step workspace: [tag][tile_prefix K+1][StepTensor K]
 struct StepLayout {
     size_t prefix, desc, total;
 };
@@ -105,19 +111,34 @@ struct StepLayout {
 StepLayout step_layout(int K)
 {
     StepLayout l;
-    l.prefix = 0;
-    l.desc = round_up(sizeof(int64_t) * (K + 1), 64);
+    l.prefix = kTagBytes;
+    l.desc = l.prefix + round_up(sizeof(int64_t) * (K + 1), 64);
     l.total = round_up(l.desc + sizeof(StepTensor) * K, 256);
     return l;
 }
 
 // ---------------------------------------------------- descriptor uploads
 //
-// The tensor-list descriptors are packed on the host into a pinned staging
-// slot and copied into the caller's workspace on the caller's stream.  A slot
-// is reused only after the event recorded behind its copy has completed, so a
-// call waits on the host only when the copy of the call eight uploads earlier
-// on the device has not run yet (a caller far ahead of the GPU).
+// A list call builds its descriptors on the host as an image of the head of its
+// workspace.  The library remembers, per workspace address, the image it last
+// copied there; when a call's image is the same, nothing is copied, so a caller
+// that repeats a step over the same tensors stages nothing on the host after the
+// first call, and those calls can be captured into a HIP graph.
+//
+// Each copy writes a new 64-bit tag into the workspace's first word, and the
+// kernels receive the tag by value: a kernel whose workspace does not hold its
+// tag (the caller wrote into the workspace, or freed it and the address came back
+// for another use) returns before it reads a descriptor, instead of following
+// stale pointers.  lt_workspace_release makes the library forget a workspace.
+//
+// Images are staged in pinned host slots.  A slot is reused once the copy out of
+// it has run (checked without waiting); when the next slot is still in use, the
+// ring grows by one slot rather than wait, so no call waits on the host.
+
+struct WsGuard {
+    const uint64_t* at;  // the workspace's tag word
+    uint64_t tag;        // the tag of the descriptors this launch expects
+};
 
 struct StagingSlot {
     void* host = nullptr;
@@ -126,19 +147,31 @@ struct StagingSlot {
     bool pending = false;
 };
 
-constexpr int kSlots = 8;
+// What a workspace holds: the image last copied into it, its tag, and an event
+// behind that copy on the stream that made it.
+struct CachedImage {
+    std::vector<uint8_t> image;
+    uint64_t tag = 0;
+    hipEvent_t copied = nullptr;
+    hipStream_t stream = nullptr;
+};
+
 constexpr int kMaxDevices = 64;
 
 struct DeviceState {
     std::mutex mu;
-    StagingSlot slots[kSlots];
-    int next = 0;
+    std::vector<StagingSlot> slots;
+    size_t next = 0;
     int cu_count = 0;
-    std::unordered_map<const void*, int> occupancy;  // workgroups per CU, by kernel
+    std::map<std::pair<const void*, size_t>, int> occupancy;  // workgroups per CU, by kernel and LDS
+    std::unordered_map<const void*, CachedImage> cache;        // by workspace address
+    std::vector<hipEvent_t> spare_events;
+    std::vector<void*> retired;  // staging buffers outgrown; freed never (a free may synchronize)
 };
 
 DeviceState g_dev[kMaxDevices];
 std::atomic<int> g_max_workgroups{0};
+std::atomic<uint64_t> g_tag_counter{0};
 
 lt_err current_device(int* dev)
 {
@@ -148,34 +181,114 @@ lt_err current_device(int* dev)
     return LT_OK;
 }
 
-lt_err upload(const void* src, size_t bytes, void* dst, hipStream_t stream)
+uint64_t mix64(uint64_t z)
+{
+    z += 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// A tag no earlier copy of this process wrote, and unlikely to be found in
+// memory by accident (never 0).
+uint64_t fresh_tag()
+{
+    static const uint64_t salt =
+        mix64(uint64_t(reinterpret_cast<uintptr_t>(&g_tag_counter)) ^
+              uint64_t(std::chrono::steady_clock::now().time_since_epoch().count()));
+    const uint64_t t = mix64(salt ^ g_tag_counter.fetch_add(1));
+    return t ? t : 1;
+}
+
+lt_err stream_capturing(hipStream_t st, bool* capturing)
+{
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    LT_HIP(hipStreamIsCapturing(st, &cs));
+    *capturing = cs != hipStreamCaptureStatusNone;
+    return LT_OK;
+}
+
+// Makes the workspace `ws` hold `image` (the bytes of its head; the first
+// kTagBytes are the tag slot, filled here) before the work enqueued next on `st`
+// reads it, and returns the guard that work's kernels check.
+lt_err put_descriptors(std::vector<uint8_t>& image, void* ws, hipStream_t st, WsGuard* guard)
 {
     int dev;
     if (lt_err e = current_device(&dev))
         return e;
+    bool capturing;
+    if (lt_err e = stream_capturing(st, &capturing))
+        return e;
     DeviceState& ds = g_dev[dev];
     std::lock_guard<std::mutex> lock(ds.mu);
+    CachedImage& c = ds.cache[ws];
+    guard->at = static_cast<const uint64_t*>(ws);
+    const size_t n = image.size();
+    if (c.tag != 0 && c.image.size() == n &&
+        std::memcmp(c.image.data() + kTagBytes, image.data() + kTagBytes, n - kTagBytes) == 0) {
+        // Already in place.  Work on another stream waits for the copy; under
+        // capture the copy must have completed before capture began (the header
+        // says so), since a graph cannot wait on work outside it.
+        if (!capturing && st != c.stream)
+            LT_HIP(hipStreamWaitEvent(st, c.copied, 0));
+        guard->tag = c.tag;
+        return LT_OK;
+    }
+    if (capturing)
+        return fail(LT_ERR_INVALID_ARG,
+                    "the descriptors of this tensor list are not in the workspace: make one "
+                    "uncaptured call with this workspace and list, and let it complete, before "
+                    "capturing");
+    const uint64_t tag = fresh_tag();
+    std::memcpy(image.data(), &tag, sizeof(tag));
+
+    if (ds.slots.empty())
+        ds.slots.resize(8);
+    if (ds.next >= ds.slots.size())
+        ds.next = 0;
+    {
+        StagingSlot& s = ds.slots[ds.next];
+        if (s.pending) {
+            const hipError_t q = hipEventQuery(s.done);
+            if (q == hipSuccess)
+                s.pending = false;
+            else if (q == hipErrorNotReady)
+                ds.slots.insert(ds.slots.begin() + ptrdiff_t(ds.next), StagingSlot{});  // grow
+            else
+                return fail(LT_ERR_HIP, std::string("hipEventQuery: ") + hipGetErrorString(q));
+        }
+    }
     StagingSlot& s = ds.slots[ds.next];
-    ds.next = (ds.next + 1) % kSlots;
+    ds.next += 1;
     if (!s.done)
         LT_HIP(hipEventCreateWithFlags(&s.done, hipEventDisableTiming));
-    if (s.pending) {
-        LT_HIP(hipEventSynchronize(s.done));
-        s.pending = false;
-    }
-    if (s.cap < bytes) {
+    if (s.cap < n) {
         if (s.host)
-            LT_HIP(hipHostFree(s.host));
+            ds.retired.push_back(s.host);
         s.host = nullptr;
         s.cap = 0;
-        size_t cap = round_up(std::max(bytes, size_t(4096)), 4096);
+        const size_t cap = round_up(std::max(n, size_t(4096)), 4096);
         LT_HIP(hipHostMalloc(&s.host, cap, hipHostMallocDefault));
         s.cap = cap;
     }
-    std::memcpy(s.host, src, bytes);
-    LT_HIP(hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream));
-    LT_HIP(hipEventRecord(s.done, stream));
+    std::memcpy(s.host, image.data(), n);
+    LT_HIP(hipMemcpyAsync(ws, s.host, n, hipMemcpyHostToDevice, st));
+    LT_HIP(hipEventRecord(s.done, st));
     s.pending = true;
+
+    if (!c.copied) {
+        if (!ds.spare_events.empty()) {
+            c.copied = ds.spare_events.back();
+            ds.spare_events.pop_back();
+        } else {
+            LT_HIP(hipEventCreateWithFlags(&c.copied, hipEventDisableTiming));
+        }
+    }
+    LT_HIP(hipEventRecord(c.copied, st));
+    c.image = image;
+    c.tag = tag;
+    c.stream = st;
+    guard->tag = tag;
     return LT_OK;
 }
 
@@ -201,17 +314,17 @@ lt_err compute_units(int* cus)
 }
 
 // Persistent grid: enough workgroups to fill every CU at the kernel's
-// occupancy, never more than there are work units.  The occupancy of each
-// kernel is queried once per device.
+// occupancy (with `lds` bytes of dynamic LDS per workgroup), never more than
+// there are work units.  The occupancy of each kernel is queried once per device.
 template <typename Kernel>
-lt_err grid_size(Kernel kernel, int64_t units, int* grid)
+lt_err grid_size(Kernel kernel, int64_t units, int* grid, size_t lds = 0)
 {
     int cus, dev;
     if (lt_err e = compute_units(&cus))
         return e;
     if (lt_err e = current_device(&dev))
         return e;
-    const void* key = reinterpret_cast<const void*>(kernel);
+    const auto key = std::make_pair(reinterpret_cast<const void*>(kernel), lds);
     int per_cu = 0;
     {
         std::lock_guard<std::mutex> lock(g_dev[dev].mu);
@@ -220,7 +333,7 @@ lt_err grid_size(Kernel kernel, int64_t units, int* grid)
             per_cu = it->second;
     }
     if (per_cu <= 0) {
-        LT_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0));
+        LT_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds));
         per_cu = std::max(per_cu, 1);
         std::lock_guard<std::mutex> lock(g_dev[dev].mu);
         g_dev[dev].occupancy[key] = per_cu;
@@ -369,6 +482,9 @@ __device__ inline int find_tensor(const int64_t* __restrict__ prefix, int n_tens
     return lo;
 }
 
+// True when the workspace holds the descriptors this launch was given the tag of.
+__device__ inline bool guard_ok(const WsGuard& g) { return *g.at == g.tag; }
+
 // ------------------------------------------------------- a1: chunk sums
 
 // One lane's share of a chunk: granules lane + 256*r, r = 0..3.
@@ -418,7 +534,8 @@ constexpr int kSqChunksPerIter = 2;
 
 // Each iteration takes U consecutive chunks.
 template <typename GT>
-__global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __restrict__ chunk_prefix,
+__global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(WsGuard guard,
+                                                            const int64_t* __restrict__ chunk_prefix,
                                                             const uint64_t* __restrict__ ptrs,
                                                             const int64_t* __restrict__ numels,
                                                             int n_tensors, int64_t n_chunks,
@@ -426,6 +543,8 @@ __global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __res
 {
     constexpr int U = kSqChunksPerIter;
     __shared__ double wave_sum[2][U][4];
+    if (!guard_ok(guard))
+        return;
     const int lane = threadIdx.x;
     const int wave = lane >> 6;
     const int64_t n_iter = (n_chunks + U - 1) / U;
@@ -479,11 +598,14 @@ __global__ __launch_bounds__(kThreads) void k_sqnorm_chunks(const int64_t* __res
 
 // ------------------------------------------------- a2: fixed-order finish
 
-__global__ __launch_bounds__(kThreads) void k_sqnorm_finish(const int64_t* __restrict__ chunk_prefix,
+__global__ __launch_bounds__(kThreads) void k_sqnorm_finish(WsGuard guard,
+                                                            const int64_t* __restrict__ chunk_prefix,
                                                             const double* __restrict__ partials,
                                                             double* __restrict__ sk)
 {
     __shared__ double acc[kThreads];
+    if (!guard_ok(guard))
+        return;
     constexpr int U = 8;  // loads in flight per accumulator; the additions stay in order
     const int k = blockIdx.x;
     const int t = threadIdx.x;
@@ -519,12 +641,22 @@ __global__ __launch_bounds__(kThreads) void k_sqnorm_finish(const int64_t* __res
     }
 }
 
-__global__ __launch_bounds__(256) void k_sqnorm_total(const double* __restrict__ sk, int n_tensors,
+// A workspace that does not hold this launch's descriptors (see guard_ok) gives
+// S = NaN and LT_STATUS_BAD_WORKSPACE, which every step then skips on.
+__global__ __launch_bounds__(256) void k_sqnorm_total(WsGuard guard, const double* __restrict__ sk,
+                                                      int n_tensors,
                                                       double* __restrict__ sk_out,
                                                       double* __restrict__ sq_total,
                                                       int32_t* __restrict__ status)
 {
     __shared__ double batch[1024];
+    if (!guard_ok(guard)) {
+        if (threadIdx.x == 0) {
+            *sq_total = __builtin_nan("");
+            *status = LT_STATUS_BAD_WORKSPACE;
+        }
+        return;
+    }
     double S = 0.0;  // kept by thread 0: the list-order sum
     for (int k0 = 0; k0 < n_tensors; k0 += 1024) {
         const int n = min(1024, n_tensors - k0);
@@ -618,17 +750,26 @@ __device__ float norm_from_sum_of_squares(double S)
     return f;
 }
 
+// status (may be null): OK or NONFINITE from S, unless it holds another value
+// (a library error), which it keeps.
 __global__ __launch_bounds__(64) void k_clip_coef(const double* __restrict__ sq_total, float max_norm,
                                                   float* __restrict__ total_norm,
-                                                  float* __restrict__ coef)
+                                                  float* __restrict__ coef,
+                                                  int32_t* __restrict__ status)
 {
     if (threadIdx.x != 0)
         return;
-    const float norm = norm_from_sum_of_squares(*sq_total);
+    const double S = *sq_total;
+    const float norm = norm_from_sum_of_squares(S);
     const float c = max_norm / (norm + 1e-6f);
     if (total_norm)
         *total_norm = norm;
     *coef = fminf(1.0f, c);
+    if (status) {
+        const int32_t old = *status;
+        if (old == LT_STATUS_OK || old == LT_STATUS_NONFINITE)
+            *status = isfinite(S) ? LT_STATUS_OK : LT_STATUS_NONFINITE;
+    }
 }
 
 // ------------------------------------------------------ a4-a10: fused step
@@ -956,7 +1097,8 @@ constexpr int kMapLinear = 0, kMapDynamic = 1;
 // instantiation keeps the copy's code out of the launches that do not).
 // MAP: the code map of both moments, kMapLinear or kMapDynamic.
 template <typename GT, int B, bool WB, int MAP>
-__global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restrict__ unit_prefix,
+__global__ __launch_bounds__(kThreads) void k_adamw8_step(WsGuard guard,
+                                                          const int64_t* __restrict__ unit_prefix,
                                                           const StepTensor* __restrict__ desc,
                                                           int n_tensors, int64_t n_units,
                                                           StepScalars s,
@@ -967,7 +1109,9 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
     constexpr int E = Geo::E, G = Geo::G, W = Geo::W, L = Geo::L, UNIT = Geo::UNIT, PH = Geo::PH;
     __shared__ float red[2][2][4];  // [buffer][m, v][wave], used when W > 1
 
-    if (status_ptr && *status_ptr == LT_STATUS_NONFINITE)
+    if (!guard_ok(guard))
+        return;  // the workspace does not hold this launch's descriptors
+    if (status_ptr && *status_ptr != LT_STATUS_OK)
         return;  // skipped step: nothing is written
     const float coef = coef_ptr ? *coef_ptr : 1.0f;
     const int lane = threadIdx.x & 63;
@@ -1191,6 +1335,198 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(const int64_t* __restr
     }
 }
 
+// ---------------------------------------- a4-a10: any block size (generic)
+//
+// Block sizes outside the set above (any multiple of 64 up to 65536, besides
+// the powers of two up to 8192) take this kernel.  It computes exactly what
+// k_adamw8_step computes, in a simpler shape: a workgroup owns one block at a
+// time and thread t takes the block's granules t, t + 256, ...  Pass 1 updates the
+// moments and the weights and finds the block maxima; pass 2 requantizes.  The
+// moments m1 and v1 reach pass 2 through LDS when the block's 8 B per element
+// fit (STASH, B <= kGenericStashMax); otherwise pass 2 reads the block's
+// gradients and old codes again and repeats pass 1's moment operations, which
+// give the same bits (4 B per element more traffic with bf16 gradients).  Only
+// the thread that wrote a stash entry reads it.
+constexpr int kGenericStashMax = 8192;
+
+// The moments of one granule from its loaded inputs (linear map: step_m, step_v;
+// dynamic map: the tables and the stored absmax).  Both passes call this.
+template <typename GT, int MAP>
+__device__ inline void granule_moments(const StepIn<GT>& in, float step_m, float step_v, float a_m,
+                                       float a_v, float coef, const StepScalars& s,
+                                       const dyn::LdsTables& tab, float (&m1)[8], float (&v1)[8])
+{
+    float g[8];
+    unpack8(in.g, g);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const uint32_t mw = e < 4 ? in.m.x : in.m.y;
+        const uint32_t vw = e < 4 ? in.v.x : in.v.y;
+        float m0, v0;
+        if constexpr (MAP == kMapLinear) {
+            m0 = float(int8_t(mw >> (8 * (e & 3)))) * step_m;
+            v0 = float((vw >> (8 * (e & 3))) & 0xFFu) * step_v;
+        } else {
+            m0 = tab.dm[(mw >> (8 * (e & 3))) & 0xFFu] * a_m;
+            v0 = tab.dv[(vw >> (8 * (e & 3))) & 0xFFu] * a_v;
+        }
+        const float gc = g[e] * coef;
+        m1[e] = __builtin_fmaf(s.beta1, m0, s.c1 * gc);
+        v1[e] = __builtin_fmaf(s.beta2, v0, s.c2 * (gc * gc));
+    }
+}
+
+template <typename GT>
+__device__ inline void load_granule(const StepTensor& d, int64_t ei, int nv, StepIn<GT>& in)
+{
+    if (nv >= kGranule)
+        load_step_full(d, ei, in);
+    else
+        load_step_ragged(d, ei, nv, in);
+}
+
+template <typename GT, bool WB, int MAP, bool STASH>
+__global__ __launch_bounds__(kThreads) void k_adamw8_generic(WsGuard guard,
+                                                             const int64_t* __restrict__ unit_prefix,
+                                                             const StepTensor* __restrict__ desc,
+                                                             int n_tensors, int64_t n_units, int B,
+                                                             StepScalars s,
+                                                             const float* __restrict__ coef_ptr,
+                                                             const int32_t* __restrict__ status_ptr)
+{
+    extern __shared__ float stash[];  // STASH: m1 at [0, B), v1 at [B, 2B)
+    __shared__ float red[2][2][4];    // [buffer][m, v][wave]
+    __shared__ __align__(16) uint8_t dyn_lds[MAP == kMapDynamic ? sizeof(dyn::LdsTables) : 16];
+    const dyn::LdsTables& tab = *reinterpret_cast<const dyn::LdsTables*>(dyn_lds);
+
+    if (!guard_ok(guard))
+        return;  // the workspace does not hold this launch's descriptors
+    if (status_ptr && *status_ptr != LT_STATUS_OK)
+        return;  // skipped step: nothing is written
+    const float coef = coef_ptr ? *coef_ptr : 1.0f;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    if constexpr (MAP == kMapDynamic) {
+        const auto* src = reinterpret_cast<const uint32_t*>(&dyn::kTables);
+        auto* dst = reinterpret_cast<uint32_t*>(dyn_lds);
+        for (int i = t; i < int(sizeof(dyn::LdsTables) / 4); i += kThreads)
+            dst[i] = src[i];
+        __syncthreads();
+    }
+
+    int k = int64_t(blockIdx.x) < n_units ? find_tensor(unit_prefix, n_tensors, blockIdx.x) : 0;
+    int buf = 0;
+    for (int64_t u = blockIdx.x; u < n_units; u += gridDim.x, buf ^= 1) {
+        while (u >= unit_prefix[k + 1])
+            ++k;
+        const StepTensor d = desc[k];
+        const int64_t blk = u - unit_prefix[k];
+        const int64_t e0 = blk * B;
+        const int len = int(i64min(B, d.numel - e0));  // >= 1
+        const int n_gran = (len + kGranule - 1) / kGranule;
+        const float a_m = gp(d.ma)[blk], a_v = gp(d.va)[blk];
+        const float step_m = MAP == kMapLinear ? a_m / 127.0f : 0.0f;
+        const float step_v = MAP == kMapLinear ? a_v / 255.0f : 0.0f;
+
+        // pass 1: moments, weights, block maxima
+        float amax_m = 0.0f, amax_v = 0.0f;
+        for (int gi = t; gi < n_gran; gi += kThreads) {
+            const int o = kGranule * gi;
+            const int nv = min(kGranule, len - o);
+            StepIn<GT> in;
+            load_granule(d, e0 + o, nv, in);
+            float m1[8], v1[8], w[8];
+            granule_moments<GT, MAP>(in, step_m, step_v, a_m, a_v, coef, s, tab, m1, v1);
+            w[0] = __uint_as_float(in.w[0].x); w[1] = __uint_as_float(in.w[0].y);
+            w[2] = __uint_as_float(in.w[0].z); w[3] = __uint_as_float(in.w[0].w);
+            w[4] = __uint_as_float(in.w[1].x); w[5] = __uint_as_float(in.w[1].y);
+            w[6] = __uint_as_float(in.w[1].z); w[7] = __uint_as_float(in.w[1].w);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float den = __builtin_fmaf(sqrtf(v1[e]), s.rbc2, s.eps);
+                w[e] = __builtin_fmaf(-s.step_size, m1[e] / den, w[e] * s.decay);
+                amax_m = fmaxf(amax_m, fabsf(m1[e]));
+                amax_v = fmaxf(amax_v, v1[e]);
+                if constexpr (STASH) {
+                    stash[o + e] = m1[e];
+                    stash[B + o + e] = v1[e];
+                }
+            }
+            if (nv >= kGranule) {
+                store16f(d.w + e0 + o, w[0], w[1], w[2], w[3]);
+                store16f(d.w + e0 + o + 4, w[4], w[5], w[6], w[7]);
+            } else {
+                for (int e = 0; e < nv; ++e)
+                    gp(d.w)[e0 + o + e] = w[e];
+            }
+            if (WB && d.wb)
+                store_bf16x8(d.wb + e0 + o, nv, w);
+        }
+        amax_m = wave_max_xor(amax_m, 64);
+        amax_v = wave_max_xor(amax_v, 64);
+        if (lane == 0) {
+            red[buf][0][wave] = amax_m;
+            red[buf][1][wave] = amax_v;
+        }
+        __syncthreads();  // also orders this buffer's reads before its next write, two blocks on
+        amax_m = fmaxf(fmaxf(red[buf][0][0], red[buf][0][1]), fmaxf(red[buf][0][2], red[buf][0][3]));
+        amax_v = fmaxf(fmaxf(red[buf][1][0], red[buf][1][1]), fmaxf(red[buf][1][2], red[buf][1][3]));
+        const float inv_m = (MAP == kMapLinear ? 127.0f : 1.0f) / amax_m;
+        const float inv_v = (MAP == kMapLinear ? 255.0f : 1.0f) / amax_v;
+        const bool ok_m = isfinite(amax_m) && isfinite(inv_m);
+        const bool ok_v = isfinite(amax_v) && isfinite(inv_v);
+
+        // pass 2: requantize
+        for (int gi = t; gi < n_gran; gi += kThreads) {
+            const int o = kGranule * gi;
+            const int nv = min(kGranule, len - o);
+            float m1[8], v1[8];
+            if constexpr (STASH) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    m1[e] = stash[o + e];
+                    v1[e] = stash[B + o + e];
+                }
+            } else {
+                StepIn<GT> in;
+                load_granule(d, e0 + o, nv, in);
+                granule_moments<GT, MAP>(in, step_m, step_v, a_m, a_v, coef, s, tab, m1, v1);
+            }
+            uint32_t bm[8], bv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                if constexpr (MAP == kMapLinear) {
+                    bm[e] = uint32_t(int32_t(fminf(fmaxf(rintf(m1[e] * inv_m), -127.0f), 127.0f))) & 0xFFu;
+                    bv[e] = uint32_t(fminf(fmaxf(rintf(v1[e] * inv_v), 0.0f), 255.0f));
+                } else {
+                    bm[e] = dyn::encode<dyn::kBaseM, dyn::kTopM>(tab.em, fabsf(m1[e]) * inv_m) |
+                            (m1[e] < 0.0f ? 0x80u : 0u);
+                    bv[e] = dyn::encode<dyn::kBaseV, dyn::kTopV>(tab.ev, v1[e] * inv_v);
+                }
+                if (!ok_m)
+                    bm[e] = 0u;
+                if (!ok_v)
+                    bv[e] = 0u;
+            }
+            const int64_t ei = e0 + o;
+            if (nv >= kGranule) {
+                store8(d.mq + ei, bm[0] | (bm[1] << 8) | (bm[2] << 16) | (bm[3] << 24),
+                       bm[4] | (bm[5] << 8) | (bm[6] << 16) | (bm[7] << 24));
+                store8(d.vq + ei, bv[0] | (bv[1] << 8) | (bv[2] << 16) | (bv[3] << 24),
+                       bv[4] | (bv[5] << 8) | (bv[6] << 16) | (bv[7] << 24));
+            } else {
+                for (int e = 0; e < nv; ++e) {
+                    gp(d.mq)[ei + e] = int8_t(bm[e]);
+                    gp(d.vq)[ei + e] = uint8_t(bv[e]);
+                }
+            }
+        }
+        if (t == 0) {
+            gp(d.ma)[blk] = ok_m ? amax_m : 0.0f;
+            gp(d.va)[blk] = ok_v ? amax_v : 0.0f;
+        }
+    }
+}
+
 // ------------------------------------------ f1: fp32-state fused AdamW
 //
 // The part of the hybrid operator that keeps fp32 moments (the role DeepSpeed
@@ -1242,7 +1578,8 @@ __device__ inline void store8f(float* p, int nv, const float (&x)[8])
 }
 
 template <typename GT, bool WB>
-__global__ __launch_bounds__(kThreads) void k_adamw32_step(const int64_t* __restrict__ unit_prefix,
+__global__ __launch_bounds__(kThreads) void k_adamw32_step(WsGuard guard,
+                                                           const int64_t* __restrict__ unit_prefix,
                                                            const Fp32Tensor* __restrict__ desc,
                                                            int n_tensors, int64_t n_units,
                                                            StepScalars s,
@@ -1250,7 +1587,9 @@ __global__ __launch_bounds__(kThreads) void k_adamw32_step(const int64_t* __rest
                                                            const int32_t* __restrict__ status_ptr)
 {
     constexpr int E = kFp32ElemsPerLane, G = E / kGranule, SPAN = 64 * E;
-    if (status_ptr && *status_ptr == LT_STATUS_NONFINITE)
+    if (!guard_ok(guard))
+        return;  // the workspace does not hold this launch's descriptors
+    if (status_ptr && *status_ptr != LT_STATUS_OK)
         return;  // skipped step: nothing is written
     const float coef = coef_ptr ? *coef_ptr : 1.0f;
     const int lane = threadIdx.x & 63;
@@ -1327,13 +1666,14 @@ __global__ __launch_bounds__(kThreads) void k_adamw32_step(const int64_t* __rest
 // copy is bf16(weights).  The kernel exits at once when the step was not
 // skipped.  Units and their prefix are those of the step launch it follows.
 template <typename Desc>
-__global__ __launch_bounds__(kThreads) void k_bf16_on_skip(const int64_t* __restrict__ unit_prefix,
+__global__ __launch_bounds__(kThreads) void k_bf16_on_skip(WsGuard guard,
+                                                           const int64_t* __restrict__ unit_prefix,
                                                            const Desc* __restrict__ desc,
                                                            int n_tensors, int64_t n_units,
                                                            int64_t unit_elems,
                                                            const int32_t* __restrict__ status_ptr)
 {
-    if (*status_ptr != LT_STATUS_NONFINITE)
+    if (!guard_ok(guard) || *status_ptr == LT_STATUS_OK)
         return;
     const int lane = threadIdx.x & 63;
     const int64_t waves = int64_t(gridDim.x) * 4;
@@ -1354,14 +1694,14 @@ __global__ __launch_bounds__(kThreads) void k_bf16_on_skip(const int64_t* __rest
 }
 
 template <typename Desc>
-lt_err launch_bf16_on_skip(const int64_t* unit_prefix, const Desc* desc, int n_tensors,
-                           int64_t n_units, int64_t unit_elems, const int32_t* status,
-                           hipStream_t st)
+lt_err launch_bf16_on_skip(const WsGuard& guard, const int64_t* unit_prefix, const Desc* desc,
+                           int n_tensors, int64_t n_units, int64_t unit_elems,
+                           const int32_t* status, hipStream_t st)
 {
     if (n_units == 0)
         return LT_OK;
     const int grid = int(std::min<int64_t>((n_units + 3) / 4, 1024));
-    k_bf16_on_skip<Desc><<<grid, kThreads, 0, st>>>(unit_prefix, desc, n_tensors, n_units,
+    k_bf16_on_skip<Desc><<<grid, kThreads, 0, st>>>(guard, unit_prefix, desc, n_tensors, n_units,
                                                     unit_elems, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
@@ -1370,9 +1710,9 @@ lt_err launch_bf16_on_skip(const int64_t* unit_prefix, const Desc* desc, int n_t
 // ================================================================ host side
 
 template <typename GT, int B>
-lt_err launch_step_b(const int64_t* prefix, const StepTensor* desc, int K, int64_t units,
-                     const StepScalars& s, const float* coef, const int32_t* status, bool wb,
-                     int map, hipStream_t stream)
+lt_err launch_step_b(const WsGuard& guard, const int64_t* prefix, const StepTensor* desc, int K,
+                     int64_t units, const StepScalars& s, const float* coef,
+                     const int32_t* status, bool wb, int map, hipStream_t stream)
 {
     // One workgroup takes four units at a time when each wave works alone.
     const int64_t wg_units = (map == kMapDynamic ? StepGeom<B, true>::W : StepGeom<B, false>::W) > 1
@@ -1386,32 +1726,71 @@ lt_err launch_step_b(const int64_t* prefix, const StepTensor* desc, int K, int64
     int grid;
     if (lt_err e = grid_size(kernel, wg_units, &grid))
         return e;
-    kernel<<<grid, kThreads, 0, stream>>>(prefix, desc, K, units, s, coef, status);
+    kernel<<<grid, kThreads, 0, stream>>>(guard, prefix, desc, K, units, s, coef, status);
+    LT_HIP(hipGetLastError());
+    return LT_OK;
+}
+
+// Block sizes of the fast step kernels; every other valid size takes the generic one.
+bool fast_block_size(int B) { return B >= 64 && B <= 8192 && (B & (B - 1)) == 0; }
+
+// The generic step kernel: one work unit per block.
+template <typename GT, bool WB, int MAP>
+lt_err launch_generic_map(const WsGuard& guard, int B, const int64_t* prefix,
+                          const StepTensor* desc, int K, int64_t units, const StepScalars& s,
+                          const float* coef, const int32_t* status, hipStream_t stream)
+{
+    const bool stash = B <= kGenericStashMax;
+    const size_t lds = stash ? size_t(B) * 2 * sizeof(float) : 0;
+    auto* kernel = stash ? k_adamw8_generic<GT, WB, MAP, true> : k_adamw8_generic<GT, WB, MAP, false>;
+    int grid;
+    if (lt_err e = grid_size(kernel, units, &grid, lds))
+        return e;
+    kernel<<<grid, kThreads, lds, stream>>>(guard, prefix, desc, K, units, B, s, coef, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
 }
 
 template <typename GT>
-lt_err launch_step(int B, const int64_t* prefix, const StepTensor* desc, int K, int64_t tiles,
-                   const StepScalars& s, const float* coef, const int32_t* status, bool wb,
-                   int map, hipStream_t stream)
+lt_err launch_generic(const WsGuard& guard, int B, const int64_t* prefix, const StepTensor* desc,
+                      int K, int64_t units, const StepScalars& s, const float* coef,
+                      const int32_t* status, bool wb, int map, hipStream_t stream)
+{
+    if (map == kMapDynamic)
+        return wb ? launch_generic_map<GT, true, kMapDynamic>(guard, B, prefix, desc, K, units, s,
+                                                               coef, status, stream)
+                  : launch_generic_map<GT, false, kMapDynamic>(guard, B, prefix, desc, K, units,
+                                                                s, coef, status, stream);
+    return wb ? launch_generic_map<GT, true, kMapLinear>(guard, B, prefix, desc, K, units, s, coef,
+                                                          status, stream)
+              : launch_generic_map<GT, false, kMapLinear>(guard, B, prefix, desc, K, units, s,
+                                                           coef, status, stream);
+}
+
+template <typename GT>
+lt_err launch_step(const WsGuard& g, int B, const int64_t* prefix, const StepTensor* desc, int K,
+                   int64_t tiles, const StepScalars& s, const float* coef, const int32_t* status,
+                   bool wb, int map, hipStream_t stream)
 {
     switch (B) {
-    case 64: return launch_step_b<GT, 64>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
-    case 128: return launch_step_b<GT, 128>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
-    case 256: return launch_step_b<GT, 256>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
-    case 512: return launch_step_b<GT, 512>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
-    case 1024: return launch_step_b<GT, 1024>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
-    case 2048: return launch_step_b<GT, 2048>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
-    case 4096: return launch_step_b<GT, 4096>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
-    case 8192: return launch_step_b<GT, 8192>(prefix, desc, K, tiles, s, coef, status, wb, map, stream);
-    default: return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
+    case 64: return launch_step_b<GT, 64>(g, prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 128: return launch_step_b<GT, 128>(g, prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 256: return launch_step_b<GT, 256>(g, prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 512: return launch_step_b<GT, 512>(g, prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 1024: return launch_step_b<GT, 1024>(g, prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 2048: return launch_step_b<GT, 2048>(g, prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 4096: return launch_step_b<GT, 4096>(g, prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    case 8192: return launch_step_b<GT, 8192>(g, prefix, desc, K, tiles, s, coef, status, wb, map, stream);
+    default: return launch_generic<GT>(g, B, prefix, desc, K, tiles, s, coef, status, wb, map, stream);
     }
 }
 
-// Elements per work unit of the step kernel (StepGeom<B, map>::UNIT).
+// Elements per work unit of the step kernel (StepGeom<B, map>::UNIT; one block
+// for the generic kernel).
 int64_t step_unit_elems(int B, int map)
 {
+    if (!fast_block_size(B))
+        return B;
     const int64_t EM = step_elems_max(B, map == kMapDynamic);
     const int64_t E = B >= 64 * EM ? EM : (B >= 512 ? B / 64 : 8);
     return B > 64 * E ? 4 * 64 * E : 64 * E;
@@ -1449,15 +1828,19 @@ bool lists_given(int K, std::initializer_list<const void*> lists)
     return true;
 }
 
+// eps must be positive after its rounding to fp32 as well: with eps = 0 an element
+// whose gradient and stored second moment are both zero divides 0 by 0.
 bool valid_hyper(double lr, double beta1, double beta2, double eps, double weight_decay,
                  int64_t step)
 {
     return std::isfinite(lr) && lr >= 0.0 && std::isfinite(weight_decay) && weight_decay >= 0.0 &&
            beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0 && std::isfinite(eps) &&
-           eps >= 0.0 && step >= 1;
+           eps > 0.0 && float(eps) > 0.0f && std::isfinite(float(eps)) && step >= 1;
 }
 
-bool valid_block_size(int B) { return B >= 64 && B <= 8192 && (B & (B - 1)) == 0; }
+constexpr int kMaxBlockSize = 65536;
+
+bool valid_block_size(int B) { return B >= 64 && B <= kMaxBlockSize && B % 64 == 0; }
 
 // Byte ranges a call reads or writes, for the no-overlap rule: no array the call
 // writes may share a byte with any other array of the call (gradients, which are
@@ -1508,8 +1891,8 @@ StepScalars make_scalars(double lr, double beta1, double beta2, double eps, doub
     return s;
 }
 
-lt_err launch_sq_chunks(int gdt, const int64_t* prefix, const uint64_t* ptrs, const int64_t* numels,
-                        int K, int64_t C, double* partials, hipStream_t st)
+lt_err launch_sq_chunks(const WsGuard& guard, int gdt, const int64_t* prefix, const uint64_t* ptrs,
+                        const int64_t* numels, int K, int64_t C, double* partials, hipStream_t st)
 {
     if (C == 0)
         return LT_OK;  // no chunks: every tensor of the list is empty
@@ -1518,11 +1901,13 @@ lt_err launch_sq_chunks(int gdt, const int64_t* prefix, const uint64_t* ptrs, co
     if (gdt == LT_DTYPE_BF16) {
         if (lt_err e = grid_size(k_sqnorm_chunks<uint16_t>, iters, &grid))
             return e;
-        k_sqnorm_chunks<uint16_t><<<grid, kThreads, 0, st>>>(prefix, ptrs, numels, K, C, partials);
+        k_sqnorm_chunks<uint16_t><<<grid, kThreads, 0, st>>>(guard, prefix, ptrs, numels, K, C,
+                                                             partials);
     } else {
         if (lt_err e = grid_size(k_sqnorm_chunks<float>, iters, &grid))
             return e;
-        k_sqnorm_chunks<float><<<grid, kThreads, 0, st>>>(prefix, ptrs, numels, K, C, partials);
+        k_sqnorm_chunks<float><<<grid, kThreads, 0, st>>>(guard, prefix, ptrs, numels, K, C,
+                                                          partials);
     }
     LT_HIP(hipGetLastError());
     return LT_OK;
@@ -1587,7 +1972,7 @@ StreamLayout stream_layout(const int64_t* numels, int K, const int* first, int L
                            int S, bool bf16_copy, bool keep_grads)
 {
     StreamLayout l;
-    size_t at = 0;
+    size_t at = kTagBytes;
     l.gprefix = at;
     at = round_up(at + sizeof(int64_t) * (K + 1), 64);
     for (int i = 0; i < L; ++i) {
@@ -1689,7 +2074,8 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
     }
     auto* ws = static_cast<uint8_t*>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (lt_err e = upload(header.data(), header.size(), ws, st))
+    WsGuard guard;
+    if (lt_err e = put_descriptors(header, ws, st, &guard))
         return e;
     const auto* d_prefix = reinterpret_cast<const int64_t*>(ws + lay.prefix);
     const auto* d_ptrs = reinterpret_cast<const uint64_t*>(ws + lay.ptrs);
@@ -1697,29 +2083,31 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
     auto* d_partials = reinterpret_cast<double*>(ws + lay.partials);
     auto* d_sk = reinterpret_cast<double*>(ws + lay.sk);
 
-    if (lt_err e = launch_sq_chunks(grad_dtype, d_prefix, d_ptrs, d_numels, K, C, d_partials, st))
+    if (lt_err e = launch_sq_chunks(guard, grad_dtype, d_prefix, d_ptrs, d_numels, K, C,
+                                    d_partials, st))
         return e;
     if (K > 0) {
-        k_sqnorm_finish<<<K, kThreads, 0, st>>>(d_prefix, d_partials, d_sk);
+        k_sqnorm_finish<<<K, kThreads, 0, st>>>(guard, d_prefix, d_partials, d_sk);
         LT_HIP(hipGetLastError());
     }
-    k_sqnorm_total<<<1, 256, 0, st>>>(d_sk, K, sq_per_tensor, sq_total, status);
+    k_sqnorm_total<<<1, 256, 0, st>>>(guard, d_sk, K, sq_per_tensor, sq_total, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
 }
 
 lt_err lt_clip_coef(const double* sq_total, float max_norm, float* total_norm, float* coef,
-                    void* stream)
+                    int32_t* status, void* stream)
 {
     g_last_error.clear();
     if (!sq_total || !coef)
         return fail(LT_ERR_INVALID_ARG, "sq_total and coef must not be NULL");
     if (!(max_norm > 0.0f))
         return fail(LT_ERR_INVALID_ARG, "max_norm must be > 0 (+inf disables clipping)");
-    if (!aligned(sq_total, 8) || !aligned(coef, 4) || (total_norm && !aligned(total_norm, 4)))
+    if (!aligned(sq_total, 8) || !aligned(coef, 4) || (total_norm && !aligned(total_norm, 4)) ||
+        (status && !aligned(status, 4)))
         return fail(LT_ERR_ALIGNMENT, "scalar arguments must be naturally aligned");
     k_clip_coef<<<1, 64, 0, static_cast<hipStream_t>(stream)>>>(sq_total, max_norm, total_norm,
-                                                                 coef);
+                                                                 coef, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
 }
@@ -1776,19 +2164,20 @@ lt_err lt_grad_sqnorm_partials(const void* const* grads, const int64_t* numels, 
     }
     auto* ws = static_cast<uint8_t*>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (lt_err e = upload(header.data(), header.size(), ws, st))
+    WsGuard guard;
+    if (lt_err e = put_descriptors(header, ws, st, &guard))
         return e;
-    return launch_sq_chunks(grad_dtype, reinterpret_cast<const int64_t*>(ws + lay.prefix),
+    return launch_sq_chunks(guard, grad_dtype, reinterpret_cast<const int64_t*>(ws + lay.prefix),
                             reinterpret_cast<const uint64_t*>(ws + lay.ptrs),
                             reinterpret_cast<const int64_t*>(ws + lay.numels), K, prefix[K],
                             partials, st);
 }
 
-// Finish workspace: [chunk prefix K+1] | [S_k K]
+// Finish workspace: [tag][chunk prefix K+1] | [S_k K]
 size_t lt_grad_sqnorm_finish_workspace_bytes(int n_tensors)
 {
     return n_tensors < 0 ? 0
-                         : round_up(sizeof(int64_t) * (n_tensors + 1), 256) +
+                         : round_up(kTagBytes + sizeof(int64_t) * (n_tensors + 1), 256) +
                                round_up(sizeof(double) * n_tensors, 256);
 }
 
@@ -1810,20 +2199,22 @@ lt_err lt_grad_sqnorm_finish(const int64_t* numels, int n_tensors, const double*
     if (!workspace || !aligned(workspace, 256) || workspace_bytes < need)
         return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
                                           std::to_string(need) + " bytes");
-    std::vector<int64_t> prefix(K + 1, 0);
+    std::vector<uint8_t> image(kTagBytes + sizeof(int64_t) * (K + 1), 0);
+    auto* prefix = reinterpret_cast<int64_t*>(image.data() + kTagBytes);
     for (int k = 0; k < K; ++k)
         prefix[k + 1] = prefix[k] + (numels[k] + kChunk - 1) / kChunk;
     auto* ws = static_cast<uint8_t*>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (lt_err e = upload(prefix.data(), sizeof(int64_t) * (K + 1), ws, st))
+    WsGuard guard;
+    if (lt_err e = put_descriptors(image, ws, st, &guard))
         return e;
-    auto* d_sk = reinterpret_cast<double*>(ws + round_up(sizeof(int64_t) * (K + 1), 256));
+    auto* d_sk = reinterpret_cast<double*>(ws + round_up(kTagBytes + sizeof(int64_t) * (K + 1), 256));
     if (K > 0) {
-        k_sqnorm_finish<<<K, kThreads, 0, st>>>(reinterpret_cast<const int64_t*>(ws), partials,
-                                                d_sk);
+        k_sqnorm_finish<<<K, kThreads, 0, st>>>(guard, reinterpret_cast<const int64_t*>(ws + kTagBytes),
+                                                partials, d_sk);
         LT_HIP(hipGetLastError());
     }
-    k_sqnorm_total<<<1, 256, 0, st>>>(d_sk, K, sq_per_tensor, sq_total, status);
+    k_sqnorm_total<<<1, 256, 0, st>>>(guard, d_sk, K, sq_per_tensor, sq_total, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
 }
@@ -1849,12 +2240,12 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
     if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
     if (!valid_block_size(block_size))
-        return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
+        return fail(LT_ERR_INVALID_ARG, "block_size must be a multiple of 64 in [64, 65536]");
     if (code_map != LT_MAP_LINEAR && code_map != LT_MAP_DYNAMIC)
         return fail(LT_ERR_INVALID_ARG, "code_map must be LT_MAP_LINEAR or LT_MAP_DYNAMIC");
     if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step))
-        return fail(LT_ERR_INVALID_ARG,
-                    "need finite lr, weight_decay, eps >= 0, 0 <= beta1, beta2 < 1 and step >= 1");
+        return fail(LT_ERR_INVALID_ARG, "need finite lr, weight_decay >= 0, finite eps > 0 (also "
+                                        "in fp32), 0 <= beta1, beta2 < 1 and step >= 1");
     if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)))
         return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned");
     const int K = n_tensors;
@@ -1914,19 +2305,20 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
 
     auto* ws = static_cast<uint8_t*>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (lt_err e = upload(host.data(), host.size(), ws, st))
+    WsGuard guard;
+    if (lt_err e = put_descriptors(host, ws, st, &guard))
         return e;
     const auto* d_prefix = reinterpret_cast<const int64_t*>(ws + lay.prefix);
     const auto* d_desc = reinterpret_cast<const StepTensor*>(ws + lay.desc);
     const bool wb = any_set(params_bf16, K);
     if (lt_err e = grad_dtype == LT_DTYPE_BF16
-                       ? launch_step<uint16_t>(block_size, d_prefix, d_desc, K, tiles, s, coef,
-                                               status, wb, code_map, st)
-                       : launch_step<float>(block_size, d_prefix, d_desc, K, tiles, s, coef,
-                                            status, wb, code_map, st))
+                       ? launch_step<uint16_t>(guard, block_size, d_prefix, d_desc, K, tiles, s,
+                                               coef, status, wb, code_map, st)
+                       : launch_step<float>(guard, block_size, d_prefix, d_desc, K, tiles, s,
+                                            coef, status, wb, code_map, st))
         return e;
     if (status && wb)
-        return launch_bf16_on_skip(d_prefix, d_desc, K, tiles, tile, status, st);
+        return launch_bf16_on_skip(guard, d_prefix, d_desc, K, tiles, tile, status, st);
     return LT_OK;
 }
 
@@ -1970,12 +2362,13 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
     if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
     if (!valid_block_size(B))
-        return fail(LT_ERR_INVALID_ARG, "block_size must be a power of two in [64, 8192]");
+        return fail(LT_ERR_INVALID_ARG, "block_size must be a multiple of 64 in [64, 65536]");
     if (code_map != LT_MAP_LINEAR && code_map != LT_MAP_DYNAMIC)
         return fail(LT_ERR_INVALID_ARG, "code_map must be LT_MAP_LINEAR or LT_MAP_DYNAMIC");
     if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step) || !(max_norm > 0.0f))
-        return fail(LT_ERR_INVALID_ARG, "need finite lr, weight_decay, eps >= 0, 0 <= beta1, "
-                                        "beta2 < 1, step >= 1 and max_norm > 0");
+        return fail(LT_ERR_INVALID_ARG, "need finite lr, weight_decay >= 0, finite eps > 0 (also "
+                                        "in fp32), 0 <= beta1, beta2 < 1, step >= 1 and "
+                                        "max_norm > 0");
     if (S < 2 || S > kMaxSlots)
         return fail(LT_ERR_INVALID_ARG, "ring_slots must be in [2, 16]");
     if (!sq_total || !coef || !status)
@@ -2058,7 +2451,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
     hipStream_t cs = static_cast<hipStream_t>(compute_stream);
     hipStream_t hs = static_cast<hipStream_t>(h2d_stream);
     hipStream_t ds = static_cast<hipStream_t>(d2h_stream);
-    if (lt_err e = upload(header.data(), header.size(), ws, cs))
+    WsGuard guard;
+    if (lt_err e = put_descriptors(header, ws, cs, &guard))
         return e;
     // Copies into a slot may start once the work that last used it is done.
     bool used[kMaxSlots] = {};
@@ -2086,7 +2480,7 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         const int Ki = layer_first[i + 1] - layer_first[i];
         const int64_t Ci = reinterpret_cast<int64_t*>(header.data() + lay.sq_prefix[i])[Ki];
         if (lt_err e = launch_sq_chunks(
-                grad_dtype, reinterpret_cast<const int64_t*>(ws + lay.sq_prefix[i]),
+                guard, grad_dtype, reinterpret_cast<const int64_t*>(ws + lay.sq_prefix[i]),
                 reinterpret_cast<const uint64_t*>(ws + lay.sq_ptrs[i]),
                 reinterpret_cast<const int64_t*>(ws + lay.sq_numels[i]), Ki, Ci,
                 d_partials + gprefix[layer_first[i]], cs))
@@ -2096,12 +2490,12 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
     }
     if (!norm_ready) {
         const auto* d_gprefix = reinterpret_cast<const int64_t*>(ws + lay.gprefix);
-        k_sqnorm_finish<<<K, kThreads, 0, cs>>>(d_gprefix, d_partials, d_sk);
+        k_sqnorm_finish<<<K, kThreads, 0, cs>>>(guard, d_gprefix, d_partials, d_sk);
         LT_HIP(hipGetLastError());
-        k_sqnorm_total<<<1, 256, 0, cs>>>(d_sk, K, nullptr, sq_total, status);
+        k_sqnorm_total<<<1, 256, 0, cs>>>(guard, d_sk, K, nullptr, sq_total, status);
         LT_HIP(hipGetLastError());
     }
-    k_clip_coef<<<1, 64, 0, cs>>>(sq_total, max_norm, total_norm, coef);
+    k_clip_coef<<<1, 64, 0, cs>>>(sq_total, max_norm, total_norm, coef, nullptr);
     LT_HIP(hipGetLastError());
 
     // Pass 2: layer in, fused step, layer out.
@@ -2133,14 +2527,14 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         const bool wb = any_set(params_bf16 ? params_bf16 + layer_first[i] : nullptr, Ki);
         lt_err e = units == 0 ? LT_OK
                    : grad_dtype == LT_DTYPE_BF16
-                       ? launch_step<uint16_t>(B, up, dp, Ki, units, sc, coef, status, wb,
+                       ? launch_step<uint16_t>(guard, B, up, dp, Ki, units, sc, coef, status, wb,
                                                code_map, cs)
-                       : launch_step<float>(B, up, dp, Ki, units, sc, coef, status, wb, code_map,
-                                            cs);
+                       : launch_step<float>(guard, B, up, dp, Ki, units, sc, coef, status, wb,
+                                            code_map, cs);
         if (e)
             return e;
         if (wb)
-            if (lt_err e2 = launch_bf16_on_skip(up, dp, Ki, units, unit, status, cs))
+            if (lt_err e2 = launch_bf16_on_skip(guard, up, dp, Ki, units, unit, status, cs))
                 return e2;
         LT_HIP(hipEventRecord(ev.computed[sl], cs));
         LT_HIP(hipStreamWaitEvent(ds, ev.computed[sl], 0));
@@ -2166,9 +2560,10 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
     return LT_OK;
 }
 
+// fp32-state workspace: [tag][unit prefix K+1][Fp32Tensor K]
 size_t lt_adamw_fp32_workspace_bytes(int n_tensors)
 {
-    return n_tensors < 0 ? 0 : round_up(round_up(sizeof(int64_t) * (n_tensors + 1), 64) +
+    return n_tensors < 0 ? 0 : round_up(kTagBytes + round_up(sizeof(int64_t) * (n_tensors + 1), 64) +
                                             sizeof(Fp32Tensor) * size_t(n_tensors), 256);
 }
 
@@ -2186,8 +2581,8 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
     if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
     if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step))
-        return fail(LT_ERR_INVALID_ARG,
-                    "need finite lr, weight_decay, eps >= 0, 0 <= beta1, beta2 < 1 and step >= 1");
+        return fail(LT_ERR_INVALID_ARG, "need finite lr, weight_decay >= 0, finite eps > 0 (also "
+                                        "in fp32), 0 <= beta1, beta2 < 1 and step >= 1");
     if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)))
         return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned");
     for (int k = 0; k < K; ++k) {
@@ -2219,14 +2614,14 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
         if (!e.empty())
             return fail(LT_ERR_INVALID_ARG, e);
     }
-    const size_t desc_at = round_up(sizeof(int64_t) * (K + 1), 64);
+    const size_t desc_at = kTagBytes + round_up(sizeof(int64_t) * (K + 1), 64);
     const size_t total = lt_adamw_fp32_workspace_bytes(K);
     if (!workspace || !aligned(workspace, 256) || workspace_bytes < total)
         return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned and hold " +
                                           std::to_string(total) + " bytes");
     constexpr int64_t span = 64 * kFp32ElemsPerLane;
     std::vector<uint8_t> host(total, 0);
-    auto* prefix = reinterpret_cast<int64_t*>(host.data());
+    auto* prefix = reinterpret_cast<int64_t*>(host.data() + kTagBytes);
     auto* desc = reinterpret_cast<Fp32Tensor*>(host.data() + desc_at);
     prefix[0] = 0;
     for (int k = 0; k < K; ++k) {
@@ -2242,9 +2637,10 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
     const StepScalars sc = make_scalars(lr, beta1, beta2, eps, weight_decay, step);
     auto* ws = static_cast<uint8_t*>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (lt_err e = upload(host.data(), host.size(), ws, st))
+    WsGuard guard;
+    if (lt_err e = put_descriptors(host, ws, st, &guard))
         return e;
-    const auto* d_prefix = reinterpret_cast<const int64_t*>(ws);
+    const auto* d_prefix = reinterpret_cast<const int64_t*>(ws + kTagBytes);
     const auto* d_desc = reinterpret_cast<const Fp32Tensor*>(ws + desc_at);
     const bool wb = any_set(params_bf16, K);
     auto* kernel = grad_dtype == LT_DTYPE_BF16
@@ -2253,10 +2649,10 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
     int grid;
     if (lt_err e = grid_size(kernel, (units + 3) / 4, &grid))
         return e;
-    kernel<<<grid, kThreads, 0, st>>>(d_prefix, d_desc, K, units, sc, coef, status);
+    kernel<<<grid, kThreads, 0, st>>>(guard, d_prefix, d_desc, K, units, sc, coef, status);
     LT_HIP(hipGetLastError());
     if (status && wb)
-        return launch_bf16_on_skip(d_prefix, d_desc, K, units, span, status, st);
+        return launch_bf16_on_skip(guard, d_prefix, d_desc, K, units, span, status, st);
     return LT_OK;
 }
 
@@ -2297,6 +2693,24 @@ lt_err lt_read_status(const int32_t* status, void* stream, int32_t* out)
     hipStream_t st = static_cast<hipStream_t>(stream);
     LT_HIP(hipMemcpyAsync(out, status, sizeof(int32_t), hipMemcpyDeviceToHost, st));
     LT_HIP(hipStreamSynchronize(st));
+    return LT_OK;
+}
+
+lt_err lt_workspace_release(const void* workspace)
+{
+    g_last_error.clear();
+    if (!workspace)
+        return LT_OK;
+    for (int d = 0; d < kMaxDevices; ++d) {
+        DeviceState& ds = g_dev[d];
+        std::lock_guard<std::mutex> lock(ds.mu);
+        auto it = ds.cache.find(workspace);
+        if (it == ds.cache.end())
+            continue;
+        if (it->second.copied)
+            ds.spare_events.push_back(it->second.copied);
+        ds.cache.erase(it);
+    }
     return LT_OK;
 }
 

@@ -12,6 +12,7 @@ from __future__ import annotations
 import ctypes
 import math
 import os
+import weakref
 from typing import Optional, Sequence
 
 import torch
@@ -19,12 +20,12 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liblazytrain.so")
 
-LT_OK, LT_ERR_INVALID_ARG, LT_ERR_ALIGNMENT, LT_ERR_WORKSPACE, LT_ERR_HIP = range(5)
-LT_STATUS_OK, LT_STATUS_NONFINITE = 0, 1
+LT_OK, LT_ERR_INVALID_ARG, LT_ERR_ALIGNMENT, LT_ERR_HIP, LT_ERR_WORKSPACE = range(5)
+LT_STATUS_OK, LT_STATUS_NONFINITE, LT_STATUS_BAD_WORKSPACE = 0, 1, 2
 LT_DTYPE_F32, LT_DTYPE_BF16 = 0, 1
 LT_MAP_LINEAR, LT_MAP_DYNAMIC = 0, 1
-ERROR_NAMES = {1: "LT_ERR_INVALID_ARG", 2: "LT_ERR_ALIGNMENT", 3: "LT_ERR_WORKSPACE",
-               4: "LT_ERR_HIP"}
+ERROR_NAMES = {1: "LT_ERR_INVALID_ARG", 2: "LT_ERR_ALIGNMENT", 3: "LT_ERR_HIP",
+               4: "LT_ERR_WORKSPACE"}
 
 _lib = None
 
@@ -60,7 +61,7 @@ def lib() -> ctypes.CDLL:
     L.lt_grad_sqnorm_workspace_bytes.restype = ctypes.c_size_t
     L.lt_grad_sqnorm.argtypes = [vpp, i64p, ctypes.c_int, ctypes.c_int, vp, ctypes.c_size_t,
                                  vp, vp, vp, vp]
-    L.lt_clip_coef.argtypes = [vp, ctypes.c_float, vp, vp, vp]
+    L.lt_clip_coef.argtypes = [vp, ctypes.c_float, vp, vp, vp, vp]
     L.lt_grad_chunk_count.argtypes = [i64p, ctypes.c_int]
     L.lt_grad_chunk_count.restype = ctypes.c_int64
     L.lt_grad_sqnorm_partials_workspace_bytes.argtypes = [ctypes.c_int]
@@ -96,12 +97,13 @@ def lib() -> ctypes.CDLL:
                                        ctypes.POINTER(ctypes.c_int64)]
     L.lt_read_status.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32)]
     L.lt_set_max_workgroups.argtypes = [ctypes.c_int]
+    L.lt_workspace_release.argtypes = [vp]
     L.lt_last_error.argtypes = []
     L.lt_last_error.restype = ctypes.c_char_p
     for name in ("lt_grad_sqnorm", "lt_clip_coef", "lt_hybrid8bit_adamw_step", "lt_read_status",
                  "lt_grad_sqnorm_partials", "lt_grad_sqnorm_finish",
                  "lt_set_max_workgroups", "lt_streamed_hybrid8bit_adamw_step",
-                 "lt_adamw_fp32_step", "lt_select_8bit_slice"):
+                 "lt_adamw_fp32_step", "lt_select_8bit_slice", "lt_workspace_release"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -185,19 +187,47 @@ def _scalar(t: Optional[torch.Tensor], device, dtype, what) -> int:
 
 
 _workspaces = {}
+_finalizers = {}
 
 
-def _workspace(device, nbytes: int, workspace: Optional[torch.Tensor], stream) -> torch.Tensor:
-    """The caller's workspace, or one cached per (device, stream).  A cached workspace
-    is allocated on the stream that uses it, so that when a larger one replaces it
-    the caching allocator hands its memory out again only in that stream's order."""
+def _forget(ptr: int, key: int) -> None:
+    _finalizers.pop(key, None)
+    try:
+        lib().lt_workspace_release(ptr)
+    except Exception:  # interpreter shutdown: nothing left to forget for
+        pass
+
+
+def _track(ws: torch.Tensor) -> None:
+    """When the workspace tensor is freed, the library forgets what it wrote there
+    (lt_workspace_release), so that a later workspace at the same address gets its
+    descriptors copied in again.  Pass the same tensor to every call (a fresh view
+    per call is released after each call and so copies the descriptors each time)."""
+    key = id(ws)
+    f = _finalizers.get(key)
+    if f is not None and f.alive:
+        return
+    _finalizers[key] = weakref.finalize(ws, _forget, ws.data_ptr(), key)
+
+
+def _workspace(device, nbytes: int, workspace: Optional[torch.Tensor], stream,
+               kind: str) -> torch.Tensor:
+    """The caller's workspace, or one cached per (device, stream, kind of call), so
+    that a call repeated over the same tensors finds its descriptors in place (the
+    library then copies nothing; see include/lazytrain.h).  A cached workspace is
+    allocated on the stream that uses it, so that when a larger one replaces it the
+    caching allocator hands its memory out again only in that stream's order; the
+    library is told to forget the old one first."""
     if workspace is not None:
         if workspace.device != device or workspace.numel() * workspace.element_size() < nbytes:
             raise ValueError(f"workspace must hold {nbytes} bytes on {device}")
+        _track(workspace)
         return workspace
-    key = (device, _stream_handle(stream, device))
+    key = (device, _stream_handle(stream, device), kind)
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
+        if ws is not None:
+            lt_workspace_release(ws)
         if stream is None:
             s = torch.cuda.current_stream(device)
         elif hasattr(stream, "cuda_stream"):
@@ -207,6 +237,7 @@ def _workspace(device, nbytes: int, workspace: Optional[torch.Tensor], stream) -
         with torch.cuda.stream(s):
             ws = torch.empty(max(nbytes, 4096), dtype=torch.uint8, device=device)
         _workspaces[key] = ws
+        _track(ws)
     return ws
 
 
@@ -232,7 +263,7 @@ def lt_grad_sqnorm(grads: Sequence[torch.Tensor], sq_total: torch.Tensor, status
     if sq_per_tensor is not None and sq_per_tensor.numel() < len(grads):
         raise ValueError("sq_per_tensor needs one float64 per tensor")
     nbytes = lt_grad_sqnorm_workspace_bytes([g.numel() for g in grads])
-    ws = _workspace(device, nbytes, workspace, stream)
+    ws = _workspace(device, nbytes, workspace, stream, "sqnorm")
     with torch.cuda.device(device):  # the library works on the current device
         _check(lib().lt_grad_sqnorm(
             _ptr_array(grads), _numel_array(grads), len(grads), gdt, ws.data_ptr(),
@@ -242,14 +273,18 @@ def lt_grad_sqnorm(grads: Sequence[torch.Tensor], sq_total: torch.Tensor, status
 
 
 def lt_clip_coef(sq_total: torch.Tensor, max_norm: float, coef: torch.Tensor,
-                 total_norm: Optional[torch.Tensor] = None, stream=None) -> None:
-    """Step a3: norm and clip coefficient into device float32 tensors."""
+                 total_norm: Optional[torch.Tensor] = None,
+                 status: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Step a3: norm and clip coefficient into device float32 tensors; status (an
+    int32 device tensor, optional) is set from the sum of squares unless it holds a
+    library error."""
     device = sq_total.device
     with torch.cuda.device(device):  # the library works on the current device
         _check(lib().lt_clip_coef(_scalar(sq_total, device, torch.float64, "sq_total"),
                                   float(max_norm),
                                   _scalar(total_norm, device, torch.float32, "total_norm"),
                                   _scalar(coef, device, torch.float32, "coef"),
+                                  _scalar(status, device, torch.int32, "status"),
                                   _stream_handle(stream, device)))
 
 
@@ -271,7 +306,7 @@ def lt_grad_sqnorm_partials(grads: Sequence[torch.Tensor], partials: torch.Tenso
             not partials.is_contiguous() or partials.numel() < need:
         raise ValueError(f"partials must be a contiguous float64 device view of >= {need} entries")
     ws = _workspace(device, int(lib().lt_grad_sqnorm_partials_workspace_bytes(len(grads))),
-                    workspace, stream)
+                    workspace, stream, "partials")
     with torch.cuda.device(device):  # the library works on the current device
         _check(lib().lt_grad_sqnorm_partials(
             _ptr_array(grads), _numel_array(grads), len(grads), gdt, partials.data_ptr(),
@@ -289,7 +324,7 @@ def lt_grad_sqnorm_finish(numels: Sequence[int], partials: torch.Tensor, sq_tota
     if sq_per_tensor is not None and sq_per_tensor.numel() < len(numels):
         raise ValueError("sq_per_tensor needs one float64 per tensor")
     ws = _workspace(device, int(lib().lt_grad_sqnorm_finish_workspace_bytes(len(numels))),
-                    workspace, stream)
+                    workspace, stream, "finish")
     arr = (ctypes.c_int64 * len(numels))(*numels)
     with torch.cuda.device(device):  # the library works on the current device
         _check(lib().lt_grad_sqnorm_finish(
@@ -347,6 +382,9 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
     _check_tensors(m_absmax, device, torch.float32, "m_absmax")
     _check_tensors(v_absmax, device, torch.float32, "v_absmax")
     gdt = _grad_dtype(grads)
+    if int(block_size) < 1:
+        raise LazyTrainError(LT_ERR_INVALID_ARG, "block_size must be a multiple of 64 in "
+                             "[64, 65536]")
     for i in range(k):
         n = params[i].numel()
         nb = -(-n // block_size)
@@ -355,7 +393,7 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
         if m_absmax[i].numel() < nb or v_absmax[i].numel() < nb:
             raise ValueError(f"tensor {i}: absmax arrays need ceil({n}/{block_size}) = {nb} entries")
     wb = _bf16_list(params_bf16, params, device)
-    ws = _workspace(device, lt_step_workspace_bytes(k), workspace, stream)
+    ws = _workspace(device, lt_step_workspace_bytes(k), workspace, stream, "step8")
     with torch.cuda.device(device):  # the library works on the current device
         _check(lib().lt_hybrid8bit_adamw_step(
             _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(m_codes), _ptr_array(m_absmax),
@@ -408,6 +446,9 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
     _check_tensors(m_absmax, cpu, torch.float32, "m_absmax")
     _check_tensors(v_absmax, cpu, torch.float32, "v_absmax")
     gdt = _grad_dtype(grads)
+    if int(block_size) < 1:
+        raise LazyTrainError(LT_ERR_INVALID_ARG, "block_size must be a multiple of 64 in "
+                             "[64, 65536]")
     for i in range(k):
         n = params[i].numel()
         nb = -(-n // block_size)
@@ -423,7 +464,7 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
     if nbytes == 0:
         raise ValueError("invalid layer_first, block_size or ring_slots")
     cs = _stream_handle(compute_stream, device)
-    workspace = _workspace(device, nbytes, workspace, compute_stream)
+    workspace = _workspace(device, nbytes, workspace, compute_stream, "streamed")
     if compute_stream is not None and hasattr(compute_stream, "cuda_stream"):
         workspace.record_stream(compute_stream)  # in use on that stream until the step is done
     first = (ctypes.c_int * len(layer_first))(*layer_first)
@@ -472,7 +513,7 @@ def lt_adamw_fp32_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Ten
         if grads[i].numel() != n or exp_avg[i].numel() != n or exp_avg_sq[i].numel() != n:
             raise ValueError(f"tensor {i}: params, grads and states must have {n} elements")
     wb = _bf16_list(params_bf16, params, device)
-    ws = _workspace(device, lt_adamw_fp32_workspace_bytes(k), workspace, stream)
+    ws = _workspace(device, lt_adamw_fp32_workspace_bytes(k), workspace, stream, "step32")
     with torch.cuda.device(device):  # the library works on the current device
         _check(lib().lt_adamw_fp32_step(
             _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(exp_avg), _ptr_array(exp_avg_sq),
@@ -505,6 +546,13 @@ def lt_set_max_workgroups(max_workgroups: int) -> None:
     _check(lib().lt_set_max_workgroups(int(max_workgroups)))
 
 
+def lt_workspace_release(workspace) -> None:
+    """Makes the library forget what it wrote into a workspace (a tensor or a device
+    address); call it before freeing or reusing a workspace passed to earlier calls."""
+    ptr = workspace.data_ptr() if hasattr(workspace, "data_ptr") else int(workspace)
+    _check(lib().lt_workspace_release(ptr))
+
+
 # ------------------------------------------------------------- optimizer object
 
 class Hybrid8bitAdamW:
@@ -519,13 +567,18 @@ class Hybrid8bitAdamW:
     NonFiniteAbort once ``max_consecutive_skips`` of them follow one another (App. C:
     three; None never aborts).  With ``bf16_copy`` the steps also keep
     ``params_bf16``, a bf16 copy of every parameter for the next forward pass,
-    written by the step kernels (valid after the first step)."""
+    written by the step kernels (valid after the first step).  The moments take the
+    non-linear decade-tree codes by default (``code_map``): with the linear codes a
+    second moment far below its block's largest rounds to code 0 while the first
+    moment does not, and the update then divides by little more than eps (the
+    drift tests measure hundreds of lr against fp64 AdamW); pass LT_MAP_LINEAR for
+    the linear codes."""
 
     def __init__(self, params: Sequence[torch.Tensor], lr: float = 1e-5,
                  betas=(0.9, 0.999), eps: float = 1e-8, weight_decay: float = 0.01,
                  max_norm: float = 1.0, block_size: int = 4096,
                  slice_fraction: Optional[float] = None, bf16_copy: bool = False,
-                 code_map: int = LT_MAP_LINEAR, max_consecutive_skips: Optional[int] = 3):
+                 code_map: int = LT_MAP_DYNAMIC, max_consecutive_skips: Optional[int] = 3):
         self.params = list(params)
         if not self.params:
             raise ValueError("no parameters")
@@ -626,6 +679,9 @@ class Hybrid8bitAdamW:
             st = int(self._status_host[0])
         else:
             st = lt_read_status(self.status, stream)
+        if st == LT_STATUS_BAD_WORKSPACE:
+            raise LazyTrainError(LT_ERR_WORKSPACE, "a workspace lost its descriptors (it was "
+                                 "written or freed without lt_workspace_release)")
         if self._unchecked:
             if st == LT_STATUS_NONFINITE:
                 self.step_count -= 1
@@ -704,7 +760,7 @@ class StreamedHybrid8bitAdamW:
     def __init__(self, params: Sequence[torch.Tensor], layer_first: Sequence[int], device,
                  lr: float = 1e-5, betas=(0.9, 0.999), eps: float = 1e-8,
                  weight_decay: float = 0.01, max_norm: float = 1.0, block_size: int = 4096,
-                 ring_slots: int = 3, keep_grads: bool = True, code_map: int = LT_MAP_LINEAR,
+                 ring_slots: int = 3, keep_grads: bool = True, code_map: int = LT_MAP_DYNAMIC,
                  max_consecutive_skips: Optional[int] = 3, grad_dtype=torch.bfloat16):
         self.params = list(params)
         if not self.params:
@@ -767,6 +823,8 @@ class StreamedHybrid8bitAdamW:
             compute_stream=cs, h2d_stream=hs, d2h_stream=ds, code_map=self.code_map,
             keep_grads=self.keep_grads)
         st = lt_read_status(self.status, cs)  # waits for the call's work, copies out included
+        if st == LT_STATUS_BAD_WORKSPACE:
+            raise LazyTrainError(LT_ERR_WORKSPACE, "the workspace lost its descriptors")
         if st == LT_STATUS_NONFINITE:
             self.consecutive_skips += 1
         else:

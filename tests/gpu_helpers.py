@@ -52,6 +52,28 @@ class State:
 
 HYPER = dict(lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01)
 
+# The smallest positive fp32.  Hand-worked golden blocks use eps = 0 to keep their
+# arithmetic exact; the library requires eps > 0, and on those blocks the oracle gives
+# the same bits with this eps (golden_eps checks it per example).
+EPS_MIN = 2.0 ** -149
+
+
+def golden_eps(ex, code_map=None):
+    """The eps to run a golden example with on the GPU: its own, or EPS_MIN in place
+    of 0 after checking that the oracle then still gives the example's expected bits."""
+    if ex["eps"] != 0:
+        return ex["eps"]
+    names = ("w", "m_codes", "m_absmax", "v_codes", "v_absmax")
+    w, mq, ma, vq, va = ([ex[k].copy()] for k in names)
+    kw = {} if code_map is None else {"code_map": code_map}
+    oracle.hybrid8bit_adamw_step(w, [ex["grad"].copy()], mq, ma, vq, va, ex["block_size"],
+                                 step=ex["t"], coef=ex["coef"], lr=ex["lr"], beta1=ex["beta1"],
+                                 beta2=ex["beta2"], eps=EPS_MIN,
+                                 weight_decay=ex["weight_decay"], **kw)
+    for k, got in zip(names, (w, mq, ma, vq, va)):
+        assert got[0].tobytes() == ex["expect_" + k].tobytes(), (ex["name"], k)
+    return EPS_MIN
+
 
 def oracle_step(st: State, grads, block, step, coef=None, status=None, n_threads=8, **hyper):
     h = dict(HYPER, **hyper)

@@ -36,11 +36,22 @@ int main() {
     if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, 2048, 7,
                                  1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_grad_sqnorm(g, n1, 1, 9, nullptr, 0, nullptr, nullptr, nullptr, nullptr) != LT_ERR_INVALID_ARG) ++bad;
-    if (lt_clip_coef(nullptr, 1.0f, nullptr, nullptr, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    if (lt_clip_coef(nullptr, 1.0f, nullptr, nullptr, nullptr, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    // eps must be > 0, also in fp32 (checked before any pointer or device call)
+    for (double bad_eps : {0.0, -1e-8, 1e-50, (double)INFINITY})
+        if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, 2048,
+                                     LT_MAP_LINEAR, 1e-4, 0.9, 0.999, bad_eps, 0.01, 1, nullptr,
+                                     nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+    // block sizes: multiples of 64 in [64, 65536]
+    for (int bad_block : {0, 32, 96 + 8, 65536 + 64})
+        if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, bad_block,
+                                     LT_MAP_LINEAR, 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr,
+                                     nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_adamw_fp32_step(p, g, LT_DTYPE_F32, p, p, nullptr, n1, 1, NAN, 0.9, 0.999, 1e-8, 0.01, 1,
                            nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     // empty lists and zero-element tensors: validated, then nothing to launch
     alignas(256) static uint8_t host_ws[4096];
+    if (lt_workspace_release(nullptr) != LT_OK || lt_workspace_release(host_ws) != LT_OK) ++bad;
     if (lt_select_8bit_slice(nullptr, 0, 0.5, nullptr, &chosen) != LT_OK || chosen != 0) ++bad;
     if (lt_hybrid8bit_adamw_step(nullptr, nullptr, LT_DTYPE_BF16, nullptr, nullptr, nullptr, nullptr,
                                  nullptr, nullptr, 0, 2048, LT_MAP_LINEAR, 1e-4, 0.9, 0.999, 1e-8,

@@ -103,3 +103,46 @@ def test_streamed_optimizer_rejects_bad_arguments_before_any_device_work():
         lt.StreamedHybrid8bitAdamW(w, [0, 2], "cuda:0", grad_dtype=torch.float16)
     with pytest.raises(TypeError):
         lt.StreamedHybrid8bitAdamW([torch.zeros(8, dtype=torch.float64)], [0, 1], "cuda:0")
+
+
+def test_enum_values_match_the_binding():
+    """The binding's constants are the header's values; the error codes are the
+    boundary's (LT_ERR_HIP = 3, LT_ERR_WORKSPACE = 4)."""
+    import paper_2608_11919_amd as lt
+    text = open(os.path.join(ROOT, "include", "lazytrain.h")).read()
+    names = ["LT_OK", "LT_ERR_INVALID_ARG", "LT_ERR_ALIGNMENT", "LT_ERR_HIP", "LT_ERR_WORKSPACE",
+             "LT_STATUS_OK", "LT_STATUS_NONFINITE", "LT_STATUS_BAD_WORKSPACE", "LT_DTYPE_F32",
+             "LT_DTYPE_BF16", "LT_MAP_LINEAR", "LT_MAP_DYNAMIC"]
+    for name in names:
+        m = re.search(rf"\b{name}\s*=\s*(\d+)", text)
+        assert m, name
+        assert int(m.group(1)) == getattr(lt, name), name
+    assert (lt.LT_ERR_HIP, lt.LT_ERR_WORKSPACE) == (3, 4)
+
+
+def test_hyperparameter_and_block_size_rejection_without_a_device():
+    """Argument checks run before any pointer or device use, so they can be called
+    here: eps must be positive also after rounding to fp32, block sizes are the
+    multiples of 64 in [64, 65536]."""
+    import paper_2608_11919_amd as lt
+    L = lt.lib()
+    # distinct fake device addresses (never dereferenced on these paths)
+    one = lambda i: (ctypes.c_void_p * 1)(0x100000 * (i + 1))
+    n1 = (ctypes.c_int64 * 1)(4096)
+
+    def step(block, eps):
+        return L.lt_hybrid8bit_adamw_step(one(0), one(1), lt.LT_DTYPE_BF16, one(2), one(3), one(4),
+                                          one(5), None, n1, 1, block, lt.LT_MAP_LINEAR, 1e-4, 0.9,
+                                          0.999, eps, 0.01, 1, None, None, None, 0, None)
+
+    for eps in (0.0, -1e-8, 1e-50, float("inf"), float("nan")):
+        assert step(2048, eps) == lt.LT_ERR_INVALID_ARG
+        assert b"eps" in L.lt_last_error()
+    for block in (0, 32, 1000, 65536 + 64, 1 << 20):
+        assert step(block, 1e-8) == lt.LT_ERR_INVALID_ARG
+        assert b"block_size" in L.lt_last_error()
+    # valid values get past these checks (to the workspace check here: none is given)
+    for block in (64, 192, 2048, 3072, 16384, 65536):
+        assert step(block, 1e-8) == lt.LT_ERR_WORKSPACE
+    assert L.lt_workspace_release(None) == lt.LT_OK
+    assert L.lt_workspace_release(0x12345600) == lt.LT_OK  # unknown: a no-op

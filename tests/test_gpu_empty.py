@@ -135,7 +135,7 @@ def test_optimizer_object_with_an_empty_parameter():
     sizes = [5000, 0, 4096 * 2 + 3]
     w0 = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
     params = [to_dev(x) for x in w0]
-    opt = lt.Hybrid8bitAdamW(params, lr=1e-5, block_size=4096)
+    opt = lt.Hybrid8bitAdamW(params, lr=1e-5, block_size=4096, code_map=lt.LT_MAP_LINEAR)
     ref = State.zero_host(w0, 4096)
     for t in (1, 2):
         g = _grads(rng, sizes)

@@ -53,7 +53,8 @@ def test_hybrid_optimizer_matches_oracle():
     sizes = [40000, 300001, 5000, 123457, 2048, 7]
     w0 = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
     params = [to_dev(x) for x in w0]
-    opt = lt.Hybrid8bitAdamW(params, lr=1e-4, block_size=2048, slice_fraction=0.3)
+    opt = lt.Hybrid8bitAdamW(params, lr=1e-4, block_size=2048, slice_fraction=0.3,
+                             code_map=lt.LT_MAP_LINEAR)
     assert opt.idx8 and opt.idx32
     ref8 = State.zero_host([w0[i] for i in opt.idx8], 2048)
     ref32 = [(w0[i].copy(), np.zeros_like(w0[i]), np.zeros_like(w0[i])) for i in opt.idx32]

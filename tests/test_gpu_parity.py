@@ -14,7 +14,7 @@ import paper_2608_11919_amd as lt
 import synth
 from golden_io import adamw_examples, dense, f32_to_bf16_bits, sqnorm_cases
 from gpu_helpers import (DEV, HYPER, State, assert_state_equal, check_stated_tolerance,
-                         gpu_norm_and_coef, gpu_step, oracle_step, to_dev, to_host)
+                         golden_eps, gpu_norm_and_coef, gpu_step, oracle_step, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -198,8 +198,11 @@ def test_step_every_block_size_ragged(block, as_bf16):
 
 def test_step_hand_worked_examples():
     """The exact blocks of tests/golden (block size 4 there): each 4-element block is a
-    tensor of its own, which is one partial block at the GPU's block size 64."""
+    tensor of its own, which is one partial block at the GPU's block size 64.  Examples
+    worked with eps = 0 run with the smallest positive eps (golden_eps); eps = 0 itself
+    is rejected by the library."""
     for ex in adamw_examples():
+        eps = golden_eps(ex)
         n, b = ex["w"].size, ex["block_size"]
         for lo in range(0, n, b):
             hi = min(n, lo + b)
@@ -208,8 +211,14 @@ def test_step_hand_worked_examples():
                        [ex["m_absmax"][blk:blk + 1].copy()], [ex["v_codes"][lo:hi].copy()],
                        [ex["v_absmax"][blk:blk + 1].copy()]).to_dev()
             c = torch.tensor([ex["coef"]], dtype=torch.float32, device=DEV)
+            if ex["eps"] == 0:
+                with pytest.raises(lt.LazyTrainError) as e:
+                    gpu_step(st, [to_dev(ex["grad"][lo:hi].copy())], 64, ex["t"], coef=c,
+                             lr=ex["lr"], beta1=ex["beta1"], beta2=ex["beta2"], eps=0.0,
+                             weight_decay=ex["weight_decay"])
+                assert e.value.code == lt.LT_ERR_INVALID_ARG
             gpu_step(st, [to_dev(ex["grad"][lo:hi].copy())], 64, ex["t"], coef=c, lr=ex["lr"],
-                     beta1=ex["beta1"], beta2=ex["beta2"], eps=ex["eps"],
+                     beta1=ex["beta1"], beta2=ex["beta2"], eps=eps,
                      weight_decay=ex["weight_decay"])
             got = st.to_host()
             assert np.array_equal(got.w[0], ex["expect_w"][lo:hi]), ex["name"]
@@ -267,15 +276,32 @@ def test_validation_errors_are_reported_before_launch():
     g = torch.zeros(4096, dtype=torch.bfloat16, device=DEV)
     mq = torch.zeros(4096, dtype=torch.int8, device=DEV)
     vq = torch.zeros(4096, dtype=torch.uint8, device=DEV)
-    ma = torch.zeros(8, dtype=torch.float32, device=DEV)  # enough for any block size tried
-    va = torch.zeros(8, dtype=torch.float32, device=DEV)
+    ma = torch.zeros(128, dtype=torch.float32, device=DEV)  # enough for any block size tried
+    va = torch.zeros(128, dtype=torch.float32, device=DEV)
     args = dict(lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, step=1)
     with pytest.raises(lt.LazyTrainError) as e:
         lt.lt_hybrid8bit_adamw_step([w[1:4097]], [g], [mq], [ma], [vq], [va], 2048, **args)
     assert e.value.code == 2  # LT_ERR_ALIGNMENT: 4-byte offset view
     with pytest.raises(lt.LazyTrainError) as e:
         lt.lt_hybrid8bit_adamw_step([w[:4096]], [g], [mq], [ma], [vq], [va], 1000, **args)
-    assert e.value.code == 1  # block size not a power of two
+    assert e.value.code == 1  # block size not a multiple of 64
+    for bad_block in (0, 32, 96, 65536 + 64):
+        with pytest.raises(lt.LazyTrainError) as e:
+            lt.lt_hybrid8bit_adamw_step([w[:4096]], [g], [mq], [ma], [vq], [va], bad_block,
+                                        **args)
+        assert e.value.code == 1
+    # eps must be positive, also once rounded to fp32 (eps = 0 divides 0 by 0 on a
+    # zero gradient over a zero second moment)
+    for bad_eps in (0.0, -1e-8, 1e-50, float("inf"), float("nan")):
+        with pytest.raises(lt.LazyTrainError) as e:
+            lt.lt_hybrid8bit_adamw_step([w[:4096]], [g], [mq], [ma], [vq], [va], 2048,
+                                        **dict(args, eps=bad_eps))
+        assert e.value.code == 1
+        m32 = torch.zeros(4096, dtype=torch.float32, device=DEV)
+        with pytest.raises(lt.LazyTrainError) as e:
+            lt.lt_adamw_fp32_step([w[:4096]], [g], [m32], [m32.clone()],
+                                  **dict(args, eps=bad_eps))
+        assert e.value.code == 1
     with pytest.raises(lt.LazyTrainError) as e:
         lt.lt_hybrid8bit_adamw_step([w[:4096]], [g], [mq], [ma], [vq], [va], 2048,
                                     **dict(args, beta1=1.0))
@@ -297,7 +323,7 @@ def test_validation_errors_are_reported_before_launch():
     numels = (ctypes.c_int64 * 1)(g.numel())
     rc = lt.lib().lt_grad_sqnorm(ptrs, numels, 1, lt.LT_DTYPE_BF16, small.data_ptr(), 256, None,
                                  S.data_ptr(), st.data_ptr(), None)
-    assert rc == 3  # LT_ERR_WORKSPACE
+    assert rc == 4  # LT_ERR_WORKSPACE
     assert b"workspace" in lt.lib().lt_last_error()
     rc = lt.lib().lt_grad_sqnorm(ptrs, numels, 1, 7, small.data_ptr(), 256, None, S.data_ptr(),
                                  st.data_ptr(), None)
@@ -305,11 +331,13 @@ def test_validation_errors_are_reported_before_launch():
 
 
 def test_optimizer_object_two_steps_against_oracle():
+    """The optimizer object with its defaults (the decade-tree code map)."""
     rng = np.random.default_rng(12)
     sizes = [5000, 4096 * 3]
     w0 = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
     params = [to_dev(x) for x in w0]
     opt = lt.Hybrid8bitAdamW(params, lr=1e-5, block_size=4096)
+    assert opt.code_map == lt.LT_MAP_DYNAMIC
     ref = State.zero_host(w0, 4096)
     for t in (1, 2):
         g = [f32_to_bf16_bits((rng.standard_t(3, size=n) * 1e-2).astype(np.float32))
@@ -318,7 +346,8 @@ def test_optimizer_object_two_steps_against_oracle():
         assert opt.last_status() == lt.LT_STATUS_OK
         _, S, st = oracle.grad_sqnorm(g)
         _, c = oracle.clip_coef(S, 1.0)
-        oracle_step(ref, g, 4096, t, coef=float(c), status=st, lr=1e-5)
+        oracle_step(ref, g, 4096, t, coef=float(c), status=st, lr=1e-5,
+                    code_map=oracle.MAP_DYNAMIC)
     got = State([to_host(p) for p in params], [to_host(x) for x in opt.m_codes],
                 [to_host(x) for x in opt.m_absmax], [to_host(x) for x in opt.v_codes],
                 [to_host(x) for x in opt.v_absmax])

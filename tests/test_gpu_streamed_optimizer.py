@@ -46,7 +46,8 @@ def test_steps_and_skip_against_oracle(keep):
     params = [torch.from_numpy(x.copy()).pin_memory() for x in w0]
     opt = lt.StreamedHybrid8bitAdamW(params, first, DEV, lr=HYPER["lr"], betas=(0.9, 0.999),
                                      eps=HYPER["eps"], weight_decay=HYPER["weight_decay"],
-                                     block_size=BLOCK, keep_grads=keep)
+                                     block_size=BLOCK, keep_grads=keep,
+                                     code_map=lt.LT_MAP_LINEAR)
     ref = State.zero_host(w0, BLOCK)
     t = 0
     for call, bad in enumerate((False, True, False, False)):
