@@ -1,14 +1,18 @@
-"""GPU parity at full size, in the launch configuration bench.py times.
+"""GPU parity at full size, in the launch configuration bench.py times: every
+block of every tensor, compared bitwise with the oracle.
 
-3B-class full model (325 tensors, 3.09e9 parameters): the sum of squares, norm and
-clip coefficient over all gradients are compared bitwise with the oracle; the step
-is compared bitwise on sampled blocks (the first and last block of every tensor and
-random blocks), which the oracle recomputes one by one from the generator; every
-block of every tensor is checked for the properties the quantizer guarantees at any
-size.  The clip-stress variant runs three steps from zero state with fresh
-gradients, all-zero blocks and +-1e4 outliers, in lockstep (the oracle starts each
-step from the GPU's state of the sampled blocks) and free-running (the oracle's own
-three-step state)."""
+* 3B-class full model (325 tensors, 3.09e9 parameters, 1,506,760 blocks of 2048):
+  the states of one prior step (t = 1, lr = 0), then the clipped step at t = 2.
+  S_k, S, the norm and the coefficient, and then the weights, both code arrays and
+  both scale arrays of all tensors are compared with the oracle's, with both code
+  maps.
+* Clip-stress variant (same shapes; gradients with +-1e4 outliers and all-zero
+  blocks): three steps from zero state.  The oracle runs free on its own state, so
+  bitwise equality of every array after every step also shows the two sides in
+  lockstep (S19): nothing drifts apart.
+
+Both sides take the same generator output: it is drawn once on the host, copied
+to HBM for the HIP path, and then updated in place by the oracle."""
 import time
 
 import numpy as np
@@ -31,42 +35,52 @@ def _hyper(w):
     return dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay)
 
 
-class Device:
-    """The workload's tensors in HBM, filled from the generator one tensor at a time."""
+def _omap(code_map):
+    return oracle.MAP_DYNAMIC if code_map == lt.LT_MAP_DYNAMIC else oracle.MAP_LINEAR
+
+
+class Model:
+    """One workload's state on both sides: host arrays (the oracle's) and device
+    tensors (the HIP path's), starting from the same generated weights and zero
+    8-bit states."""
 
     def __init__(self, w, n_threads):
-        self.w, self.B = w, w.block_size
-        big = max(w.numels)
+        self.w, self.B, self.n_threads = w, w.block_size, n_threads
+        K = len(w.numels)
+        t0 = time.time()
+        self.hw = [w.weights(k, n_threads=n_threads) for k in range(K)]
+        self.hmq = [np.zeros(n, np.int8) for n in w.numels]
+        self.hvq = [np.zeros(n, np.uint8) for n in w.numels]
+        nb = [-(-n // self.B) for n in w.numels]
+        self.hma = [np.zeros(n, np.float32) for n in nb]
+        self.hva = [np.zeros(n, np.float32) for n in nb]
+        self.params = [torch.from_numpy(x).to(DEV) for x in self.hw]
+        self.mq = [torch.zeros(n, dtype=torch.int8, device=DEV) for n in w.numels]
+        self.vq = [torch.zeros(n, dtype=torch.uint8, device=DEV) for n in w.numels]
+        self.ma = [torch.zeros(n, dtype=torch.float32, device=DEV) for n in nb]
+        self.va = [torch.zeros(n, dtype=torch.float32, device=DEV) for n in nb]
         gdt = torch.bfloat16 if w.grad_dtype == synth.BF16 else torch.float32
-        self.stage_w = torch.empty(big, dtype=torch.float32, pin_memory=True)
-        self.stage_g = torch.empty(big, dtype=gdt, pin_memory=True)
-        self.n_threads = n_threads
-        self.params, self.grads, self.mq, self.vq, self.ma, self.va = [], [], [], [], [], []
-        for k, n in enumerate(w.numels):
-            synth.fill_ptr(self.stage_w.data_ptr(), synth.F32, 0, n, w.seed,
-                           synth.STREAM_WEIGHTS, k, w.weight_recipe, n_threads)
-            self.params.append(self.stage_w[:n].to(DEV))
-            self.grads.append(torch.empty(n, dtype=gdt, device=DEV))
-            nb = -(-n // self.B)
-            self.mq.append(torch.zeros(n, dtype=torch.int8, device=DEV))
-            self.vq.append(torch.zeros(n, dtype=torch.uint8, device=DEV))
-            self.ma.append(torch.zeros(nb, dtype=torch.float32, device=DEV))
-            self.va.append(torch.zeros(nb, dtype=torch.float32, device=DEV))
+        self.grads = [torch.empty(n, dtype=gdt, device=DEV) for n in w.numels]
         self.S = torch.zeros(1, dtype=torch.float64, device=DEV)
-        self.sk = torch.zeros(len(w.numels), dtype=torch.float64, device=DEV)
+        self.sk = torch.zeros(K, dtype=torch.float64, device=DEV)
         self.status = torch.zeros(1, dtype=torch.int32, device=DEV)
         self.coef = torch.zeros(1, dtype=torch.float32, device=DEV)
         self.norm = torch.zeros(1, dtype=torch.float32, device=DEV)
+        torch.cuda.synchronize()
+        _say(f"{w.name}: {w.n_params} params generated and in HBM ({time.time() - t0:.1f} s)")
 
-    def load_grads(self, stream):
-        w = self.w
-        for k, n in enumerate(w.numels):
-            synth.fill_ptr(self.stage_g.data_ptr(), w.grad_dtype, 0, n, w.seed, stream, k,
-                           w.grad_recipe, self.n_threads)
-            self.grads[k].copy_(self.stage_g[:n])
+    def host_grads(self, stream):
+        return [self.w.grads(k, stream, n_threads=self.n_threads)
+                for k in range(len(self.w.numels))]
+
+    def load(self, hg):
+        for d, h in zip(self.grads, hg):
+            src = torch.from_numpy(h.view(np.int16)).view(torch.bfloat16) \
+                if h.dtype == np.uint16 else torch.from_numpy(h)
+            d.copy_(src)
         torch.cuda.synchronize()
 
-    def step(self, t, clip=True, code_map=lt.LT_MAP_LINEAR, **over):
+    def gpu_step(self, t, code_map, clip=True, **over):
         h = dict(_hyper(self.w), **over)
         if clip:
             lt.lt_grad_sqnorm(self.grads, self.S, self.status, sq_per_tensor=self.sk)
@@ -79,170 +93,95 @@ class Device:
                                         self.va, self.B, step=t, code_map=code_map, **h)
         torch.cuda.synchronize()
 
-    def read_blocks(self, blocks):
-        """Host copies of (w, m codes, m absmax, v codes, v absmax) of blocks (k, b)."""
-        out = []
-        for k, b in blocks:
-            lo = b * self.B
-            hi = min(self.w.numels[k], lo + self.B)
-            out.append((to_host(self.params[k][lo:hi]), to_host(self.mq[k][lo:hi]),
-                        to_host(self.ma[k][b:b + 1]), to_host(self.vq[k][lo:hi]),
-                        to_host(self.va[k][b:b + 1])))
-        return out
+    def oracle_step(self, hg, t, code_map, coef=None, status=None, **over):
+        h = dict(_hyper(self.w), **over)
+        oracle.hybrid8bit_adamw_step(self.hw, hg, self.hmq, self.hma, self.hvq, self.hva, self.B,
+                                     step=t, coef=coef, status=status, n_threads=self.n_threads,
+                                     code_map=_omap(code_map), **h)
+
+    def check_norm(self, hg):
+        """S_k, S, norm and coefficient bitwise; returns the oracle's (S, status, coef)."""
+        rsk, rS, rst = oracle.grad_sqnorm(hg, n_threads=self.n_threads)
+        rnorm, rcoef = oracle.clip_coef(rS, self.w.max_norm)
+        assert to_host(self.S)[0].hex() == rS.hex()
+        assert to_host(self.sk).tobytes() == rsk.tobytes()
+        assert int(to_host(self.status)[0]) == rst == oracle.STATUS_OK
+        assert to_host(self.norm)[0] == rnorm and to_host(self.coef)[0] == rcoef
+        return rS, rst, rcoef, rnorm
+
+    def compare_all(self, what):
+        """Every array of every tensor bitwise; returns the number of blocks compared."""
+        blocks = 0
+        pairs = (("w", self.params, self.hw), ("m codes", self.mq, self.hmq),
+                 ("m absmax", self.ma, self.hma), ("v codes", self.vq, self.hvq),
+                 ("v absmax", self.va, self.hva))
+        for k in range(len(self.w.numels)):
+            for name, dev, host in pairs:
+                a, b = to_host(dev[k]), host[k]
+                if a.tobytes() != b.tobytes():
+                    bad = np.flatnonzero(a.view(np.uint8 if a.itemsize == 1 else np.uint32) !=
+                                         b.view(np.uint8 if b.itemsize == 1 else np.uint32))
+                    raise AssertionError(f"{what}: tensor {k} {name} differs at {bad.size} "
+                                         f"positions (first {bad[:3]}, block {bad[0] // self.B})")
+            blocks += self.hma[k].size
+        return blocks
 
 
-def _sample_blocks(w, n_random, seed):
-    B = w.block_size
-    blocks = set()
-    for k, n in enumerate(w.numels):
-        nb = -(-n // B)
-        blocks.add((k, 0))
-        blocks.add((k, nb - 1))
-    rng = np.random.default_rng(seed)
-    p = np.array(w.numels, dtype=np.float64)
-    ks = rng.choice(len(w.numels), size=n_random, p=p / p.sum())
-    for k in ks:
-        blocks.add((int(k), int(rng.integers(0, -(-w.numels[k] // w.block_size)))))
-    return sorted(blocks)
+def _total_blocks(w):
+    return sum(-(-n // w.block_size) for n in w.numels)
 
 
-def _host_slices(w, blocks, stream):
-    B = w.block_size
-    gs = []
-    for k, b in blocks:
-        lo = b * B
-        n = min(w.numels[k], lo + B) - lo
-        gs.append(w.grads(k, stream, offset=lo, n=n, n_threads=1))
-    return gs
-
-
-def _full_grads(w, stream, n_threads):
-    return [w.grads(k, stream, n_threads=n_threads) for k in range(len(w.numels))]
-
-
-def _compare_blocks(got, want, what):
-    for i, (g, r) in enumerate(zip(got, want)):
-        for name, a, b in zip(("w", "m codes", "m absmax", "v codes", "v absmax"), g, r):
-            if a.tobytes() != b.tobytes():
-                bad = np.flatnonzero(a != b)
-                raise AssertionError(f"{what}: block #{i} {name} differs at {bad.size} "
-                                     f"positions (first {bad[:3]})")
-
-
-def _check_code_properties(dev, code_map=lt.LT_MAP_LINEAR):
-    """At any size: a block with a positive stored absmax holds a code of magnitude
-    127 (m) or 255 (v), since its largest element maps to full scale; a block with
-    absmax 0 holds only zero codes; every m code magnitude lies in [0, 127] (linear
-    codes are two's complement, dynamic codes sign-magnitude)."""
-    B = dev.B
-    for k, n in enumerate(dev.w.numels):
-        nb_full = n // B
-        for codes, absmax, top in ((dev.mq[k], dev.ma[k], 127), (dev.vq[k], dev.va[k], 255)):
-            if code_map == lt.LT_MAP_DYNAMIC and top == 127:
-                c = codes.view(torch.uint8).to(torch.int16) & 0x7F
-            else:
-                c = codes.to(torch.int16).abs()
-            assert int(c.max()) <= top
-            if nb_full:
-                blk_max = c[:nb_full * B].view(nb_full, B).amax(dim=1)
-                a = absmax[:nb_full]
-                assert bool(torch.all(torch.where(a > 0, blk_max == top, blk_max == 0)))
-                assert bool(torch.all(torch.isfinite(a)))
-
-
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("code_map", [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC])
-def test_full_3b_model_step_parity(code_map):
+def test_full_3b_model_every_block(code_map):
     w = synth.full_3b()
-    n_threads = synth.default_threads()
-    B, K = w.block_size, len(w.shapes)
-    _say(f"{w.name}: generating {w.n_params} params on the host and in HBM")
-    dev = Device(w, n_threads)
-    dev.load_grads(synth.STREAM_PRIOR_GRAD)
-    dev.step(1, clip=False, code_map=code_map, lr=0.0)  # states from one prior step
-    dev.load_grads(synth.grad_stream(w.step))
-    _say(f"GPU step at t = 2 (sum of squares, clip, fused step), code map {code_map}")
-    dev.step(w.step, code_map=code_map)
-    assert lt.lt_read_status(dev.status) == lt.LT_STATUS_OK
-
-    _say("oracle sum of squares over all gradients")
-    host_g = _full_grads(w, synth.grad_stream(w.step), n_threads)
-    rsk, rS, rst = oracle.grad_sqnorm(host_g, n_threads=n_threads)
-    del host_g
-    rnorm, rcoef = oracle.clip_coef(rS, w.max_norm)
-    assert to_host(dev.S)[0].hex() == rS.hex()
-    assert to_host(dev.sk).tobytes() == rsk.tobytes()
-    assert to_host(dev.norm)[0] == rnorm and to_host(dev.coef)[0] == rcoef
-    _say(f"S = {rS!r}, norm = {float(rnorm):.6g}, coef = {float(rcoef):.6g}: bitwise equal")
-
-    blocks = _sample_blocks(w, 3000, seed=11)
-    _say(f"oracle on {len(blocks)} sampled blocks")
-    ws, g0s, gs = [], _host_slices(w, blocks, synth.STREAM_PRIOR_GRAD), \
-        _host_slices(w, blocks, synth.grad_stream(w.step))
-    for k, b in blocks:
-        lo = b * B
-        ws.append(w.weights(k, offset=lo, n=min(w.numels[k], lo + B) - lo, n_threads=1))
-    mq = [np.zeros(x.size, np.int8) for x in ws]
-    vq = [np.zeros(x.size, np.uint8) for x in ws]
-    ma = [np.zeros(1, np.float32) for _ in ws]
-    va = [np.zeros(1, np.float32) for _ in ws]
-    h = _hyper(w)
-    oracle.hybrid8bit_adamw_step(ws, g0s, mq, ma, vq, va, B, step=1, n_threads=n_threads,
-                                 code_map=code_map, **dict(h, lr=0.0))
-    oracle.hybrid8bit_adamw_step(ws, gs, mq, ma, vq, va, B, step=w.step, coef=float(rcoef),
-                                 status=rst, n_threads=n_threads, code_map=code_map, **h)
-    _compare_blocks(dev.read_blocks(blocks), list(zip(ws, mq, ma, vq, va)), w.name)
-    _say("sampled blocks bitwise equal; checking code properties of every block")
-    _check_code_properties(dev, code_map)
+    m = Model(w, synth.default_threads())
+    g0 = m.host_grads(synth.STREAM_PRIOR_GRAD)
+    m.load(g0)
+    m.gpu_step(1, code_map, clip=False, lr=0.0)  # the states of one prior step
+    m.oracle_step(g0, 1, code_map, lr=0.0)
+    del g0
+    hg = m.host_grads(synth.grad_stream(w.step))
+    m.load(hg)
+    _say(f"GPU step at t = {w.step} (sum of squares, clip, fused step), code map {code_map}")
+    m.gpu_step(w.step, code_map)
+    rS, rst, rcoef, rnorm = m.check_norm(hg)
+    _say(f"S = {rS!r}, norm {float(rnorm):.6g}, coef {float(rcoef):.6g}: bitwise equal")
+    m.oracle_step(hg, w.step, code_map, coef=float(rcoef), status=rst)
+    n = m.compare_all(f"{w.name}, map {code_map}")
+    assert n == _total_blocks(w) == 1506760
+    _say(f"all {n} blocks of {len(w.numels)} tensors bitwise equal (w, codes, scales)")
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("code_map", [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC])
-def test_clip_stress_three_steps(code_map):
+def test_clip_stress_three_steps_every_block(code_map):
     w = synth.clip_stress()
-    n_threads = synth.default_threads()
-    B = w.block_size
-    _say(f"{w.name}: generating {w.n_params} params")
-    dev = Device(w, n_threads)
-    blocks = _sample_blocks(w, 2000, seed=12)
-    # add sampled all-zero blocks
-    zero_blocks = [(k, b) for (k, b) in _sample_blocks(w, 20000, seed=13)
-                   if synth.block_is_zero(w.seed, k, b, w.grad_recipe.zero_mod)][:200]
-    blocks = sorted(set(blocks) | set(zero_blocks))
-    h = _hyper(w)
-    free = None  # the oracle's own state of the sampled blocks (free-running)
+    m = Model(w, synth.default_threads())
+    # all-zero blocks of the gradients (the same in every step), checked by name below
+    rng = np.random.default_rng(13)
+    zero_blocks = []
+    while len(zero_blocks) < 200:
+        k = int(rng.integers(0, len(w.numels)))
+        b = int(rng.integers(0, -(-w.numels[k] // w.block_size)))
+        if synth.block_is_zero(w.seed, k, b, w.grad_recipe.zero_mod):
+            zero_blocks.append((k, b))
     for t in (1, 2, 3):
-        stream = synth.grad_stream(t)
-        before = dev.read_blocks(blocks)
-        if free is None:
-            free = [tuple(a.copy() for a in blk) for blk in before]
-        dev.load_grads(stream)
-        _say(f"step t = {t}: GPU")
-        dev.step(t, code_map=code_map)
-        assert lt.lt_read_status(dev.status) == lt.LT_STATUS_OK
-        host_g = _full_grads(w, stream, n_threads)
-        rsk, rS, rst = oracle.grad_sqnorm(host_g, n_threads=n_threads)
-        del host_g
-        rnorm, rcoef = oracle.clip_coef(rS, w.max_norm)
-        assert to_host(dev.S)[0].hex() == rS.hex()
-        assert to_host(dev.coef)[0] == rcoef
+        hg = m.host_grads(synth.grad_stream(t))
+        m.load(hg)
+        _say(f"step t = {t}: GPU, code map {code_map}")
+        m.gpu_step(t, code_map)
+        rS, rst, rcoef, rnorm = m.check_norm(hg)
         _say(f"  S bitwise equal; norm {float(rnorm):.6g}, coef {float(rcoef):.6g}")
-        gs = _host_slices(w, blocks, stream)
-        # lockstep: the oracle starts from the GPU's state of each sampled block
-        lock = [tuple(a.copy() for a in blk) for blk in before]
-        oracle.hybrid8bit_adamw_step([x[0] for x in lock], gs, [x[1] for x in lock],
-                                     [x[2] for x in lock], [x[3] for x in lock],
-                                     [x[4] for x in lock], B, step=t, coef=float(rcoef),
-                                     status=rst, n_threads=n_threads, code_map=code_map, **h)
-        after = dev.read_blocks(blocks)
-        _compare_blocks(after, lock, f"lockstep t = {t}")
-        oracle.hybrid8bit_adamw_step([x[0] for x in free], gs, [x[1] for x in free],
-                                     [x[2] for x in free], [x[3] for x in free],
-                                     [x[4] for x in free], B, step=t, coef=float(rcoef),
-                                     status=rst, n_threads=n_threads, code_map=code_map, **h)
-        _compare_blocks(after, free, f"free-running t = {t}")
-        for (k, b), blk in zip(blocks, after):
-            if (k, b) in zero_blocks:
-                assert not blk[1].any() and not blk[3].any() and blk[2][0] == 0 and blk[4][0] == 0
-        _say(f"  {len(blocks)} sampled blocks bitwise equal (lockstep and free-running)")
-    _check_code_properties(dev, code_map)
+        m.oracle_step(hg, t, code_map, coef=float(rcoef), status=rst)
+        del hg
+        n = m.compare_all(f"{w.name}, map {code_map}, t = {t}")
+        assert n == _total_blocks(w)
+        _say(f"  all {n} blocks bitwise equal to the free-running oracle")
+        B = w.block_size
+        for k, b in zero_blocks:
+            lo, hi = b * B, min(w.numels[k], (b + 1) * B)
+            assert not m.hmq[k][lo:hi].any() and not m.hvq[k][lo:hi].any()
+            assert m.hma[k][b] == 0 and m.hva[k][b] == 0
     # the reading of this workload: norm ~ 1.76e7 from the +-9984 outliers
     assert 1.5e7 < float(rnorm) < 2.0e7

@@ -9,9 +9,9 @@ configuration bench.py times (27B-class decoder layers of hidden 5120, FFN 17408
   the oracle's.  (Pass 2 writes the shared host state of several layers, so its
   results are not checked here.)
 * Eight distinct layers (2.6e9 parameters, every tensor at its full size) from zero
-  state, with the gradients copied in twice and kept in HBM between the passes: S and the coefficient bitwise, and the updated weights, codes and scales of
-  sampled blocks (the first and last block of every tensor and random ones),
-  which the oracle recomputes block by block from the generator."""
+  state, with the gradients copied in twice and kept in HBM between the passes: S
+  and the coefficient bitwise, and the updated weights, codes and scales of every
+  block of every tensor against the oracle run over the same host data."""
 import time
 
 import numpy as np
@@ -102,8 +102,9 @@ def test_whole_model_norm_and_coefficient_as_benchmarked(host_model):
     _say(f"S = {S_o!r}, norm {float(n_o):.6g}, coef {float(c_o):.6g}: bitwise equal")
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("keep", [False, True])
-def test_eight_full_size_layers_against_oracle_blocks(host_model, keep):
+def test_eight_full_size_layers_against_oracle(host_model, keep):
     w8, h = host_model
     B = w8.block_size
     # fresh state: the weights from the generator, zero codes and scales
@@ -130,25 +131,23 @@ def test_eight_full_size_layers_against_oracle_blocks(host_model, keep):
     assert int(to_host(status)[0]) == st_o == oracle.STATUS_OK
     assert to_host(S)[0].hex() == S_o.hex() and to_host(coef)[0] == c_o
 
-    rng = np.random.default_rng(27)
-    blocks = set()
-    for k, n in enumerate(w8.numels):
-        nb = -(-n // B)
-        blocks.update({(k, 0), (k, nb - 1)})
-        blocks.update((k, int(b)) for b in rng.integers(0, nb, size=4))
-    _say(f"oracle on {len(blocks)} sampled blocks")
-    for k, b in sorted(blocks):
-        lo = b * B
-        n = min(w8.numels[k], lo + B) - lo
-        wr = w8.weights(k, offset=lo, n=n, n_threads=1)
-        gr = _grad_bits(h["g"][k])[lo:lo + n].copy()
-        mq, vq = np.zeros(n, np.int8), np.zeros(n, np.uint8)
-        ma, va = np.zeros(1, np.float32), np.zeros(1, np.float32)
-        oracle.hybrid8bit_adamw_step([wr], [gr], [mq], [ma], [vq], [va], B, step=1,
-                                     coef=float(c_o), status=st_o, **_hyper(w8))
-        got = (h["w"][k][lo:lo + n].numpy(), h["mq"][k][lo:lo + n].numpy(),
-               h["ma"][k][b:b + 1].numpy(), h["vq"][k][lo:lo + n].numpy(),
-               h["va"][k][b:b + 1].numpy())
-        for name, a, r in zip(("w", "m codes", "m absmax", "v codes", "v absmax"), got,
-                              (wr, mq, ma, vq, va)):
-            assert a.tobytes() == r.tobytes(), f"tensor {k} block {b}: {name} differs"
+    _say("oracle over all 72 tensors (every block)")
+    ref_w = [w8.weights(k, n_threads=n_threads) for k in range(len(w8.numels))]
+    ref_g = [_grad_bits(g) for g in h["g"]]
+    ref_mq = [np.zeros(n, np.int8) for n in w8.numels]
+    ref_vq = [np.zeros(n, np.uint8) for n in w8.numels]
+    ref_ma = [np.zeros(-(-n // B), np.float32) for n in w8.numels]
+    ref_va = [np.zeros(-(-n // B), np.float32) for n in w8.numels]
+    oracle.hybrid8bit_adamw_step(ref_w, ref_g, ref_mq, ref_ma, ref_vq, ref_va, B, step=1,
+                                 coef=float(c_o), status=st_o, n_threads=n_threads,
+                                 **_hyper(w8))
+    blocks = 0
+    for k in range(len(w8.numels)):
+        for name, got, want in (("w", h["w"][k], ref_w[k]), ("m codes", h["mq"][k], ref_mq[k]),
+                                ("m absmax", h["ma"][k], ref_ma[k]),
+                                ("v codes", h["vq"][k], ref_vq[k]),
+                                ("v absmax", h["va"][k], ref_va[k])):
+            assert got.numpy().tobytes() == want.tobytes(), f"tensor {k}: {name} differs"
+        blocks += ref_ma[k].size
+    assert blocks == sum(-(-n // B) for n in w8.numels)
+    _say(f"all {blocks} blocks of the 8 layers bitwise equal (keep_grads {keep})")
