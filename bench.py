@@ -399,6 +399,51 @@ def stream_ceiling(n_elements: int, pattern: str = "step8"):
     return json.loads(r.stdout.strip().splitlines()[-1])
 
 
+def same_array_probe(params, grads, m_codes, v_codes, gbytes, dev, stream, reps=3):
+    """Times paper_2608_11919_amd/libltprobe.so (csrc/mix_probe.hip) over the step's
+    own arrays, in this process: the fused step's per-element bytes (the weight, the
+    gradient and both codes read; the weight and both codes written back in place)
+    in the step kernel's geometry and unit order, with no arithmetic.  An even number
+    of passes XORs every array back to its contents.  Returns (median ms, bytes)."""
+    import ctypes
+
+    import torch
+    path = os.path.join(ROOT, "paper_2608_11919_amd", "libltprobe.so")
+    if not os.path.exists(path):
+        log("libltprobe.so is not built; no same-array probe")
+        return None
+    L = ctypes.CDLL(path)
+    L.ltp_mix_same_arrays.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                      ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    L.ltp_mix_same_arrays.restype = ctypes.c_int
+    K = len(params)
+    units = [-(-p.numel() // 2048) for p in params]
+    prefix = [0]
+    for u in units:
+        prefix.append(prefix[-1] + u)
+    d_prefix = torch.tensor(prefix, dtype=torch.int64, device=dev)
+    table = torch.zeros((K, 8), dtype=torch.int64)
+    for k in range(K):
+        table[k, :5] = torch.tensor([params[k].data_ptr(), grads[k].data_ptr(),
+                                     m_codes[k].data_ptr(), v_codes[k].data_ptr(),
+                                     params[k].numel()], dtype=torch.int64)
+    d_table = table.to(dev)
+    grid = 3 * torch.cuda.get_device_properties(dev).multi_processor_count
+    ms = []
+    for _ in range(2 * reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        rc = L.ltp_mix_same_arrays(d_prefix.data_ptr(), d_table.data_ptr(), K, prefix[-1], gbytes,
+                                   grid, stream.cuda_stream)
+        b.record(stream)
+        if rc != 0:
+            raise RuntimeError(f"ltp_mix_same_arrays failed ({rc})")
+        torch.cuda.synchronize()
+        ms.append(a.elapsed_time(b))
+    n = sum(p.numel() for p in params)
+    return sorted(ms)[len(ms) // 2], n * (12 + gbytes)
+
+
 def copy_probe(dev, nbytes: int, reps: int):
     """A plain copy kernel of known size, for scaling the HBM byte counters."""
     import torch
@@ -442,6 +487,15 @@ def main() -> int:
                     help="skip the data-movement ceiling probe")
     ap.add_argument("--copy-probe-bytes", type=int, default=0,
                     help="also run a plain copy of this many bytes (counter scaling)")
+    ap.add_argument("--flush-bytes", type=int, default=0,
+                    help="write a scratch buffer of this many bytes between steps, outside the "
+                         "timed events, so no step finds the previous one's data in the 256 MB "
+                         "Infinity Cache (for workloads that fit in it); the step time is then "
+                         "the mean of the per-step events")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one whole step (norm, clip, step at a fixed step index) in a "
+                         "HIP graph after the warmup and time replays of it (launch-bound "
+                         "small workloads)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -505,26 +559,36 @@ def main() -> int:
         wb = [torch.empty(n, dtype=torch.bfloat16, device=dev) for n in w.numels]
         wb8, wb32 = [wb[k] for k in idx8], [wb[k] for k in idx32]
 
-    def one_step(t, ev=None):
+    def one_step(t, ev=None, st=None):
+        st = stream if st is None else st
         if ev:
-            ev[0].record(stream)
-        lt.lt_grad_sqnorm(grads, sq_total, status, workspace=ws_sq, stream=stream)
-        lt.lt_clip_coef(sq_total, w.max_norm, coef, total_norm=norm, stream=stream)
+            ev[0].record(st)
+        lt.lt_grad_sqnorm(grads, sq_total, status, workspace=ws_sq, stream=st)
+        lt.lt_clip_coef(sq_total, w.max_norm, coef, total_norm=norm, stream=st)
         if ev:
-            ev[1].record(stream)
+            ev[1].record(st)
         if p8:
             lt.lt_hybrid8bit_adamw_step(p8, g8, *s8, B, step=t, coef=coef, status=status,
-                                        workspace=ws_step, stream=stream, params_bf16=wb8,
+                                        workspace=ws_step, stream=st, params_bf16=wb8,
                                         code_map=code_map, **hyper)
         if p32:
             lt.lt_adamw_fp32_step(p32, g32, exp_avg, exp_avg_sq, step=t, coef=coef,
-                                  status=status, workspace=ws_32, stream=stream,
+                                  status=status, workspace=ws_32, stream=st,
                                   params_bf16=wb32, **hyper)
         if ev:
-            ev[2].record(stream)
+            ev[2].record(st)
+
+    scratch = None
+    if args.flush_bytes:
+        scratch = torch.empty(args.flush_bytes // 4, dtype=torch.float32, device=dev)
+
+    def flush():
+        if scratch is not None:
+            scratch.fill_(float(t))  # a kernel that writes every byte (no memset node)
 
     t = t_first
     for _ in range(args.warmup):
+        flush()
         one_step(t)
         t += 1
     torch.cuda.synchronize()
@@ -532,15 +596,46 @@ def main() -> int:
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        flush()
         one_step(t, events[i])
         t += 1
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     st = lt.lt_read_status(status)
+    graph = None
+    if args.graph:
+        # The calls above left every descriptor in its workspace, so the step captures
+        # whole; each replay is one full step at step index t.  The eager steps above
+        # give the per-kernel events; the replays give the step time.
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(stream)
+        with torch.cuda.graph(graph, stream=side):
+            one_step(t, st=side)
+        torch.cuda.synchronize()
+        log(f"one step captured in a HIP graph (step index {t})")
+        gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        graph.replay()  # a first replay outside the timed region
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            flush()
+            gev[i][0].record(stream)
+            graph.replay()
+            gev[i][1].record(stream)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        st = lt.lt_read_status(status)
 
     norm_ms = [e[0].elapsed_time(e[1]) for e in events]
     step_ms = [e[1].elapsed_time(e[2]) for e in events]
     whole_ms = [e[0].elapsed_time(e[2]) for e in events]
+    if graph is not None:
+        whole_ms = [e[0].elapsed_time(e[1]) for e in gev]
+    if scratch is not None:
+        # the flushes between steps are not step work: the step time is the mean of
+        # the per-step events
+        elapsed = sum(whole_ms) * 1e-3
 
     def pct(xs, q):  # nearest-rank percentile
         xs = sorted(xs)
@@ -565,6 +660,8 @@ def main() -> int:
         f"({nbytes / avg_norm_s / 1e9:.0f} GB/s)")
 
     out_workload = (w.name + (f"-block{B}" if args.block_size else "") +
+                    ("+graph" if graph is not None else "") +
+                    ("+cache-flushed" if scratch is not None else "") +
                     ("" if not idx32 else f"-hybrid-{args.slice_fraction:g}-8bit") +
                     ("+bf16-copy" if args.bf16_copy else "") +
                     ("+dynamic-map" if args.code_map == "dynamic" else ""))
@@ -582,6 +679,10 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "step_ms_events": spread(whole_ms),
+        "timing": ("per-step events, a write of " + str(args.flush_bytes) + " bytes between "
+                   "steps outside them" if scratch is not None else
+                   "wall clock over the timed steps") +
+                  ("; replays of one captured step" if graph is not None else ""),
         "config": {"workload": out_workload,
                    "params": w.n_params, "tensors": K, "block_size": B,
                    "params_8bit": sum(w.numels[k] for k in idx8),
@@ -605,6 +706,20 @@ def main() -> int:
                      "bytes_per_launch": kbytes},
         "status": st,
     }
+    if not args.no_ceiling and not idx32 and not args.bf16_copy:
+        probe = same_array_probe(p8, g8, s8[0], s8[2], gb, dev, stream)
+        if probe is not None:
+            p_ms, p_bytes = probe
+            p_gbps = p_bytes / (p_ms * 1e-3) / 1e9
+            out["same_array_probe"] = {
+                "probe": "csrc/mix_probe.hip over the step's own arrays in this process: the "
+                         "step kernel's bytes per element, geometry and unit order, no "
+                         "arithmetic (scales not moved)",
+                "ms": round(p_ms, 4), "bytes": p_bytes, "gbps": round(p_gbps, 1),
+                "frac_of_peak": round(p_gbps / PEAK_HBM_GBPS, 4),
+                "step_kernel_frac_of_probe": round(achieved / p_gbps, 4)}
+            log(f"same-array probe: {p_ms:.3f} ms, {p_gbps:.0f} GB/s; the step kernel runs at "
+                f"{achieved / p_gbps:.3f} of it")
     if not args.no_ceiling and gb == 2:
         # the probe pattern of each step kernel, at the whole model's size; the hybrid
         # step's two kernels are priced at their own patterns' rates

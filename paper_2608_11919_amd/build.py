@@ -29,6 +29,8 @@ def hipcc() -> str:
 
 CEILING = os.path.join(HERE, "stream_ceiling")
 CEILING_SOURCE = os.path.join(HERE, "csrc", "stream_ceiling.hip")
+PROBE = os.path.join(HERE, "libltprobe.so")
+PROBE_SOURCE = os.path.join(HERE, "csrc", "mix_probe.hip")
 
 
 def build(verbose: bool = False, extra_flags=()) -> str:
@@ -39,6 +41,7 @@ def build(verbose: bool = False, extra_flags=()) -> str:
     subprocess.run(cmd, check=True)
     os.replace(LIB + ".tmp", LIB)
     build_ceiling_probe(verbose)
+    build_mix_probe(verbose)
     return LIB
 
 
@@ -51,6 +54,17 @@ def build_ceiling_probe(verbose: bool = False) -> str:
     subprocess.run(cmd, check=True)
     os.replace(CEILING + ".tmp", CEILING)
     return CEILING
+
+
+def build_mix_probe(verbose: bool = False) -> str:
+    """The same-array data-movement probe bench.py times beside the step (a library
+    of its own: nothing of the optimizer loads it)."""
+    cmd = [hipcc()] + HIPCC_FLAGS + ["-o", PROBE + ".tmp", PROBE_SOURCE]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(PROBE + ".tmp", PROBE)
+    return PROBE
 
 
 if __name__ == "__main__":
