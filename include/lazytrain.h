@@ -131,6 +131,24 @@ lt_err lt_grad_sqnorm(const void* const* grads, const int64_t* numels, int n_ten
                       double* sq_per_tensor, double* sq_total, int32_t* status, void* stream);
 
 /*
+ * For callers that cannot allocate device memory: code under HIP graph capture,
+ * serving loops and harnesses that forbid hipMalloc.  Steps a1-a2 exactly as
+ * lt_grad_sqnorm (same arguments without the workspace, same results bit for
+ * bit), with the descriptors and partial sums held in a 16 MiB array of the
+ * library's own in device memory (one per device, for the process's lifetime),
+ * written by kernels from kernel arguments: the call allocates nothing, stages
+ * nothing on the host and copies nothing from it.  Lists whose descriptors and
+ * partials need more than 16 MiB (about 2 million 8192-element chunks, some
+ * 1.7e10 elements) return LT_ERR_INVALID_ARG before any device work.  All calls
+ * on one device share that array: calls that overlap on the device (on different
+ * streams, or from different host threads) race and give undefined results; calls
+ * in one stream's order do not.  Nothing in the array needs to start at zero.
+ */
+lt_err lt_grad_sqnorm_noalloc(const void* const* grads, const int64_t* numels, int n_tensors,
+                              int grad_dtype, double* sq_per_tensor, double* sq_total,
+                              int32_t* status, void* stream);
+
+/*
  * Step a3: clip coefficient, device-resident (Sec. 3.5 scale step; App. C max
  * grad norm).  total_norm = fp32(sqrt(*sq_total)): the fp64 square root, correctly
  * rounded, then rounded to fp32 (ties to even);

@@ -13,5 +13,6 @@ from .lazytrain import (  # noqa: F401
     lt_read_status, lt_set_max_workgroups, lt_step_workspace_bytes,
     lt_streamed_hybrid8bit_adamw_step, lt_streamed_workspace_bytes, lt_adamw_fp32_step,
     lt_adamw_fp32_workspace_bytes, lt_select_8bit_slice, lt_grad_chunk_count,
-    lt_grad_sqnorm_partials, lt_grad_sqnorm_finish, lt_workspace_release, GradNormAccumulator,
+    lt_grad_sqnorm_partials, lt_grad_sqnorm_finish, lt_workspace_release, lt_grad_sqnorm_noalloc,
+    GradNormAccumulator,
     StreamedHybrid8bitAdamW)

@@ -2021,6 +2021,89 @@ bool valid_layers(const int* first, int L, int K)
     return true;
 }
 
+// ------------------------------------- the sum of squares without allocation
+//
+// lt_grad_sqnorm_noalloc keeps what lt_grad_sqnorm keeps in its workspace (the
+// descriptors, one fp64 partial per chunk, S_k) in `scratch`, a device array of
+// this file that every device the library runs on holds until the process ends.
+// Its descriptors are written by k_put_words from kernel arguments, so the call
+// needs no staging buffer and no copy from the host, and allocates nothing.  In
+// host code `scratch` names a host-side stand-in: the device address comes from
+// hipGetSymbolAddress, once per device, and only that address is used.
+constexpr size_t kScratchBytes = size_t(16) << 20;  // 16 MiB per device
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+struct ScratchAddress {
+    uint8_t* ptr = nullptr;  // this device's copy of `scratch`
+    bool ready = false;
+};
+ScratchAddress g_scratch[kMaxDevices];
+
+// The device address of `scratch` on the current device (looked up on the first
+// call on that device, with it current).
+lt_err scratch_address(uint8_t** out)
+{
+    int dev;
+    if (lt_err e = current_device(&dev))
+        return e;
+    std::lock_guard<std::mutex> lock(g_dev[dev].mu);
+    ScratchAddress& a = g_scratch[dev];
+    if (!a.ready) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(LT_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") +
+                                        hipGetErrorString(e));
+        a.ptr = static_cast<uint8_t*>(p);
+        a.ready = true;
+    }
+    *out = a.ptr;
+    return LT_OK;
+}
+
+// One launch writes up to kPutWords consecutive 8-byte words at base + offset.
+constexpr int kPutWords = 440;  // 3.5 KB of kernel arguments
+struct PutWords {
+    uint64_t offset;  // bytes, a multiple of 8
+    uint32_t n;
+    uint32_t pad;
+    uint64_t w[kPutWords];
+};
+
+__global__ __launch_bounds__(256) void k_put_words(uint8_t* __restrict__ base, PutWords a)
+{
+    auto* dst = reinterpret_cast<uint64_t*>(base + a.offset);
+    for (uint32_t i = threadIdx.x; i < a.n; i += blockDim.x)
+        dst[i] = a.w[i];
+}
+
+// Collects runs of consecutive words and launches k_put_words for each full or
+// finished run.
+struct WordWriter {
+    uint8_t* base;
+    hipStream_t st;
+    PutWords a;
+    lt_err put(size_t offset, uint64_t word)
+    {
+        if (a.n > 0 && (a.n == kPutWords || offset != a.offset + 8 * size_t(a.n)))
+            if (lt_err e = flush())
+                return e;
+        if (a.n == 0)
+            a.offset = offset;
+        a.w[a.n++] = word;
+        return LT_OK;
+    }
+    lt_err flush()
+    {
+        if (a.n == 0)
+            return LT_OK;
+        k_put_words<<<1, 256, 0, st>>>(base, a);
+        LT_HIP(hipGetLastError());
+        a.n = 0;
+        return LT_OK;
+    }
+};
+
 }  // namespace
 
 // =================================================================== C ABI
@@ -2108,6 +2191,78 @@ lt_err lt_clip_coef(const double* sq_total, float max_norm, float* total_norm, f
         return fail(LT_ERR_ALIGNMENT, "scalar arguments must be naturally aligned");
     k_clip_coef<<<1, 64, 0, static_cast<hipStream_t>(stream)>>>(sq_total, max_norm, total_norm,
                                                                  coef, status);
+    LT_HIP(hipGetLastError());
+    return LT_OK;
+}
+
+lt_err lt_grad_sqnorm_noalloc(const void* const* grads, const int64_t* numels, int n_tensors,
+                              int grad_dtype, double* sq_per_tensor, double* sq_total,
+                              int32_t* status, void* stream)
+{
+    g_last_error.clear();
+    if (!valid_list(numels, n_tensors) || !lists_given(n_tensors, {grads}))
+        return fail(LT_ERR_INVALID_ARG, "grads/numels must hold n_tensors >= 0 entries with numel >= 0");
+    if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
+        return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
+    if (!sq_total || !status)
+        return fail(LT_ERR_INVALID_ARG, "sq_total and status must not be NULL");
+    if (!aligned(sq_total, 8) || !aligned(status, 4) || (sq_per_tensor && !aligned(sq_per_tensor, 8)))
+        return fail(LT_ERR_ALIGNMENT, "scalar outputs must be naturally aligned");
+    for (int k = 0; k < n_tensors; ++k) {
+        if (numels[k] == 0)
+            continue;
+        if (!grads[k])
+            return fail(LT_ERR_INVALID_ARG, "grads[" + std::to_string(k) + "] is NULL");
+        if (!aligned(grads[k], 16))
+            return fail(LT_ERR_ALIGNMENT, "grads[" + std::to_string(k) + "] is not 16-byte aligned");
+    }
+    const int K = n_tensors;
+    const int64_t C = sq_chunks_of(numels, K);
+    const SqLayout lay = sq_layout(K, C);
+    if (lay.total > kScratchBytes)
+        return fail(LT_ERR_INVALID_ARG,
+                    "the list needs " + std::to_string(lay.total) + " bytes of scratch; the "
+                    "no-allocation sum of squares holds " + std::to_string(kScratchBytes) +
+                    " (about 2 million 8192-element chunks); use lt_grad_sqnorm");
+    uint8_t* ws;
+    if (lt_err e = scratch_address(&ws))
+        return e;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+
+    // The descriptors, as lt_grad_sqnorm lays them out, written by kernels.
+    const WsGuard guard{reinterpret_cast<const uint64_t*>(ws), fresh_tag()};
+    WordWriter out{ws, st, {}};
+    if (lt_err e = out.put(0, guard.tag))
+        return e;
+    int64_t prefix = 0;
+    for (int k = 0; k <= K; ++k) {
+        if (lt_err e = out.put(lay.prefix + 8 * size_t(k), uint64_t(prefix)))
+            return e;
+        if (k < K)
+            prefix += (numels[k] + kChunk - 1) / kChunk;
+    }
+    for (int k = 0; k < K; ++k)
+        if (lt_err e = out.put(lay.ptrs + 8 * size_t(k), reinterpret_cast<uint64_t>(grads[k])))
+            return e;
+    for (int k = 0; k < K; ++k)
+        if (lt_err e = out.put(lay.numels + 8 * size_t(k), uint64_t(numels[k])))
+            return e;
+    if (lt_err e = out.flush())
+        return e;
+
+    const auto* d_prefix = reinterpret_cast<const int64_t*>(ws + lay.prefix);
+    auto* d_partials = reinterpret_cast<double*>(ws + lay.partials);
+    auto* d_sk = reinterpret_cast<double*>(ws + lay.sk);
+    if (lt_err e = launch_sq_chunks(guard, grad_dtype, d_prefix,
+                                    reinterpret_cast<const uint64_t*>(ws + lay.ptrs),
+                                    reinterpret_cast<const int64_t*>(ws + lay.numels), K, C,
+                                    d_partials, st))
+        return e;
+    if (K > 0) {
+        k_sqnorm_finish<<<K, kThreads, 0, st>>>(guard, d_prefix, d_partials, d_sk);
+        LT_HIP(hipGetLastError());
+    }
+    k_sqnorm_total<<<1, 256, 0, st>>>(guard, d_sk, K, sq_per_tensor, sq_total, status);
     LT_HIP(hipGetLastError());
     return LT_OK;
 }

@@ -61,6 +61,7 @@ def lib() -> ctypes.CDLL:
     L.lt_grad_sqnorm_workspace_bytes.restype = ctypes.c_size_t
     L.lt_grad_sqnorm.argtypes = [vpp, i64p, ctypes.c_int, ctypes.c_int, vp, ctypes.c_size_t,
                                  vp, vp, vp, vp]
+    L.lt_grad_sqnorm_noalloc.argtypes = [vpp, i64p, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp]
     L.lt_clip_coef.argtypes = [vp, ctypes.c_float, vp, vp, vp, vp]
     L.lt_grad_chunk_count.argtypes = [i64p, ctypes.c_int]
     L.lt_grad_chunk_count.restype = ctypes.c_int64
@@ -103,7 +104,8 @@ def lib() -> ctypes.CDLL:
     for name in ("lt_grad_sqnorm", "lt_clip_coef", "lt_hybrid8bit_adamw_step", "lt_read_status",
                  "lt_grad_sqnorm_partials", "lt_grad_sqnorm_finish",
                  "lt_set_max_workgroups", "lt_streamed_hybrid8bit_adamw_step",
-                 "lt_adamw_fp32_step", "lt_select_8bit_slice", "lt_workspace_release"):
+                 "lt_adamw_fp32_step", "lt_select_8bit_slice", "lt_workspace_release",
+                 "lt_grad_sqnorm_noalloc"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -268,6 +270,24 @@ def lt_grad_sqnorm(grads: Sequence[torch.Tensor], sq_total: torch.Tensor, status
         _check(lib().lt_grad_sqnorm(
             _ptr_array(grads), _numel_array(grads), len(grads), gdt, ws.data_ptr(),
             ws.numel() * ws.element_size(), _scalar(sq_per_tensor, device, torch.float64, "sq_per_tensor"),
+            _scalar(sq_total, device, torch.float64, "sq_total"),
+            _scalar(status, device, torch.int32, "status"), _stream_handle(stream, device)))
+
+
+def lt_grad_sqnorm_noalloc(grads: Sequence[torch.Tensor], sq_total: torch.Tensor,
+                           status: torch.Tensor, sq_per_tensor: Optional[torch.Tensor] = None,
+                           stream=None) -> None:
+    """lt_grad_sqnorm without a workspace: the library's own device scratch holds the
+    descriptors and partial sums, and the call allocates nothing (see the header)."""
+    device = sq_total.device
+    _check_tensors(grads, device, what="grads")
+    gdt = _grad_dtype(grads)
+    if sq_per_tensor is not None and sq_per_tensor.numel() < len(grads):
+        raise ValueError("sq_per_tensor needs one float64 per tensor")
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_grad_sqnorm_noalloc(
+            _ptr_array(grads), _numel_array(grads), len(grads), gdt,
+            _scalar(sq_per_tensor, device, torch.float64, "sq_per_tensor"),
             _scalar(sq_total, device, torch.float64, "sq_total"),
             _scalar(status, device, torch.int32, "status"), _stream_handle(stream, device)))
 
