@@ -337,6 +337,17 @@ size_t lt_streamed_workspace_bytes(const int64_t* numels, int n_tensors, const i
  *                       inputs when norm_ready is set).  A NONFINITE status
  *                       skips the update: weights, codes and scales are copied
  *                       back unchanged.
+ *   layer_events        NULL, or a host array of 8 * n_layers hipEvent_t created by
+ *                       the caller (entries may be NULL), which the call records
+ *                       around layer i's work: [8i] and [8i+1] on h2d_stream before
+ *                       and after its pass-1 gradient copies (not recorded with
+ *                       norm_ready), [8i+2] and [8i+3] before and after its pass-2
+ *                       copies in, [8i+6] and [8i+7] on compute_stream before and
+ *                       after its step kernels, [8i+4] and [8i+5] on d2h_stream
+ *                       before and after its copies out.  Each "before" is recorded
+ *                       once the stream may start that work, so timing events give
+ *                       each phase's own duration; an executor can also wait on
+ *                       them.
  *   compute_stream, h2d_stream, d2h_stream: the copies in, the kernels and the
  *                       copies out are ordered by events; the call's work ends on
  *                       compute_stream (synchronize it before reading results).
@@ -363,7 +374,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                          int ring_slots, void* workspace,
                                          size_t workspace_bytes, double* sq_total,
                                          float* total_norm, float* coef, int32_t* status,
-                                         void* compute_stream, void* h2d_stream, void* d2h_stream);
+                                         void* const* layer_events, void* compute_stream,
+                                         void* h2d_stream, void* d2h_stream);
 
 /* Bytes of device workspace lt_adamw_fp32_step needs for n_tensors tensors. */
 size_t lt_adamw_fp32_workspace_bytes(int n_tensors);

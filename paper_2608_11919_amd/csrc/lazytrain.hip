@@ -2504,7 +2504,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
                                          int ring_slots, void* workspace,
                                          size_t workspace_bytes, double* sq_total,
                                          float* total_norm, float* coef, int32_t* status,
-                                         void* compute_stream, void* h2d_stream, void* d2h_stream)
+                                         void* const* layer_events, void* compute_stream,
+                                         void* h2d_stream, void* d2h_stream)
 {
     g_last_error.clear();
     const int K = n_tensors, L = n_layers, S = ring_slots, B = block_size;
@@ -2617,6 +2618,13 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
     auto* d_sk = reinterpret_cast<double*>(ws + lay.sk);
     const auto H2D = hipMemcpyHostToDevice, D2H = hipMemcpyDeviceToHost;
 
+    // The caller's events, when given: mark(i, m, stream) records event m of layer i.
+    auto mark = [&](int i, int m, hipStream_t s) -> lt_err {
+        if (layer_events && layer_events[8 * size_t(i) + m])
+            LT_HIP(hipEventRecord(static_cast<hipEvent_t>(layer_events[8 * size_t(i) + m]), s));
+        return LT_OK;
+    };
+
     // Pass 1: gradients in, chunk sums at their global indices.  Skipped when the
     // caller summed the gradients as they arrived (sq_total and status are given).
     // Resident gradients each have their own region, so their copies wait for no
@@ -2626,10 +2634,14 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         if (used[sl] && !resident)
             LT_HIP(hipStreamWaitEvent(hs, ev.freed[sl], 0));
         uint8_t* base = slot_base(i);
+        if (lt_err e = mark(i, 0, hs))
+            return e;
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j)
             if (numels[k] > 0)
                 LT_HIP(hipMemcpyAsync(grad_at(k, base, places[i][j]), grads[k],
                                       size_t(numels[k]) * gbytes, H2D, hs));
+        if (lt_err e = mark(i, 1, hs))
+            return e;
         LT_HIP(hipEventRecord(ev.in[sl], hs));
         LT_HIP(hipStreamWaitEvent(cs, ev.in[sl], 0));
         const int Ki = layer_first[i + 1] - layer_first[i];
@@ -2660,6 +2672,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         if (used[sl])
             LT_HIP(hipStreamWaitEvent(hs, ev.freed[sl], 0));
         uint8_t* base = slot_base(i);
+        if (lt_err e = mark(i, 2, hs))
+            return e;
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
             const SlotTensor& t = places[i][j];
             const size_t n = size_t(numels[k]), nb = size_t((numels[k] + B - 1) / B);
@@ -2673,8 +2687,12 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
             LT_HIP(hipMemcpyAsync(base + t.ma, m_absmax[k], nb * 4, H2D, hs));
             LT_HIP(hipMemcpyAsync(base + t.va, v_absmax[k], nb * 4, H2D, hs));
         }
+        if (lt_err e = mark(i, 3, hs))
+            return e;
         LT_HIP(hipEventRecord(ev.in[sl], hs));
         LT_HIP(hipStreamWaitEvent(cs, ev.in[sl], 0));
+        if (lt_err e = mark(i, 6, cs))
+            return e;
         const int Ki = layer_first[i + 1] - layer_first[i];
         const auto* up = reinterpret_cast<const int64_t*>(ws + lay.st_prefix[i]);
         const auto* dp = reinterpret_cast<const StepTensor*>(ws + lay.st_desc[i]);
@@ -2691,8 +2709,12 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
         if (wb)
             if (lt_err e2 = launch_bf16_on_skip(guard, up, dp, Ki, units, unit, status, cs))
                 return e2;
+        if (lt_err e = mark(i, 7, cs))
+            return e;
         LT_HIP(hipEventRecord(ev.computed[sl], cs));
         LT_HIP(hipStreamWaitEvent(ds, ev.computed[sl], 0));
+        if (lt_err e = mark(i, 4, ds))
+            return e;
         for (int k = layer_first[i], j = 0; k < layer_first[i + 1]; ++k, ++j) {
             const SlotTensor& t = places[i][j];
             const size_t n = size_t(numels[k]), nb = size_t((numels[k] + B - 1) / B);
@@ -2706,6 +2728,8 @@ lt_err lt_streamed_hybrid8bit_adamw_step(float* const* params, const void* const
             if (bf16_copy && params_bf16[k])
                 LT_HIP(hipMemcpyAsync(params_bf16[k], base + t.wb, n * 2, D2H, ds));
         }
+        if (lt_err e = mark(i, 5, ds))
+            return e;
         LT_HIP(hipEventRecord(ev.freed[sl], ds));
         used[sl] = true;
     }

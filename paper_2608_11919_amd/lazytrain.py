@@ -88,7 +88,7 @@ def lib() -> ctypes.CDLL:
         vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, vpp, i64p, ctypes.c_int, ip, ctypes.c_int,
         ctypes.c_int, ctypes.c_int] + [ctypes.c_double] * 5 + [ctypes.c_int64, ctypes.c_float, ctypes.c_int,
                                                  ctypes.c_int, ctypes.c_int, vp, ctypes.c_size_t,
-                                                 vp, vp, vp, vp, vp, vp, vp]
+                                                 vp, vp, vp, vp, vpp, vp, vp, vp]
     L.lt_adamw_fp32_workspace_bytes.argtypes = [ctypes.c_int]
     L.lt_adamw_fp32_workspace_bytes.restype = ctypes.c_size_t
     L.lt_adamw_fp32_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, i64p, ctypes.c_int] + [
@@ -446,14 +446,16 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
                                       d2h_stream=None, params_bf16=None,
                                       norm_ready: bool = False,
                                       code_map: int = LT_MAP_LINEAR,
-                                      keep_grads: bool = False) -> None:
+                                      keep_grads: bool = False, layer_events=None) -> None:
     """Step a11: host-resident tensors (CPU, ideally pinned) streamed layer by layer
     through HBM; scalar outputs are device tensors (see include/lazytrain.h).
     params_bf16 (optional, host bf16 tensors or None) receives the bf16 weight copy.
     With norm_ready, sq_total and status already hold S and its status (summed as the
     gradients arrived) and the first streamed pass is skipped.  With keep_grads every
     gradient stays in HBM from the first pass to the second (2 or 4 B/param of
-    workspace), so it crosses the link once."""
+    workspace), so it crosses the link once.  layer_events (optional): 8 torch.cuda.Event
+    (or None) per layer, recorded around each layer's copies and kernels (see the
+    header for which is which)."""
     k = len(params)
     if k == 0 or not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) ==
                       len(v_absmax) == k):
@@ -488,6 +490,15 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
     if compute_stream is not None and hasattr(compute_stream, "cuda_stream"):
         workspace.record_stream(compute_stream)  # in use on that stream until the step is done
     first = (ctypes.c_int * len(layer_first))(*layer_first)
+    events = None
+    if layer_events is not None:
+        if len(layer_events) != 8 * (len(layer_first) - 1):
+            raise ValueError("layer_events needs 8 entries per layer")
+        for e in layer_events:
+            if e is not None and not e.cuda_event:  # torch creates an event at its first record
+                e.record(torch.cuda.current_stream(device))
+        events = (ctypes.c_void_p * len(layer_events))(
+            *[0 if e is None else e.cuda_event for e in layer_events])
     hs = _stream_handle(h2d_stream, device) if h2d_stream is not None else cs
     ds = _stream_handle(d2h_stream, device) if d2h_stream is not None else cs
     with torch.cuda.device(device):  # the library works on the current device
@@ -503,7 +514,7 @@ def lt_streamed_hybrid8bit_adamw_step(params, grads, m_codes, m_absmax, v_codes,
             _scalar(sq_total, device, torch.float64, "sq_total"),
             _scalar(total_norm, device, torch.float32, "total_norm"),
             _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
-            cs, hs, ds))
+            events, cs, hs, ds))
 
 
 def lt_adamw_fp32_workspace_bytes(n_tensors: int) -> int:

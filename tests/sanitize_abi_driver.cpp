@@ -122,7 +122,7 @@ int main() {
             const lt_err e = lt_streamed_hybrid8bit_adamw_step(
                 pw, gw, LT_DTYPE_BF16, mqw, maw, vqw, vaw, nullptr, sn, 2, lf, 1, 2048,
                 LT_MAP_LINEAR, 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, 1.0f, 0, keep, 3, mem,
-                keep ? kept - 256 : kept, &dS, &dn, &dc, &dst, nullptr, nullptr, nullptr);
+                keep ? kept - 256 : kept, &dS, &dn, &dc, &dst, nullptr, nullptr, nullptr, nullptr);
             if (e != LT_ERR_WORKSPACE) ++bad;
         }
     }
