@@ -101,6 +101,57 @@ typedef enum lt_code_map {
     LT_MAP_DYNAMIC = 1 /* this library's decade-tree codes: sign-magnitude m, unsigned v, 1e-7 .. 1 */
 } lt_code_map;
 
+/* Device-resident step count, for callers that enqueue steps ahead of the GPU
+ * without reading each step's status first (App. C: a step with a non-finite
+ * gradient is skipped and does not count; training stops after three skips in a
+ * row).  A step state is caller-owned device memory of lt_step_state_bytes: this
+ * header, then table_len entries; entry i holds the parts of the bias corrections
+ * of step t = i + 1 that do not depend on the learning rate.  A step entry point
+ * given a step state applies step t = applied + 1 with
+ * step_size = fp32(lr / one_minus_beta1_t) (fp64 division on the device) and that
+ * entry's rbc2: bitwise the scalars the host computes for that t.
+ * lt_step_state_advance, enqueued after a step's kernels, counts the step. */
+typedef struct lt_step_state {
+    int64_t applied;      /* steps applied so far */
+    int64_t table_len;    /* entries after this header */
+    int32_t skips;        /* consecutive steps skipped */
+    int32_t max_skips;    /* stop after this many skips in a row; 0: never */
+    int32_t stopped;      /* 1: max_skips skips in a row; 2: the table ran out.  Every
+                             later step then skips (writes nothing). */
+    int32_t reserved[9];
+} lt_step_state;          /* 64 bytes */
+
+typedef struct lt_step_table_entry {
+    double one_minus_beta1_t; /* 1 - beta1^t in fp64 (the C library's pow) */
+    float rbc2;               /* fp32(1 / sqrt(1 - beta2^t)), computed in fp64 */
+    float reserved;
+} lt_step_table_entry;        /* 16 bytes */
+
+/* Bytes of a step state with table_len entries; 0 if table_len < 1. */
+size_t lt_step_state_bytes(int64_t table_len);
+
+/* Host only: table entries of t = t_first .. t_first + count - 1 into out[count]. */
+lt_err lt_step_table(double beta1, double beta2, int64_t t_first, int64_t count,
+                     lt_step_table_entry* out);
+
+/*
+ * Writes a step state into device memory `state` (bytes >= lt_step_state_bytes(
+ * table_len), 16-byte aligned), on `stream`: the table of t = 1 .. table_len for
+ * beta1, beta2 (0 <= beta < 1), and the header with `applied` (>= 0), `skips`,
+ * `max_skips` (>= 0) and stopped = 0.  from_state: NULL, or another device step
+ * state whose applied, skips, max_skips and stopped the new one takes instead, on
+ * the device in stream order (to grow a table without reading the count back).
+ */
+lt_err lt_step_state_init(void* state, size_t bytes, int64_t table_len, double beta1,
+                          double beta2, int64_t applied, int32_t skips, int32_t max_skips,
+                          const void* from_state, void* stream);
+
+/* Counts one step on the device, after its step kernels on `stream`: with
+ * *status == LT_STATUS_OK, applied += 1 and skips = 0 (or stopped = 2 if the table
+ * did not reach the step); otherwise skips += 1, and stopped = 1 once skips reaches
+ * a nonzero max_skips.  A stopped state is left as it is. */
+lt_err lt_step_state_advance(void* state, const int32_t* status, void* stream);
+
 /* Bytes of device workspace lt_grad_sqnorm needs for this list (descriptors,
  * one fp64 partial per 8192-element chunk, one fp64 per tensor); never 0 for a
  * valid list.  Returns 0 if n_tensors < 0, numels is NULL for n_tensors > 0 or
@@ -258,7 +309,12 @@ size_t lt_step_workspace_bytes(int n_tensors);
  *            by fp32 distance, ties to the smaller code, NaN to magnitude 0; the
  *            same absmax and zero-block rule.  A second moment down to 5e-8 of its
  *            block's absmax keeps a nonzero code (2e-3 with the linear map).
- *   step     1-based index t of the step being applied (>= 1).
+ *   step     1-based index t of the step being applied (>= 1), unless step_state
+ *            is given.
+ *   step_state  NULL, or a device step state (lt_step_state): the step index and
+ *            its bias corrections come from it on the device (t = applied + 1;
+ *            `step` is then ignored), and a stopped state makes the step write
+ *            nothing.  The caller enqueues lt_step_state_advance after the step.
  *   lr, weight_decay >= 0; 0 <= beta1, beta2 < 1; eps > 0, also after its
  *            rounding to fp32 (with eps = 0 a zero gradient on a zero second
  *            moment divides 0 by 0); all finite.  Otherwise LT_ERR_INVALID_ARG.
@@ -284,7 +340,8 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
                                 int n_tensors, int block_size, int code_map, double lr,
                                 double beta1, double beta2, double eps, double weight_decay,
                                 int64_t step, const float* coef, const int32_t* status,
-                                void* workspace, size_t workspace_bytes, void* stream);
+                                const void* step_state, void* workspace, size_t workspace_bytes,
+                                void* stream);
 
 /* Bytes of device workspace lt_streamed_hybrid8bit_adamw_step needs: the
  * descriptors of every layer, one fp64 partial per 8192-element chunk of the
@@ -387,8 +444,8 @@ size_t lt_adamw_fp32_workspace_bytes(int n_tensors);
  * variant table).  exp_avg[k], exp_avg_sq[k] are device float[numels[k]], read
  * and written.  Per element, the same fp32 operations as
  * lt_hybrid8bit_adamw_step with m0, v0 taken from and m1, v1 stored to these
- * arrays.  coef, status and params_bf16 (NULL or a list of device bf16 copies,
- * entries may be NULL) as there.  Pointers 16-byte aligned; workspace
+ * arrays.  coef, status, step_state and params_bf16 (NULL or a list of device bf16
+ * copies, entries may be NULL) as there.  Pointers 16-byte aligned; workspace
  * 256-byte aligned.  As there, written arrays may not overlap any other array of
  * the call (LT_ERR_INVALID_ARG).
  */
@@ -396,8 +453,8 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
                           float* const* exp_avg, float* const* exp_avg_sq,
                           uint16_t* const* params_bf16, const int64_t* numels, int n_tensors, double lr, double beta1, double beta2, double eps,
                           double weight_decay, int64_t step, const float* coef,
-                          const int32_t* status, void* workspace, size_t workspace_bytes,
-                          void* stream);
+                          const int32_t* status, const void* step_state, void* workspace,
+                          size_t workspace_bytes, void* stream);
 
 /*
  * Chooses the tensors that take 8-bit states when only a fraction of the

@@ -14,5 +14,6 @@ from .lazytrain import (  # noqa: F401
     lt_streamed_hybrid8bit_adamw_step, lt_streamed_workspace_bytes, lt_adamw_fp32_step,
     lt_adamw_fp32_workspace_bytes, lt_select_8bit_slice, lt_grad_chunk_count,
     lt_grad_sqnorm_partials, lt_grad_sqnorm_finish, lt_workspace_release, lt_grad_sqnorm_noalloc,
+    lt_step_state_bytes, lt_step_table, lt_step_state_init, lt_step_state_advance,
     GradNormAccumulator,
     StreamedHybrid8bitAdamW)

@@ -77,6 +77,8 @@ static_assert(sizeof(StepTensor) == 64, "descriptor is one 64-byte line");
 
 struct StepScalars {
     float beta1, beta2, eps, c1, c2, decay, step_size, rbc2;
+    const uint8_t* state;  // the caller's step state, or null: step_size and rbc2 as given
+    double lr;             // for step_size from the step state's table
 };
 
 constexpr size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -208,6 +210,48 @@ lt_err stream_capturing(hipStream_t st, bool* capturing)
     return LT_OK;
 }
 
+// Copies n bytes from host memory to device address dst on stream st through a
+// pinned staging slot (ds.mu held).  A slot is reused once its copy has run,
+// checked without waiting; when the next one is still in flight the ring grows by
+// a slot, so the call never waits for the device.
+lt_err stage_copy_locked(DeviceState& ds, const void* src, size_t n, void* dst, hipStream_t st)
+{
+    if (ds.slots.empty())
+        ds.slots.resize(8);
+    if (ds.next >= ds.slots.size())
+        ds.next = 0;
+    {
+        StagingSlot& s = ds.slots[ds.next];
+        if (s.pending) {
+            const hipError_t q = hipEventQuery(s.done);
+            if (q == hipSuccess)
+                s.pending = false;
+            else if (q == hipErrorNotReady)
+                ds.slots.insert(ds.slots.begin() + ptrdiff_t(ds.next), StagingSlot{});  // grow
+            else
+                return fail(LT_ERR_HIP, std::string("hipEventQuery: ") + hipGetErrorString(q));
+        }
+    }
+    StagingSlot& s = ds.slots[ds.next];
+    ds.next += 1;
+    if (!s.done)
+        LT_HIP(hipEventCreateWithFlags(&s.done, hipEventDisableTiming));
+    if (s.cap < n) {
+        if (s.host)
+            ds.retired.push_back(s.host);
+        s.host = nullptr;
+        s.cap = 0;
+        const size_t cap = round_up(std::max(n, size_t(4096)), 4096);
+        LT_HIP(hipHostMalloc(&s.host, cap, hipHostMallocDefault));
+        s.cap = cap;
+    }
+    std::memcpy(s.host, src, n);
+    LT_HIP(hipMemcpyAsync(dst, s.host, n, hipMemcpyHostToDevice, st));
+    LT_HIP(hipEventRecord(s.done, st));
+    s.pending = true;
+    return LT_OK;
+}
+
 // Makes the workspace `ws` hold `image` (the bytes of its head; the first
 // kTagBytes are the tag slot, filled here) before the work enqueued next on `st`
 // reads it, and returns the guard that work's kernels check.
@@ -241,40 +285,8 @@ lt_err put_descriptors(std::vector<uint8_t>& image, void* ws, hipStream_t st, Ws
                     "capturing");
     const uint64_t tag = fresh_tag();
     std::memcpy(image.data(), &tag, sizeof(tag));
-
-    if (ds.slots.empty())
-        ds.slots.resize(8);
-    if (ds.next >= ds.slots.size())
-        ds.next = 0;
-    {
-        StagingSlot& s = ds.slots[ds.next];
-        if (s.pending) {
-            const hipError_t q = hipEventQuery(s.done);
-            if (q == hipSuccess)
-                s.pending = false;
-            else if (q == hipErrorNotReady)
-                ds.slots.insert(ds.slots.begin() + ptrdiff_t(ds.next), StagingSlot{});  // grow
-            else
-                return fail(LT_ERR_HIP, std::string("hipEventQuery: ") + hipGetErrorString(q));
-        }
-    }
-    StagingSlot& s = ds.slots[ds.next];
-    ds.next += 1;
-    if (!s.done)
-        LT_HIP(hipEventCreateWithFlags(&s.done, hipEventDisableTiming));
-    if (s.cap < n) {
-        if (s.host)
-            ds.retired.push_back(s.host);
-        s.host = nullptr;
-        s.cap = 0;
-        const size_t cap = round_up(std::max(n, size_t(4096)), 4096);
-        LT_HIP(hipHostMalloc(&s.host, cap, hipHostMallocDefault));
-        s.cap = cap;
-    }
-    std::memcpy(s.host, image.data(), n);
-    LT_HIP(hipMemcpyAsync(ws, s.host, n, hipMemcpyHostToDevice, st));
-    LT_HIP(hipEventRecord(s.done, st));
-    s.pending = true;
+    if (lt_err e = stage_copy_locked(ds, image.data(), n, ws, st))
+        return e;
 
     if (!c.copied) {
         if (!ds.spare_events.empty()) {
@@ -484,6 +496,25 @@ __device__ inline int find_tensor(const int64_t* __restrict__ prefix, int n_tens
 
 // True when the workspace holds the descriptors this launch was given the tag of.
 __device__ inline bool guard_ok(const WsGuard& g) { return *g.at == g.tag; }
+
+// With a caller's step state: the step applied is t = applied + 1, its step size
+// fp32(lr / (1 - beta1^t)) by an fp64 division of the table's fp64 1 - beta1^t
+// (the host's expression and rounding), its rbc2 the table's.  False when the
+// state lets no step apply (stopped, or its table does not reach t).
+__device__ inline bool resolve_step(StepScalars& s)
+{
+    if (!s.state)
+        return true;
+    const auto* h = reinterpret_cast<const lt_step_state*>(s.state);
+    const int64_t a = h->applied;
+    if (h->stopped != 0 || a < 0 || a >= h->table_len)
+        return false;
+    const lt_step_table_entry e =
+        reinterpret_cast<const lt_step_table_entry*>(s.state + sizeof(lt_step_state))[a];
+    s.step_size = float(s.lr / e.one_minus_beta1_t);
+    s.rbc2 = e.rbc2;
+    return true;
+}
 
 // ------------------------------------------------------- a1: chunk sums
 
@@ -1113,6 +1144,8 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_step(WsGuard guard,
         return;  // the workspace does not hold this launch's descriptors
     if (status_ptr && *status_ptr != LT_STATUS_OK)
         return;  // skipped step: nothing is written
+    if (!resolve_step(s))
+        return;  // the step state lets no step apply
     const float coef = coef_ptr ? *coef_ptr : 1.0f;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -1403,6 +1436,8 @@ __global__ __launch_bounds__(kThreads) void k_adamw8_generic(WsGuard guard,
         return;  // the workspace does not hold this launch's descriptors
     if (status_ptr && *status_ptr != LT_STATUS_OK)
         return;  // skipped step: nothing is written
+    if (!resolve_step(s))
+        return;  // the step state lets no step apply
     const float coef = coef_ptr ? *coef_ptr : 1.0f;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     if constexpr (MAP == kMapDynamic) {
@@ -1591,6 +1626,8 @@ __global__ __launch_bounds__(kThreads) void k_adamw32_step(WsGuard guard,
         return;  // the workspace does not hold this launch's descriptors
     if (status_ptr && *status_ptr != LT_STATUS_OK)
         return;  // skipped step: nothing is written
+    if (!resolve_step(s))
+        return;  // the step state lets no step apply
     const float coef = coef_ptr ? *coef_ptr : 1.0f;
     const int lane = threadIdx.x & 63;
     // Units go to the waves in turn, as in the 8-bit step.
@@ -1888,7 +1925,54 @@ StepScalars make_scalars(double lr, double beta1, double beta2, double eps, doub
     s.decay = float(1.0 - lr * weight_decay);
     s.step_size = float(lr / (1.0 - std::pow(beta1, t)));
     s.rbc2 = float(1.0 / std::sqrt(1.0 - std::pow(beta2, t)));
+    s.state = nullptr;
+    s.lr = lr;
     return s;
+}
+
+// The table entry of step t, by the same expressions as make_scalars.
+lt_step_table_entry step_table_entry(double beta1, double beta2, int64_t step)
+{
+    const double t = double(step);
+    lt_step_table_entry e;
+    e.one_minus_beta1_t = 1.0 - std::pow(beta1, t);
+    e.rbc2 = float(1.0 / std::sqrt(1.0 - std::pow(beta2, t)));
+    e.reserved = 0.0f;
+    return e;
+}
+
+static_assert(sizeof(lt_step_state) == 64 && sizeof(lt_step_table_entry) == 16,
+              "step state layout");
+
+// Takes applied, skips, max_skips and stopped from another step state.
+__global__ void k_step_state_copy(lt_step_state* __restrict__ dst,
+                                  const lt_step_state* __restrict__ src)
+{
+    if (threadIdx.x != 0)
+        return;
+    dst->applied = src->applied;
+    dst->skips = src->skips;
+    dst->max_skips = src->max_skips;
+    dst->stopped = src->stopped;
+}
+
+__global__ void k_step_state_advance(lt_step_state* __restrict__ h,
+                                     const int32_t* __restrict__ status)
+{
+    if (threadIdx.x != 0 || h->stopped != 0)
+        return;
+    if (*status == LT_STATUS_OK) {
+        if (h->applied >= h->table_len) {
+            h->stopped = 2;  // the steps found no table entry and wrote nothing
+            return;
+        }
+        h->applied += 1;
+        h->skips = 0;
+    } else {
+        h->skips += 1;
+        if (h->max_skips > 0 && h->skips >= h->max_skips)
+            h->stopped = 1;
+    }
 }
 
 lt_err launch_sq_chunks(const WsGuard& guard, int gdt, const int64_t* prefix, const uint64_t* ptrs,
@@ -2386,7 +2470,8 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
                                 int n_tensors, int block_size, int code_map, double lr,
                                 double beta1, double beta2, double eps, double weight_decay,
                                 int64_t step, const float* coef, const int32_t* status,
-                                void* workspace, size_t workspace_bytes, void* stream)
+                                const void* step_state, void* workspace, size_t workspace_bytes,
+                                void* stream)
 {
     g_last_error.clear();
     if (!valid_list(numels, n_tensors) ||
@@ -2398,11 +2483,12 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
         return fail(LT_ERR_INVALID_ARG, "block_size must be a multiple of 64 in [64, 65536]");
     if (code_map != LT_MAP_LINEAR && code_map != LT_MAP_DYNAMIC)
         return fail(LT_ERR_INVALID_ARG, "code_map must be LT_MAP_LINEAR or LT_MAP_DYNAMIC");
-    if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step))
+    if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step_state ? 1 : step))
         return fail(LT_ERR_INVALID_ARG, "need finite lr, weight_decay >= 0, finite eps > 0 (also "
                                         "in fp32), 0 <= beta1, beta2 < 1 and step >= 1");
-    if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)))
-        return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned");
+    if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)) ||
+        (step_state && !aligned(step_state, 16)))
+        return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned, step_state 16-byte");
     const int K = n_tensors;
     for (int k = 0; k < K; ++k) {
         if (numels[k] == 0)
@@ -2456,7 +2542,8 @@ lt_err lt_hybrid8bit_adamw_step(float* const* params, const void* const* grads, 
     if (tiles == 0)
         return LT_OK;  // every tensor is empty
 
-    const StepScalars s = make_scalars(lr, beta1, beta2, eps, weight_decay, step);
+    StepScalars s = make_scalars(lr, beta1, beta2, eps, weight_decay, step_state ? 1 : step);
+    s.state = static_cast<const uint8_t*>(step_state);
 
     auto* ws = static_cast<uint8_t*>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -2750,8 +2837,8 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
                           float* const* exp_avg, float* const* exp_avg_sq,
                           uint16_t* const* params_bf16, const int64_t* numels, int n_tensors, double lr, double beta1, double beta2, double eps,
                           double weight_decay, int64_t step, const float* coef,
-                          const int32_t* status, void* workspace, size_t workspace_bytes,
-                          void* stream)
+                          const int32_t* status, const void* step_state, void* workspace,
+                          size_t workspace_bytes, void* stream)
 {
     g_last_error.clear();
     const int K = n_tensors;
@@ -2759,11 +2846,12 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
         return fail(LT_ERR_INVALID_ARG, "tensor lists must hold n_tensors >= 0 entries with numel >= 0");
     if (grad_dtype != LT_DTYPE_F32 && grad_dtype != LT_DTYPE_BF16)
         return fail(LT_ERR_INVALID_ARG, "grad_dtype must be LT_DTYPE_F32 or LT_DTYPE_BF16");
-    if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step))
+    if (!valid_hyper(lr, beta1, beta2, eps, weight_decay, step_state ? 1 : step))
         return fail(LT_ERR_INVALID_ARG, "need finite lr, weight_decay >= 0, finite eps > 0 (also "
                                         "in fp32), 0 <= beta1, beta2 < 1 and step >= 1");
-    if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)))
-        return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned");
+    if ((coef && !aligned(coef, 4)) || (status && !aligned(status, 4)) ||
+        (step_state && !aligned(step_state, 16)))
+        return fail(LT_ERR_ALIGNMENT, "coef and status must be 4-byte aligned, step_state 16-byte");
     for (int k = 0; k < K; ++k) {
         if (numels[k] == 0)
             continue;
@@ -2813,7 +2901,8 @@ lt_err lt_adamw_fp32_step(float* const* params, const void* const* grads, int gr
     const int64_t units = prefix[K];
     if (units == 0)
         return LT_OK;  // every tensor is empty
-    const StepScalars sc = make_scalars(lr, beta1, beta2, eps, weight_decay, step);
+    StepScalars sc = make_scalars(lr, beta1, beta2, eps, weight_decay, step_state ? 1 : step);
+    sc.state = static_cast<const uint8_t*>(step_state);
     auto* ws = static_cast<uint8_t*>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
     WsGuard guard;
@@ -2861,6 +2950,77 @@ lt_err lt_select_8bit_slice(const int64_t* numels, int n_tensors, double fractio
         }
     if (n_8bit_params)
         *n_8bit_params = chosen;
+    return LT_OK;
+}
+
+size_t lt_step_state_bytes(int64_t table_len)
+{
+    return table_len < 1 ? 0 : sizeof(lt_step_state) + sizeof(lt_step_table_entry) * size_t(table_len);
+}
+
+lt_err lt_step_table(double beta1, double beta2, int64_t t_first, int64_t count,
+                     lt_step_table_entry* out)
+{
+    g_last_error.clear();
+    if (!(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0) || t_first < 1 ||
+        count < 0 || (count > 0 && !out))
+        return fail(LT_ERR_INVALID_ARG, "need 0 <= beta1, beta2 < 1, t_first >= 1, count >= 0");
+    for (int64_t i = 0; i < count; ++i)
+        out[i] = step_table_entry(beta1, beta2, t_first + i);
+    return LT_OK;
+}
+
+lt_err lt_step_state_init(void* state, size_t bytes, int64_t table_len, double beta1,
+                          double beta2, int64_t applied, int32_t skips, int32_t max_skips,
+                          const void* from_state, void* stream)
+{
+    g_last_error.clear();
+    if (table_len < 1 || applied < 0 || skips < 0 || max_skips < 0 ||
+        !(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0))
+        return fail(LT_ERR_INVALID_ARG, "need table_len >= 1, applied, skips, max_skips >= 0 and "
+                                        "0 <= beta1, beta2 < 1");
+    if (!state || bytes < lt_step_state_bytes(table_len))
+        return fail(LT_ERR_WORKSPACE, "the step state must hold " +
+                                          std::to_string(lt_step_state_bytes(table_len)) + " bytes");
+    if (!aligned(state, 16) || (from_state && !aligned(from_state, 16)))
+        return fail(LT_ERR_ALIGNMENT, "step states must be 16-byte aligned");
+    std::vector<uint8_t> image(lt_step_state_bytes(table_len), 0);
+    auto* h = reinterpret_cast<lt_step_state*>(image.data());
+    h->applied = applied;
+    h->table_len = table_len;
+    h->skips = skips;
+    h->max_skips = max_skips;
+    h->stopped = 0;
+    auto* table = reinterpret_cast<lt_step_table_entry*>(image.data() + sizeof(lt_step_state));
+    for (int64_t i = 0; i < table_len; ++i)
+        table[i] = step_table_entry(beta1, beta2, i + 1);
+    int dev;
+    if (lt_err e = current_device(&dev))
+        return e;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    {
+        std::lock_guard<std::mutex> lock(g_dev[dev].mu);
+        if (lt_err e = stage_copy_locked(g_dev[dev], image.data(), image.size(), state, st))
+            return e;
+    }
+    if (from_state) {
+        k_step_state_copy<<<1, 64, 0, st>>>(static_cast<lt_step_state*>(state),
+                                             static_cast<const lt_step_state*>(from_state));
+        LT_HIP(hipGetLastError());
+    }
+    return LT_OK;
+}
+
+lt_err lt_step_state_advance(void* state, const int32_t* status, void* stream)
+{
+    g_last_error.clear();
+    if (!state || !status)
+        return fail(LT_ERR_INVALID_ARG, "state and status must not be NULL");
+    if (!aligned(state, 16) || !aligned(status, 4))
+        return fail(LT_ERR_ALIGNMENT, "state must be 16-byte aligned, status 4-byte");
+    k_step_state_advance<<<1, 64, 0, static_cast<hipStream_t>(stream)>>>(
+        static_cast<lt_step_state*>(state), status);
+    LT_HIP(hipGetLastError());
     return LT_OK;
 }
 

@@ -78,7 +78,7 @@ def lib() -> ctypes.CDLL:
     L.lt_hybrid8bit_adamw_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, vpp, vpp,
                                            i64p, ctypes.c_int, ctypes.c_int, ctypes.c_int] + [
                                                ctypes.c_double] * 5 + [
-                                               ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp]
+                                               ctypes.c_int64, vp, vp, vp, vp, ctypes.c_size_t, vp]
     ip = ctypes.POINTER(ctypes.c_int)
     L.lt_streamed_workspace_bytes.argtypes = [i64p, ctypes.c_int, ip, ctypes.c_int, ctypes.c_int,
                                               ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -92,7 +92,15 @@ def lib() -> ctypes.CDLL:
     L.lt_adamw_fp32_workspace_bytes.argtypes = [ctypes.c_int]
     L.lt_adamw_fp32_workspace_bytes.restype = ctypes.c_size_t
     L.lt_adamw_fp32_step.argtypes = [vpp, vpp, ctypes.c_int, vpp, vpp, vpp, i64p, ctypes.c_int] + [
-        ctypes.c_double] * 5 + [ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp]
+        ctypes.c_double] * 5 + [ctypes.c_int64, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.lt_step_state_bytes.argtypes = [ctypes.c_int64]
+    L.lt_step_state_bytes.restype = ctypes.c_size_t
+    L.lt_step_table.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_int64, ctypes.c_int64,
+                                vp]
+    L.lt_step_state_init.argtypes = [vp, ctypes.c_size_t, ctypes.c_int64, ctypes.c_double,
+                                     ctypes.c_double, ctypes.c_int64, ctypes.c_int32,
+                                     ctypes.c_int32, vp, vp]
+    L.lt_step_state_advance.argtypes = [vp, vp, vp]
     L.lt_select_8bit_slice.argtypes = [i64p, ctypes.c_int, ctypes.c_double,
                                        ctypes.POINTER(ctypes.c_uint8),
                                        ctypes.POINTER(ctypes.c_int64)]
@@ -105,7 +113,8 @@ def lib() -> ctypes.CDLL:
                  "lt_grad_sqnorm_partials", "lt_grad_sqnorm_finish",
                  "lt_set_max_workgroups", "lt_streamed_hybrid8bit_adamw_step",
                  "lt_adamw_fp32_step", "lt_select_8bit_slice", "lt_workspace_release",
-                 "lt_grad_sqnorm_noalloc"):
+                 "lt_grad_sqnorm_noalloc", "lt_step_table", "lt_step_state_init",
+                 "lt_step_state_advance"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -387,10 +396,13 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
                              coef: Optional[torch.Tensor] = None,
                              status: Optional[torch.Tensor] = None,
                              workspace: Optional[torch.Tensor] = None, stream=None,
-                             params_bf16=None, code_map: int = LT_MAP_LINEAR) -> None:
+                             params_bf16=None, code_map: int = LT_MAP_LINEAR,
+                             step_state: Optional[torch.Tensor] = None) -> None:
     """Steps a4-a10 in place on params, codes and absmax (see include/lazytrain.h);
     params_bf16 (optional, one bf16 tensor or None per parameter) receives the bf16
-    copy of the updated weights; code_map selects the linear or dynamic codes."""
+    copy of the updated weights; code_map selects the linear or dynamic codes;
+    step_state (optional, a device uint8 tensor from lt_step_state_init) supplies the
+    step index on the device instead of `step`."""
     k = len(params)
     if not (len(grads) == len(m_codes) == len(m_absmax) == len(v_codes) == len(v_absmax) == k):
         raise ValueError("tensor lists must be of equal length")
@@ -421,7 +433,8 @@ def lt_hybrid8bit_adamw_step(params: Sequence[torch.Tensor], grads: Sequence[tor
             int(code_map),
             float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step),
             _scalar(coef, device, torch.float32, "coef"), _scalar(status, device, torch.int32, "status"),
-            ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
+            _state_ptr(step_state, device), ws.data_ptr(), ws.numel() * ws.element_size(),
+            _stream_handle(stream, device)))
 
 
 def lt_streamed_workspace_bytes(numels: Sequence[int], layer_first: Sequence[int],
@@ -527,7 +540,7 @@ def lt_adamw_fp32_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Ten
                        step: int, coef: Optional[torch.Tensor] = None,
                        status: Optional[torch.Tensor] = None,
                        workspace: Optional[torch.Tensor] = None, stream=None,
-                       params_bf16=None) -> None:
+                       params_bf16=None, step_state: Optional[torch.Tensor] = None) -> None:
     """fp32-state AdamW, in place on params, exp_avg and exp_avg_sq (device tensors);
     params_bf16 as in lt_hybrid8bit_adamw_step."""
     k = len(params)
@@ -550,8 +563,8 @@ def lt_adamw_fp32_step(params: Sequence[torch.Tensor], grads: Sequence[torch.Ten
             _ptr_array(params), _ptr_array(grads), gdt, _ptr_array(exp_avg), _ptr_array(exp_avg_sq),
             wb, _numel_array(params), k, float(lr), float(beta1), float(beta2), float(eps),
             float(weight_decay), int(step), _scalar(coef, device, torch.float32, "coef"),
-            _scalar(status, device, torch.int32, "status"), ws.data_ptr(),
-            ws.numel() * ws.element_size(), _stream_handle(stream, device)))
+            _scalar(status, device, torch.int32, "status"), _state_ptr(step_state, device),
+            ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(stream, device)))
 
 
 def lt_select_8bit_slice(numels: Sequence[int], fraction: float):
@@ -561,6 +574,52 @@ def lt_select_8bit_slice(numels: Sequence[int], fraction: float):
     chosen = ctypes.c_int64()
     _check(lib().lt_select_8bit_slice(n, len(numels), float(fraction), out, ctypes.byref(chosen)))
     return [bool(x) for x in out], chosen.value
+
+
+def _state_ptr(state: Optional[torch.Tensor], device) -> int:
+    if state is None:
+        return 0
+    if state.device != device or state.dtype != torch.uint8 or not state.is_contiguous():
+        raise ValueError(f"step_state must be a contiguous uint8 tensor on {device}")
+    return state.data_ptr()
+
+
+STEP_STATE_HEADER = 64  # bytes of lt_step_state before the table
+
+
+def lt_step_state_bytes(table_len: int) -> int:
+    return int(lib().lt_step_state_bytes(int(table_len)))
+
+
+def lt_step_table(beta1: float, beta2: float, t_first: int, count: int):
+    """Host table entries of steps t_first .. t_first + count - 1, as a numpy structured
+    array (one_minus_beta1_t float64, rbc2 float32)."""
+    import numpy as np
+    out = np.zeros(count, dtype=[("one_minus_beta1_t", "<f8"), ("rbc2", "<f4"),
+                                 ("reserved", "<f4")])
+    _check(lib().lt_step_table(float(beta1), float(beta2), int(t_first), int(count),
+                               out.ctypes.data if count else None))
+    return out
+
+
+def lt_step_state_init(state: torch.Tensor, table_len: int, beta1: float, beta2: float,
+                       applied: int = 0, skips: int = 0, max_skips: int = 0,
+                       from_state: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Writes a device step state (see include/lazytrain.h) into a uint8 tensor."""
+    device = state.device
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_step_state_init(
+            _state_ptr(state, device), state.numel(), int(table_len), float(beta1), float(beta2),
+            int(applied), int(skips), int(max_skips), _state_ptr(from_state, device),
+            _stream_handle(stream, device)))
+
+
+def lt_step_state_advance(state: torch.Tensor, status: torch.Tensor, stream=None) -> None:
+    device = state.device
+    with torch.cuda.device(device):  # the library works on the current device
+        _check(lib().lt_step_state_advance(_state_ptr(state, device),
+                                           _scalar(status, device, torch.int32, "status"),
+                                           _stream_handle(stream, device)))
 
 
 def lt_read_status(status: torch.Tensor, stream=None) -> int:
@@ -592,18 +651,29 @@ class Hybrid8bitAdamW:
     without a host synchronization.  With ``slice_fraction`` None every tensor keeps
     8-bit states; otherwise lt_select_8bit_slice picks the tensors that do (the
     paper's 2% slice) and the others keep fp32 states (lt_adamw_fp32_step), all under
-    one global norm.  A step whose norm is not finite writes nothing (the kernels
-    skip it on the device); the object counts such skips in a row when it reads a
-    step's status (at the next ``step()`` or ``last_status()``) and raises
-    NonFiniteAbort once ``max_consecutive_skips`` of them follow one another (App. C:
-    three; None never aborts).  With ``bf16_copy`` the steps also keep
-    ``params_bf16``, a bf16 copy of every parameter for the next forward pass,
-    written by the step kernels (valid after the first step).  The moments take the
-    non-linear decade-tree codes by default (``code_map``): with the linear codes a
-    second moment far below its block's largest rounds to code 0 while the first
-    moment does not, and the update then divides by little more than eps (the
-    drift tests measure hundreds of lr against fp64 AdamW); pass LT_MAP_LINEAR for
-    the linear codes."""
+    one global norm.
+
+    The step count lives on the device (a step state, see lt_step_state_init): each
+    step takes its index and bias corrections there, and lt_step_state_advance counts
+    it, so ``step()`` never waits for an earlier step and can run any number of steps
+    ahead of the GPU.  A step whose norm is not finite writes nothing and does not
+    count; after ``max_consecutive_skips`` of them in a row (App. C: three; None
+    never stops) the device skips every later step too.  The host learns of both
+    from status snapshots copied behind each step and read without waiting:
+    ``step()`` raises NonFiniteAbort once it has seen the stop, ``last_status()``
+    waits for the last step and raises then.  ``step_count`` and
+    ``consecutive_skips`` are the device's as last seen (exact after
+    ``last_status()``).  With ``bf16_copy`` the steps also keep ``params_bf16``, a
+    bf16 copy of every parameter for the next forward pass, written by the step
+    kernels (valid after the first step).  The moments take the non-linear
+    decade-tree codes by default (``code_map``): with the linear codes a second
+    moment far below its block's largest rounds to code 0 while the first moment
+    does not, and the update then divides by little more than eps (the drift tests
+    measure hundreds of lr against fp64 AdamW); pass LT_MAP_LINEAR for the linear
+    codes."""
+
+    TABLE = 4096     # step-table entries to start with; doubled on the device as needed
+    SNAPSHOTS = 64   # status snapshots in flight (step() waits only beyond this many)
 
     def __init__(self, params: Sequence[torch.Tensor], lr: float = 1e-5,
                  betas=(0.9, 0.999), eps: float = 1e-8, weight_decay: float = 0.01,
@@ -616,8 +686,8 @@ class Hybrid8bitAdamW:
         if max_consecutive_skips is not None and max_consecutive_skips < 1:
             raise ValueError("max_consecutive_skips must be >= 1 or None")
         self.max_consecutive_skips = max_consecutive_skips
-        self.consecutive_skips = 0
         dev = self.params[0].device
+        self.device = dev
         self.lr, self.betas, self.eps, self.weight_decay = lr, betas, eps, weight_decay
         self.max_norm, self.block_size, self.code_map = max_norm, block_size, code_map
         if slice_fraction is None:
@@ -641,13 +711,87 @@ class Hybrid8bitAdamW:
         self.total_norm = torch.zeros(1, dtype=torch.float32, device=dev)
         self.params_bf16 = [torch.empty(p.numel(), dtype=torch.bfloat16, device=dev)
                             for p in self.params] if bf16_copy else None
-        self.step_count = 0  # steps applied (skipped steps do not count)
-        self._unchecked = False
-        # the status of the last step, copied to pinned host memory behind it on its
-        # stream, so reading it waits for that step only, not for later work
-        self._status_host = torch.zeros(1, dtype=torch.int32, pin_memory=True)
-        self._status_event = torch.cuda.Event()
-        self._status_pending = False
+        # snapshots: per step, the state's first 32 bytes and the status, in pinned memory
+        self._snap = torch.zeros((self.SNAPSHOTS, 48), dtype=torch.uint8, pin_memory=True)
+        self._snap_events = [None] * self.SNAPSHOTS
+        self._pending = []  # snapshot slots enqueued and not yet read, oldest first
+        self._next_slot = 0
+        self._reset_state(0, 0)
+        # the zeroed states and the step state were written on the current stream; steps
+        # may come on any stream
+        torch.cuda.synchronize(dev)
+
+    # ------------------------------------------------------------ step state
+    def _reset_state(self, applied: int, skips: int, stream=None) -> None:
+        """A fresh device step state with this count (enqueued on the stream)."""
+        self._table_len = max(self.TABLE, 2 * (applied + 1))
+        self._state = torch.empty(lt_step_state_bytes(self._table_len), dtype=torch.uint8,
+                                  device=self.device)
+        lt_step_state_init(self._state, self._table_len, self.betas[0], self.betas[1],
+                           applied=applied, skips=skips,
+                           max_skips=self.max_consecutive_skips or 0, stream=stream)
+        self._bound = applied  # the device count cannot exceed this
+        self._seen = {"applied": applied, "skips": skips, "stopped": 0,
+                      "status": LT_STATUS_OK}
+
+    def _grow_state(self, stream) -> None:
+        """Doubles the step table; the count moves over on the device, unread."""
+        old = self._state
+        self._table_len *= 2
+        self._state = torch.empty(lt_step_state_bytes(self._table_len), dtype=torch.uint8,
+                                  device=self.device)
+        lt_step_state_init(self._state, self._table_len, self.betas[0], self.betas[1],
+                           max_skips=self.max_consecutive_skips or 0, from_state=old,
+                           stream=stream)
+        old.record_stream(self._torch_stream(stream))
+
+    def _read_snapshot(self, slot: int) -> None:
+        import struct
+        raw = bytes(self._snap[slot].numpy())
+        applied, _, skips, _, stopped = struct.unpack_from("<qqiii", raw, 0)
+        status = struct.unpack_from("<i", raw, 32)[0]
+        self._seen = {"applied": applied, "skips": skips, "stopped": stopped, "status": status}
+        if status == LT_STATUS_BAD_WORKSPACE:
+            raise LazyTrainError(LT_ERR_WORKSPACE, "a workspace lost its descriptors (it was "
+                                 "written or freed without lt_workspace_release)")
+
+    def _observe(self, wait: bool) -> None:
+        """Reads the snapshots whose copies have completed (all of them with wait)."""
+        while self._pending:
+            slot = self._pending[0]
+            ev = self._snap_events[slot]
+            if wait:
+                ev.synchronize()
+            elif not ev.query():
+                return
+            self._pending.pop(0)
+            self._read_snapshot(slot)
+
+    @property
+    def step_count(self) -> int:
+        """Steps applied, as last seen from the device."""
+        return self._seen["applied"]
+
+    @property
+    def consecutive_skips(self) -> int:
+        return self._seen["skips"]
+
+    @consecutive_skips.setter
+    def consecutive_skips(self, value: int) -> None:
+        """Sets the device's count of skips in a row (and clears a stop), in stream
+        order, so that a caller can go on after NonFiniteAbort."""
+        self._observe(wait=True)
+        v = torch.tensor([int(value)], dtype=torch.int32).view(torch.uint8)
+        self._state[16:20].copy_(v)                        # skips
+        self._state[24:28].zero_()                         # stopped
+        torch.cuda.synchronize(self.device)  # before steps on any stream read it
+        self._seen = dict(self._seen, skips=int(value), stopped=0)
+
+    def _raise_if_stopped(self) -> None:
+        if self._seen["stopped"] == 1:
+            raise NonFiniteAbort(self._seen["skips"])
+        if self._seen["stopped"] == 2:
+            raise LazyTrainError(LT_ERR_INVALID_ARG, "the step table ran out")
 
     def _torch_stream(self, stream):
         dev = self.params[0].device
@@ -657,6 +801,7 @@ class Hybrid8bitAdamW:
             return stream
         return torch.cuda.ExternalStream(int(stream), device=dev)
 
+    # ------------------------------------------------------------------ step
     def step(self, grads: Sequence[torch.Tensor], stream=None) -> None:
         """One clipped step with one gradient per parameter, in the order of the
         parameters (a zero-element parameter takes a zero-element gradient)."""
@@ -671,16 +816,16 @@ class Hybrid8bitAdamW:
             if g.numel() != p.numel():
                 raise ValueError(f"gradient {i} has {g.numel()} elements, its parameter "
                                  f"{p.numel()}")
-        if self._unchecked:
-            self.last_status(stream)  # the bias correction needs the true step count
-        self._raise_if_aborted()
-        t = self.step_count + 1
+        self._observe(wait=False)
+        self._raise_if_stopped()
+        if self._bound + 1 > self._table_len:
+            self._grow_state(stream)
         lt_grad_sqnorm(grads, self.sq_total, self.status, stream=stream)
         clip = self.max_norm if self.max_norm is not None else math.inf
         lt_clip_coef(self.sq_total, clip, self.coef, self.total_norm, stream=stream)
         hyper = dict(lr=self.lr, beta1=self.betas[0], beta2=self.betas[1], eps=self.eps,
-                     weight_decay=self.weight_decay, step=t, coef=self.coef, status=self.status,
-                     stream=stream)
+                     weight_decay=self.weight_decay, step=0, coef=self.coef, status=self.status,
+                     stream=stream, step_state=self._state)
         wb = self.params_bf16
         if self.idx8:
             lt_hybrid8bit_adamw_step([self.params[i] for i in self.idx8],
@@ -693,50 +838,38 @@ class Hybrid8bitAdamW:
                                [grads[i] for i in self.idx32], self.exp_avg, self.exp_avg_sq,
                                params_bf16=None if wb is None else [wb[i] for i in self.idx32],
                                **hyper)
+        lt_step_state_advance(self._state, self.status, stream=stream)
+        self._bound += 1
+        # a snapshot of the count and the status, read later without waiting
+        slot = self._next_slot
+        self._next_slot = (slot + 1) % self.SNAPSHOTS
+        if slot in self._pending:  # more than SNAPSHOTS steps ahead: wait for the oldest
+            self._observe(wait=True)
         s = self._torch_stream(stream)
         with torch.cuda.stream(s):
-            self._status_host.copy_(self.status, non_blocking=True)
-        self._status_event.record(s)
-        self._status_pending = True
-        self.step_count = t
-        self._unchecked = True
+            self._snap[slot, :32].copy_(self._state[:32], non_blocking=True)
+            self._snap[slot, 32:36].copy_(self.status.view(torch.uint8), non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record(s)
+        self._snap_events[slot] = ev
+        self._pending.append(slot)
 
     def last_status(self, stream=None) -> int:
-        """Reads the status of the last step, waiting for that step only (not for work
-        enqueued after it); a skipped step is taken off the step count once and
-        counted towards the consecutive-skip limit, which raises NonFiniteAbort."""
-        if self._status_pending:
-            self._status_event.synchronize()
-            st = int(self._status_host[0])
+        """Waits for the last step only (not for work enqueued after it) and returns
+        its status; raises NonFiniteAbort if the device has stopped after
+        max_consecutive_skips skips in a row."""
+        if self._pending:
+            self._observe(wait=True)
         else:
-            st = lt_read_status(self.status, stream)
-        if st == LT_STATUS_BAD_WORKSPACE:
-            raise LazyTrainError(LT_ERR_WORKSPACE, "a workspace lost its descriptors (it was "
-                                 "written or freed without lt_workspace_release)")
-        if self._unchecked:
-            if st == LT_STATUS_NONFINITE:
-                self.step_count -= 1
-                self.consecutive_skips += 1
-            else:
-                self.consecutive_skips = 0
-        self._unchecked = False
-        self._raise_if_aborted()
-        return st
-
-    def _raise_if_aborted(self) -> None:
-        """Once the limit is reached every step() and last_status() raises, until the
-        caller sets consecutive_skips back (or loads a checkpoint)."""
-        if (self.max_consecutive_skips is not None and
-                self.consecutive_skips >= self.max_consecutive_skips):
-            raise NonFiniteAbort(self.consecutive_skips)
+            self._seen["status"] = lt_read_status(self.status, stream)
+        self._raise_if_stopped()
+        return self._seen["status"]
 
     def state_dict(self, stream=None) -> dict:
         """The optimizer state for a checkpoint: the step count, the hyperparameters,
         which tensors are 8-bit, and host copies of the codes, scales and fp32 moments
-        (the master weights are the caller's parameters).  Reads the last status first,
-        so the step count is exact."""
-        if self._unchecked:
-            self.last_status(stream)
+        (the master weights are the caller's parameters).  Waits for the last step."""
+        self._observe(wait=True)
         host = lambda ts: [t.detach().cpu().clone() for t in ts]
         return {
             "step_count": self.step_count,
@@ -770,9 +903,9 @@ class Hybrid8bitAdamW:
                 if a.shape != b.shape or a.dtype != b.dtype:
                     raise ValueError(f"{name}: shape or dtype differs from the checkpoint")
                 a.copy_(b)
-        self.step_count = int(state["step_count"])
-        self.consecutive_skips = int(state.get("consecutive_skips", 0))
-        self._unchecked = False
+        self._observe(wait=True)
+        self._reset_state(int(state["step_count"]), int(state.get("consecutive_skips", 0)))
+        torch.cuda.synchronize(self.device)
 
 
 class StreamedHybrid8bitAdamW:

@@ -30,38 +30,38 @@ int main() {
     int8_t* mq[1] = {nullptr}; uint8_t* vq[1] = {nullptr}; float* a[1] = {nullptr};
     int64_t n1[1] = {16};
     if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, 2048, LT_MAP_LINEAR,
-                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, 1000, LT_MAP_LINEAR,
-                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, 2048, 7,
-                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_grad_sqnorm(g, n1, 1, 9, nullptr, 0, nullptr, nullptr, nullptr, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_clip_coef(nullptr, 1.0f, nullptr, nullptr, nullptr, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     // eps must be > 0, also in fp32 (checked before any pointer or device call)
     for (double bad_eps : {0.0, -1e-8, 1e-50, (double)INFINITY})
         if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, 2048,
                                      LT_MAP_LINEAR, 1e-4, 0.9, 0.999, bad_eps, 0.01, 1, nullptr,
-                                     nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+                                     nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     // block sizes: multiples of 64 in [64, 65536]
     for (int bad_block : {0, 32, 96 + 8, 65536 + 64})
         if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n1, 1, bad_block,
                                      LT_MAP_LINEAR, 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr,
-                                     nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+                                     nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_adamw_fp32_step(p, g, LT_DTYPE_F32, p, p, nullptr, n1, 1, NAN, 0.9, 0.999, 1e-8, 0.01, 1,
-                           nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
+                           nullptr, nullptr, nullptr, nullptr, 0, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     // empty lists and zero-element tensors: validated, then nothing to launch
     alignas(256) static uint8_t host_ws[4096];
     if (lt_workspace_release(nullptr) != LT_OK || lt_workspace_release(host_ws) != LT_OK) ++bad;
     if (lt_select_8bit_slice(nullptr, 0, 0.5, nullptr, &chosen) != LT_OK || chosen != 0) ++bad;
     if (lt_hybrid8bit_adamw_step(nullptr, nullptr, LT_DTYPE_BF16, nullptr, nullptr, nullptr, nullptr,
                                  nullptr, nullptr, 0, 2048, LT_MAP_LINEAR, 1e-4, 0.9, 0.999, 1e-8,
-                                 0.01, 1, nullptr, nullptr, host_ws, sizeof host_ws, nullptr) != LT_OK) ++bad;
+                                 0.01, 1, nullptr, nullptr, nullptr, host_ws, sizeof host_ws, nullptr) != LT_OK) ++bad;
     int64_t n0[2] = {0, 0};
     if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, n0, 1, 2048, LT_MAP_DYNAMIC,
-                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, host_ws,
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, host_ws,
                                  sizeof host_ws, nullptr) != LT_OK) ++bad;
     if (lt_adamw_fp32_step(nullptr, nullptr, LT_DTYPE_F32, nullptr, nullptr, nullptr, nullptr, 0, 1e-4,
-                           0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, host_ws, sizeof host_ws,
+                           0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, host_ws, sizeof host_ws,
                            nullptr) != LT_OK) ++bad;
     const void* g2[2] = {nullptr, nullptr};  // pointers of empty tensors are not read
     if (lt_grad_sqnorm_partials(g2, n0, 2, LT_DTYPE_BF16, nullptr, nullptr, 0, nullptr) != LT_OK) ++bad;
@@ -69,7 +69,7 @@ int main() {
         LT_ERR_INVALID_ARG) ++bad;  // a NULL list of two tensors
     int64_t nneg[1] = {-1};
     if (lt_hybrid8bit_adamw_step(p, g, LT_DTYPE_BF16, mq, a, vq, a, nullptr, nneg, 1, 2048, LT_MAP_LINEAR,
-                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, host_ws,
+                                 1e-4, 0.9, 0.999, 1e-8, 0.01, 1, nullptr, nullptr, nullptr, host_ws,
                                  sizeof host_ws, nullptr) != LT_ERR_INVALID_ARG) ++bad;
     if (lt_grad_chunk_count(n0, 2) != 0 || lt_grad_sqnorm_workspace_bytes(nullptr, 0) == 0) ++bad;
     // overlap rule: the addresses are compared before anything is read or launched
@@ -86,7 +86,7 @@ int main() {
     auto step8 = [&]() {
         return lt_hybrid8bit_adamw_step(pw, gw, LT_DTYPE_BF16, mqw, maw, vqw, vaw, nullptr, n2, 2,
                                         2048, LT_MAP_LINEAR, 1e-4, 0.9, 0.999, 1e-8, 0.01, 1,
-                                        nullptr, nullptr, nullptr, 0, nullptr);
+                                        nullptr, nullptr, nullptr, nullptr, 0, nullptr);
     };
     if (step8() != LT_ERR_WORKSPACE) ++bad;       // disjoint, shared gradient
     pw[1] = (float*)(mem + 4080);                 // params[1] shares the last 16 bytes of params[0]
@@ -103,7 +103,7 @@ int main() {
     float* es[2] = {(float*)(mem + 28672), (float*)(mem + 32768)};
     auto step32 = [&]() {
         return lt_adamw_fp32_step(pw, gw, LT_DTYPE_BF16, ea, es, nullptr, n2, 2, 1e-4, 0.9, 0.999,
-                                  1e-8, 0.01, 1, nullptr, nullptr, nullptr, 0, nullptr);
+                                  1e-8, 0.01, 1, nullptr, nullptr, nullptr, nullptr, 0, nullptr);
     };
     if (step32() != LT_ERR_WORKSPACE) ++bad;
     es[0] = (float*)(mem + 24576 + 4080);         // exp_avg_sq[0] shares 16 bytes with exp_avg[1]

@@ -133,7 +133,7 @@ def test_hyperparameter_and_block_size_rejection_without_a_device():
     def step(block, eps):
         return L.lt_hybrid8bit_adamw_step(one(0), one(1), lt.LT_DTYPE_BF16, one(2), one(3), one(4),
                                           one(5), None, n1, 1, block, lt.LT_MAP_LINEAR, 1e-4, 0.9,
-                                          0.999, eps, 0.01, 1, None, None, None, 0, None)
+                                          0.999, eps, 0.01, 1, None, None, None, None, 0, None)
 
     for eps in (0.0, -1e-8, 1e-50, float("inf"), float("nan")):
         assert step(2048, eps) == lt.LT_ERR_INVALID_ARG

@@ -163,8 +163,9 @@ def test_checkpoint_resume_is_bitwise_uninterrupted(code_map, tmp_path):
 
 def test_optimizer_aborts_after_three_consecutive_skips():
     """App. C safety checks: a non-finite gradient skips the step; skips in a row are
-    counted when the status is read, a finite step resets the count, and the third
-    consecutive skip raises NonFiniteAbort with the weights untouched since the last
+    counted on the device, a finite step resets the count, and after the third
+    consecutive skip the device applies no further step and the host raises
+    NonFiniteAbort when it reads the state, with the weights untouched since the last
     applied step.  max_consecutive_skips=None never aborts."""
     rng = np.random.default_rng(46)
     sizes = [3000, 4096]
@@ -196,10 +197,24 @@ def test_optimizer_aborts_after_three_consecutive_skips():
     opt.step(grads(False))
     assert opt.last_status() == lt.LT_STATUS_OK and opt.step_count == 3
 
-    # the abort also comes from step() when the status was not read in between
-    opt = lt.Hybrid8bitAdamW([to_dev(x) for x in w0], lr=1e-4, block_size=2048)
+    # without reading any status in between: the device stops after the third skip,
+    # so a finite step enqueued behind it writes nothing either; the abort surfaces at
+    # the first step() that has seen the stop (the copies of the gradients from
+    # pageable memory here may let the host see it already) or at the next read, and
+    # every later step() raises
+    params2 = [to_dev(x) for x in w0]
+    opt = lt.Hybrid8bitAdamW(params2, lr=1e-4, block_size=2048)
     for _ in range(3):
         opt.step(grads(True))
+    try:
+        opt.step(grads(False))
+    except lt.NonFiniteAbort:
+        pass
+    with pytest.raises(lt.NonFiniteAbort) as e:
+        opt.last_status()
+    assert e.value.skips == 3 and opt.step_count == 0
+    for a, p in zip(w0, params2):
+        assert to_host(p).tobytes() == a.tobytes()
     with pytest.raises(lt.NonFiniteAbort):
         opt.step(grads(False))
 
