@@ -201,6 +201,36 @@ def counter_traffic(workload_name: str):
     return None
 
 
+_pinned_keep = []
+
+
+def pinned(n: int, dtype, zero: bool = False):
+    """A CPU tensor of n elements in pinned memory of exactly its size (hipHostMalloc;
+    torch's pinned allocator rounds each allocation up to a power of two, which at the
+    27B-class model's 169 GB would cost up to twice the memory).  Kept until exit."""
+    import ctypes
+
+    import numpy as np
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipHostMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t,
+                                  ctypes.c_uint]
+    hip.hipHostMalloc.restype = ctypes.c_int
+    item = torch.empty(0, dtype=dtype).element_size()
+    nbytes = max(n * item, 1)
+    ptr = ctypes.c_void_p()
+    rc = hip.hipHostMalloc(ctypes.byref(ptr), nbytes, 0)
+    if rc != 0:
+        hip.hipGetLastError()  # the failure would otherwise surface at the next HIP call
+        raise RuntimeError(f"hipHostMalloc of {nbytes} bytes failed ({rc})")
+    buf = (ctypes.c_uint8 * nbytes).from_address(ptr.value)
+    t = torch.from_numpy(np.frombuffer(buf, dtype=np.uint8, count=n * item)).view(dtype)
+    _pinned_keep.append(buf)
+    if zero:
+        t.zero_()
+    return t
+
+
 def pcie_rates(dev, nbytes: int):
     """Pinned host <-> HBM copy rates on this machine: H2D alone, D2H alone and both at
     once on two streams (GB/s each), with hipMemcpyAsync as the streamed step issues
@@ -274,21 +304,20 @@ def run_streamed(args, w, dev, n_threads) -> int:
             k = r * per_layer + j
             n = w.numels[k]
             nb = -(-n // B)
-            wt = torch.empty(n, dtype=torch.float32, pin_memory=True)
+            wt = pinned(n, torch.float32)
             synth.fill_ptr(wt.data_ptr(), synth.F32, 0, n, w.seed, synth.STREAM_WEIGHTS, k,
                            w.weight_recipe, n_threads)
-            gt = torch.empty(n, dtype=torch.bfloat16, pin_memory=True)
+            gt = pinned(n, torch.bfloat16)
             synth.fill_ptr(gt.data_ptr(), synth.BF16, 0, n, w.seed, synth.grad_stream(w.step), k,
                            w.grad_recipe, n_threads)
             host["w"].append(wt)
             host["g"].append(gt)
-            host["mq"].append(torch.zeros(n, dtype=torch.int8, pin_memory=True))
-            host["vq"].append(torch.zeros(n, dtype=torch.uint8, pin_memory=True))
-            host["ma"].append(torch.zeros(nb, dtype=torch.float32, pin_memory=True))
-            host["va"].append(torch.zeros(nb, dtype=torch.float32, pin_memory=True))
+            host["mq"].append(pinned(n, torch.int8, zero=True))
+            host["vq"].append(pinned(n, torch.uint8, zero=True))
+            host["ma"].append(pinned(nb, torch.float32, zero=True))
+            host["va"].append(pinned(nb, torch.float32, zero=True))
             if args.bf16_copy:
-                host.setdefault("wb", []).append(torch.empty(n, dtype=torch.bfloat16,
-                                                             pin_memory=True))
+                host.setdefault("wb", []).append(pinned(n, torch.bfloat16))
         log(f"host layer {r + 1}/{R} ready ({time.time() - t0:.1f} s)")
     lists = {name: [v[(l % R) * per_layer + j] for l in range(L) for j in range(per_layer)]
              for name, v in host.items()}
@@ -310,7 +339,9 @@ def run_streamed(args, w, dev, n_threads) -> int:
         acc = lt.GradNormAccumulator(w.numels, dev)
     torch.cuda.synchronize()
 
-    def step(t):
+    lev = [torch.cuda.Event(enable_timing=True) for _ in range(8 * L)]
+
+    def step(t, events=None):
         if acc is not None:
             with torch.cuda.stream(cs):
                 for l in reversed(range(L)):  # backward order
@@ -324,7 +355,7 @@ def run_streamed(args, w, dev, n_threads) -> int:
             d2h_stream=ds, params_bf16=lists.get("wb"), norm_ready=acc is not None,
             keep_grads=args.keep_grads,
             code_map=lt.LT_MAP_DYNAMIC if args.code_map == "dynamic" else lt.LT_MAP_LINEAR,
-            **hyper)
+            layer_events=events, **hyper)
 
     t = 1
     for _ in range(args.warmup):
@@ -334,13 +365,14 @@ def run_streamed(args, w, dev, n_threads) -> int:
         log(f"warmup step done")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(t)
+    for i in range(args.steps):
+        step(t, lev if i == args.steps - 1 else None)  # the last step records its phases
         t += 1
         cs.synchronize()
         log(f"timed step done ({time.perf_counter() - t0:.2f} s)")
     elapsed = time.perf_counter() - t0
     st = lt.lt_read_status(status, cs)
+    phases = streamed_phases(lev, L, w, B, args)
     per = elapsed / args.steps
     n = w.n_params
     nb = sum(-(-x // B) for x in w.numels)
@@ -361,7 +393,10 @@ def run_streamed(args, w, dev, n_threads) -> int:
                    ("+dynamic-map" if args.code_map == "dynamic" else ""), "params": n,
                    "tensors": len(w.shapes), "layers": L,
                    "block_size": B, "grad_dtype": "bf16", "ring_slots": slots,
-                   "host_layers": R, "host_state": "pinned, cycled over host_layers"},
+                   "host_layers": R,
+                   "host_state": "pinned, every layer distinct" if R == L else
+                                 "pinned, cycled over host_layers"},
+        "phases_last_step": phases,
         "pcie": {"h2d_bytes_per_step": h2d, "d2h_bytes_per_step": d2h, **rates,
                  "link_bound_ms": round(bound * 1e3, 1),
                  "h2d_gbps_achieved": round(h2d / per / 1e9, 2),
@@ -378,6 +413,38 @@ def run_streamed(args, w, dev, n_threads) -> int:
         out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
     return 0
+
+
+def streamed_phases(ev, L: int, w, B: int, args):
+    """Per-phase times of one streamed step from the events the call recorded around
+    each layer's work: the summed durations of the pass-1 gradient copies, the pass-2
+    copies in, the step kernels and the copies out, their bytes and rates, and the
+    span from the first copy in to the last copy out."""
+    def total(a, b):
+        return sum(ev[8 * i + a].elapsed_time(ev[8 * i + b]) for i in range(L))
+    per_layer = len(w.numels) // L
+    n = w.n_params
+    nb = sum(-(-x // B) for x in w.numels)
+    once = args.keep_grads and not args.norm_on_arrival
+    out = {}
+    p1_bytes = 0 if args.norm_on_arrival else 2 * n
+    if p1_bytes:
+        ms = total(0, 1)
+        out["pass1_h2d"] = {"ms": round(ms, 1), "bytes": p1_bytes,
+                            "gbps": round(p1_bytes / ms / 1e6, 1)}
+    in_bytes = n * (6 if once else 8) + nb * 8
+    out_bytes = n * (8 if args.bf16_copy else 6) + nb * 8
+    for name, a, b, nbytes in (("pass2_h2d", 2, 3, in_bytes), ("d2h", 4, 5, out_bytes),
+                               ("step_kernels", 6, 7, None)):
+        ms = total(a, b)
+        out[name] = {"ms": round(ms, 1)}
+        if nbytes:
+            out[name].update(bytes=nbytes, gbps=round(nbytes / ms / 1e6, 1))
+    first = 0 if p1_bytes else 2
+    out["span_ms"] = round(ev[first].elapsed_time(ev[8 * (L - 1) + 5]), 1)
+    out["note"] = ("each phase's summed per-layer durations; the copies in and out of "
+                   "different layers run at the same time, sharing the link")
+    return out
 
 
 def stream_ceiling(n_elements: int, pattern: str = "step8"):
@@ -444,6 +511,33 @@ def same_array_probe(params, grads, m_codes, v_codes, gbytes, dev, stream, reps=
     return sorted(ms)[len(ms) // 2], n * (12 + gbytes)
 
 
+def warm_kernels(dev, gdt, B: int, code_map: int, stream, fp32_states: bool):
+    """Runs each kernel the timed steps use once, on a scratch list of one block, so that
+    the first timed step does not pay for loading their code (the clip-stress workload
+    times its first three steps from zero state, with no warmup steps).  The workload's
+    own tensors are not touched."""
+    import torch
+
+    import paper_2608_11919_amd as lt
+    n = B
+    w = torch.zeros(n, dtype=torch.float32, device=dev)
+    g = torch.zeros(n, dtype=gdt, device=dev)
+    S = torch.zeros(1, dtype=torch.float64, device=dev)
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    coef = torch.zeros(1, dtype=torch.float32, device=dev)
+    h = dict(lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1, coef=coef,
+             status=st, stream=stream)
+    lt.lt_grad_sqnorm([g], S, st, stream=stream)
+    lt.lt_clip_coef(S, 1.0, coef, stream=stream)
+    lt.lt_hybrid8bit_adamw_step([w], [g], [torch.zeros(n, dtype=torch.int8, device=dev)],
+                                [torch.zeros(1, device=dev)],
+                                [torch.zeros(n, dtype=torch.uint8, device=dev)],
+                                [torch.zeros(1, device=dev)], B, code_map=code_map, **h)
+    if fp32_states:
+        lt.lt_adamw_fp32_step([w], [g], [torch.zeros_like(w)], [torch.zeros_like(w)], **h)
+    torch.cuda.synchronize()
+
+
 def copy_probe(dev, nbytes: int, reps: int):
     """A plain copy kernel of known size, for scaling the HBM byte counters."""
     import torch
@@ -481,7 +575,8 @@ def main() -> int:
                          "already in HBM (as they arrive in backward) and the step skips its "
                          "first streamed pass")
     ap.add_argument("--host-layers", type=int, default=8,
-                    help="streamed workload: distinct pinned host layers the model cycles over")
+                    help="streamed workload: distinct pinned host layers the model cycles over "
+                         "(these boxes pin about 63 GB, 24 layers, of the 169 GB all 64 need)")
     ap.add_argument("--ring-slots", type=int, default=3, help="streamed workload: device slots")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the data-movement ceiling probe")
@@ -586,6 +681,7 @@ def main() -> int:
         if scratch is not None:
             scratch.fill_(float(t))  # a kernel that writes every byte (no memset node)
 
+    warm_kernels(dev, grads[0].dtype, B, code_map, stream, bool(idx32))
     t = t_first
     for _ in range(args.warmup):
         flush()
