@@ -466,12 +466,14 @@ def stream_ceiling(n_elements: int, pattern: str = "step8"):
     return json.loads(r.stdout.strip().splitlines()[-1])
 
 
-def same_array_probe(params, grads, m_codes, v_codes, gbytes, dev, stream, reps=3):
-    """Times paper_2608_11919_amd/libltprobe.so (csrc/mix_probe.hip) over the step's
+def same_array_probe(params, grads, m_states, v_states, gbytes, state_bytes, dev, stream,
+                     reps=3):
+    """Times paper_2608_11919_amd/libltprobe.so (csrc/mix_probe.hip) over a step's
     own arrays, in this process: the fused step's per-element bytes (the weight, the
-    gradient and both codes read; the weight and both codes written back in place)
-    in the step kernel's geometry and unit order, with no arithmetic.  An even number
-    of passes XORs every array back to its contents.  Returns (median ms, bytes)."""
+    gradient and both moment states read; the weight and both states written back in
+    place; state_bytes 1 for the 8-bit codes, 4 for fp32 moments) in the step kernel's
+    geometry and unit order, with no arithmetic.  An even number of passes XORs every
+    array back to its contents.  Returns (median ms, bytes)."""
     import ctypes
 
     import torch
@@ -481,7 +483,8 @@ def same_array_probe(params, grads, m_codes, v_codes, gbytes, dev, stream, reps=
         return None
     L = ctypes.CDLL(path)
     L.ltp_mix_same_arrays.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
-                                      ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+                                      ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      ctypes.c_void_p]
     L.ltp_mix_same_arrays.restype = ctypes.c_int
     K = len(params)
     units = [-(-p.numel() // 2048) for p in params]
@@ -492,7 +495,7 @@ def same_array_probe(params, grads, m_codes, v_codes, gbytes, dev, stream, reps=
     table = torch.zeros((K, 8), dtype=torch.int64)
     for k in range(K):
         table[k, :5] = torch.tensor([params[k].data_ptr(), grads[k].data_ptr(),
-                                     m_codes[k].data_ptr(), v_codes[k].data_ptr(),
+                                     m_states[k].data_ptr(), v_states[k].data_ptr(),
                                      params[k].numel()], dtype=torch.int64)
     d_table = table.to(dev)
     grid = 3 * torch.cuda.get_device_properties(dev).multi_processor_count
@@ -501,14 +504,15 @@ def same_array_probe(params, grads, m_codes, v_codes, gbytes, dev, stream, reps=
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
         rc = L.ltp_mix_same_arrays(d_prefix.data_ptr(), d_table.data_ptr(), K, prefix[-1], gbytes,
-                                   grid, stream.cuda_stream)
+                                   state_bytes, grid, stream.cuda_stream)
         b.record(stream)
         if rc != 0:
             raise RuntimeError(f"ltp_mix_same_arrays failed ({rc})")
         torch.cuda.synchronize()
         ms.append(a.elapsed_time(b))
     n = sum(p.numel() for p in params)
-    return sorted(ms)[len(ms) // 2], n * (12 + gbytes)
+    # per element: the weight read and written, the gradient read, each state read and written
+    return sorted(ms)[len(ms) // 2], n * (8 + gbytes + 4 * state_bytes)
 
 
 def warm_kernels(dev, gdt, B: int, code_map: int, stream, fp32_states: bool):
@@ -802,19 +806,33 @@ def main() -> int:
                      "bytes_per_launch": kbytes},
         "status": st,
     }
-    if not args.no_ceiling and not idx32 and not args.bf16_copy:
-        probe = same_array_probe(p8, g8, s8[0], s8[2], gb, dev, stream)
-        if probe is not None:
-            p_ms, p_bytes = probe
+    if not args.no_ceiling and not args.bf16_copy:
+        # each step kernel's byte pattern over its own arrays; the hybrid step's two
+        # kernels run one after the other, so their probe times add
+        runs = []
+        if p8:
+            runs.append(("k_adamw8_step", same_array_probe(p8, g8, s8[0], s8[2], gb, 1, dev,
+                                                           stream)))
+        if p32:
+            runs.append(("k_adamw32_step", same_array_probe(p32, g32, exp_avg, exp_avg_sq, gb,
+                                                            4, dev, stream)))
+        if runs and all(r is not None for _, r in runs):
+            p_ms = sum(r[0] for _, r in runs)
+            p_bytes = sum(r[1] for _, r in runs)
             p_gbps = p_bytes / (p_ms * 1e-3) / 1e9
+            # the step's rate counts its block scales (16 B per block), the probe's does not
             out["same_array_probe"] = {
-                "probe": "csrc/mix_probe.hip over the step's own arrays in this process: the "
-                         "step kernel's bytes per element, geometry and unit order, no "
+                "probe": "csrc/mix_probe.hip over the step's own arrays in this process: "
+                         "each step kernel's bytes per element, geometry and unit order, no "
                          "arithmetic (scales not moved)",
                 "ms": round(p_ms, 4), "bytes": p_bytes, "gbps": round(p_gbps, 1),
                 "frac_of_peak": round(p_gbps / PEAK_HBM_GBPS, 4),
                 "step_kernel_frac_of_probe": round(achieved / p_gbps, 4)}
-            log(f"same-array probe: {p_ms:.3f} ms, {p_gbps:.0f} GB/s; the step kernel runs at "
+            if len(runs) > 1:
+                out["same_array_probe"]["kernels"] = {
+                    k: {"ms": round(r[0], 4), "bytes": r[1],
+                        "gbps": round(r[1] / (r[0] * 1e-3) / 1e9, 1)} for k, r in runs}
+            log(f"same-array probe: {p_ms:.3f} ms, {p_gbps:.0f} GB/s; the step runs at "
                 f"{achieved / p_gbps:.3f} of it")
     if not args.no_ceiling and gb == 2:
         # the probe pattern of each step kernel, at the whole model's size; the hybrid

@@ -15,12 +15,20 @@
 // handed to the waves in turn.  The other two patterns are timed as wave tiles of 16
 // and 32 elements per lane.  Prints one JSON line.
 // Usage: stream_ceiling [n] [reps] [step8 | step8_copy | adamw32]
+//
+// Placement mode: stream_ceiling n reps step8|adamw32 sets K allocates K sets of
+// the pattern's arrays, each array its own hipMalloc and all sets alive at once,
+// and times the pattern (wave tiles of 32 elements per lane, 3 workgroups per CU)
+// on each set, then on each set again.  Sets that differ only in where the
+// allocator placed them show how much the rate depends on physical placement.
+// Prints one JSON line per pass over the sets.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <vector>
 
 #define CK(x)                                                                       \
     do {                                                                            \
@@ -220,6 +228,77 @@ __global__ __launch_bounds__(kThreads) void k_read(const u32x4* __restrict__ g, 
         sink[0] = acc;
 }
 
+// One set of a pattern's arrays (step8: w, g, m, v; adamw32: w, g, m4, v4).
+struct ArraySet {
+    uint4 *w = nullptr, *g = nullptr, *m4 = nullptr, *v4 = nullptr;
+    uint2 *m = nullptr, *v = nullptr;
+};
+
+int run_sets(int64_t n, int reps, int pattern, const char* pname, int K)
+{
+    int cus;
+    CK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0));
+    std::vector<ArraySet> sets(K);
+    for (ArraySet& s : sets) {
+        CK(hipMalloc(&s.w, n * 4));
+        CK(hipMalloc(&s.g, n * 2));
+        CK(hipMemset(s.w, 1, n * 4));
+        CK(hipMemset(s.g, 2, n * 2));
+        if (pattern == kAdamW32) {
+            CK(hipMalloc(&s.m4, n * 4));
+            CK(hipMalloc(&s.v4, n * 4));
+            CK(hipMemset(s.m4, 3, n * 4));
+            CK(hipMemset(s.v4, 4, n * 4));
+        } else {
+            CK(hipMalloc(&s.m, n));
+            CK(hipMalloc(&s.v, n));
+            CK(hipMemset(s.m, 3, n));
+            CK(hipMemset(s.v, 4, n));
+        }
+    }
+    hipEvent_t a, b;
+    CK(hipEventCreate(&a));
+    CK(hipEventCreate(&b));
+    const int grid = 3 * cus;
+    const int64_t tiles = n / 2048;  // n is a multiple of 2048
+    const double per_elem = pattern == kStep8 ? 14.0 : 26.0;
+    for (int pass = 0; pass < 2; ++pass) {
+        printf("{\"n\": %lld, \"pattern\": \"%s\", \"pass\": %d, \"sets\": [", (long long)n,
+               pname, pass);
+        for (int k = 0; k < K; ++k) {
+            const ArraySet& s = sets[k];
+            float ms;
+            if (pattern == kStep8) {
+                k_mix_tiles<<<grid, kThreads>>>(s.w, s.g, s.m, s.v, tiles);  // warm
+                CK(hipGetLastError());
+                CK(hipEventRecord(a));
+                for (int r = 0; r < reps; ++r)
+                    k_mix_tiles<<<grid, kThreads>>>(s.w, s.g, s.m, s.v, tiles);
+                CK(hipEventRecord(b));
+                CK(hipEventSynchronize(b));
+                CK(hipEventElapsedTime(&ms, a, b));
+                ms /= reps;
+            } else {
+                ms = time_pattern<kAdamW32, 4>(grid, reps, s.w, s.g, nullptr, nullptr, s.m4, s.v4,
+                                               nullptr, n, a, b);
+                if (ms < 0.f) {
+                    fprintf(stderr, "pattern kernel launch or timing failed\n");
+                    return 1;
+                }
+            }
+            printf("%s{\"set\": %d, \"ms\": %.4f, \"gbps\": %.1f}", k ? ", " : "", k, ms,
+                   double(n) * per_elem / ms / 1e6);
+        }
+        printf("]}\n");
+        fflush(stdout);
+    }
+    for (ArraySet& s : sets)
+        for (void* p : {(void*)s.w, (void*)s.g, (void*)s.m, (void*)s.v, (void*)s.m4, (void*)s.v4})
+            if (p)
+                CK(hipFree(p));
+    return 0;
+}
+
 int main(int argc, char** argv)
 {
     const int64_t n_req = argc > 1 ? atoll(argv[1]) : 3085844480LL;
@@ -235,6 +314,15 @@ int main(int argc, char** argv)
         fprintf(stderr, "need n >= %lld, reps >= 1 and pattern step8, step8_copy or adamw32\n",
                 (long long)kIter);
         return 2;
+    }
+    if (argc > 4) {
+        const int K = argc > 5 && !strcmp(argv[4], "sets") ? atoi(argv[5]) : 0;
+        if (K < 1 || K > 64 || pattern == kStep8Copy) {
+            fprintf(stderr, "placement mode: stream_ceiling n reps step8|adamw32 sets K "
+                            "(1 <= K <= 64)\n");
+            return 2;
+        }
+        return run_sets(n, reps, pattern, pname, K);
     }
     int cus;
     CK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0));
