@@ -22,7 +22,8 @@ SUB = np.float32(1e-40)  # fp32 subnormal
 
 def _edge_problem(block, code_map, seed):
     rng = np.random.default_rng(seed)
-    nb = 10
+    # at least 10 blocks, and two whole wave spans plus a ragged one at small blocks
+    nb = max(10, 2 * 2048 // block + 3)
     n = nb * block - 37  # ragged last block
     w = (rng.standard_normal(n) * 0.02).astype(np.float32)
     g32 = (rng.standard_t(3, size=n) * 1e-3).astype(np.float32)
@@ -41,6 +42,7 @@ def _edge_problem(block, code_map, seed):
     ma[5], va[5] = F32_MAX, F32_MAX                  # largest finite scales
     mq[blk(6)] = -128                                # the code the linear map never writes
     va[7] = -np.inf
+    ma[nb - 1], va[nb - 2] = np.nan, np.inf          # in the last, ragged wave span
     # weights and gradients with special values, spread over the blocks
     idx = rng.choice(n, size=64, replace=False)
     w[idx[:8]] = np.nan
@@ -73,7 +75,7 @@ def _assert_equal_nan_aware(got: State, ref: State, what):
                                      f"first {bad[0]}: gpu {a[bad[0]]!r} oracle {b[bad[0]]!r}")
 
 
-@pytest.mark.parametrize("block", [256, 2048])
+@pytest.mark.parametrize("block", [64, 128, 256, 512, 2048])
 @pytest.mark.parametrize("code_map", [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC])
 @pytest.mark.parametrize("coef", [None, 0.37])
 def test_step_on_extreme_and_corrupted_states(block, code_map, coef):
