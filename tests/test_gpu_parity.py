@@ -99,6 +99,36 @@ def test_sqnorm_nonfinite_status(bad):
     assert not math.isfinite(to_host(S)[0])
 
 
+def test_sqnorm_repeated_calls_on_one_workspace():
+    """Forty calls on one workspace alternate between a list of 1500 tensors (the
+    total reads S_k in two batches of at most 1024) and one of 2 tensors: repeats of
+    a list reuse the descriptors already in the workspace, each switch uploads new
+    ones.  Every S_k and S stays bitwise the oracle's."""
+    rng = np.random.default_rng(77)
+    lists = [[(rng.standard_normal(int(n)) * 1e-2).astype(np.float32)
+              for n in rng.integers(1, 3000, size=1500)],
+             [(rng.standard_normal(n) * 1e-2).astype(np.float32) for n in (70000, 9)]]
+    refs = [oracle.grad_sqnorm(h, n_threads=8) for h in lists]
+    devs = [[to_dev(a) for a in h] for h in lists]
+    ws = torch.empty(max(lt.lt_grad_sqnorm_workspace_bytes([a.size for a in h]) for h in lists),
+                     dtype=torch.uint8, device=DEV)
+    try:
+        for i in range(40):
+            j = (i // 3) % 2  # three calls per list, then switch
+            K = len(devs[j])
+            sk = torch.empty(K, dtype=torch.float64, device=DEV)
+            S = torch.empty(1, dtype=torch.float64, device=DEV)
+            status = torch.empty(1, dtype=torch.int32, device=DEV)
+            lt.lt_grad_sqnorm(devs[j], S, status, sq_per_tensor=sk, workspace=ws)
+            rsk, rS, rst = refs[j]
+            assert to_host(sk).tobytes() == rsk.tobytes(), f"call {i}"
+            assert to_host(S)[0].hex() == rS.hex(), f"call {i}"
+            assert int(to_host(status)[0]) == rst, f"call {i}"
+    finally:
+        torch.cuda.synchronize()
+        lt.lt_workspace_release(ws)
+
+
 def test_sqnorm_subnormal_gradients():
     x = np.full(4097, np.float32(2.0 ** -140), np.float32)
     _sq_parity([x])
