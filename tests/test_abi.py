@@ -11,7 +11,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def _declared(header):
-    text = open(header).read()
+    with open(header) as fh:
+        text = fh.read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(lto?_[a-z0-9_]+)\s*\(", text)))
 
@@ -48,7 +49,8 @@ def test_workspace_size_queries():
 
 def test_library_is_built_for_gfx950():
     so = os.path.join(ROOT, "paper_2608_11919_amd", "liblazytrain.so")
-    assert b"gfx950" in open(so, "rb").read()
+    with open(so, "rb") as fh:
+        assert b"gfx950" in fh.read()
 
 
 def test_product_path_never_imports_the_oracle():
@@ -56,7 +58,8 @@ def test_product_path_never_imports_the_oracle():
     for dirpath, _, files in os.walk(pkg):
         for f in files:
             if f.endswith((".py", ".hip", ".h", ".cpp")):
-                src = open(os.path.join(dirpath, f)).read()
+                with open(os.path.join(dirpath, f)) as fh:
+                    src = fh.read()
                 assert "import oracle" not in src and "lazytrain_oracle" not in src, f
 
 
@@ -109,7 +112,8 @@ def test_enum_values_match_the_binding():
     """The binding's constants are the header's values; the error codes are the
     boundary's (LT_ERR_HIP = 3, LT_ERR_WORKSPACE = 4)."""
     import paper_2608_11919_amd as lt
-    text = open(os.path.join(ROOT, "include", "lazytrain.h")).read()
+    with open(os.path.join(ROOT, "include", "lazytrain.h")) as fh:
+        text = fh.read()
     names = ["LT_OK", "LT_ERR_INVALID_ARG", "LT_ERR_ALIGNMENT", "LT_ERR_HIP", "LT_ERR_WORKSPACE",
              "LT_STATUS_OK", "LT_STATUS_NONFINITE", "LT_STATUS_BAD_WORKSPACE", "LT_DTYPE_F32",
              "LT_DTYPE_BF16", "LT_MAP_LINEAR", "LT_MAP_DYNAMIC"]
