@@ -43,7 +43,7 @@ def _config(seed):
         grad_scale=float(rng.choice([1e-6, 1e-3, 1.0])))
 
 
-@pytest.mark.parametrize("seed", range(40))
+@pytest.mark.parametrize("seed", range(80))
 def test_random_configuration_matches_oracle(seed):
     c = _config(seed)
     rng, sizes, B = c["rng"], c["sizes"], c["block"]
