@@ -10,6 +10,8 @@ block of every tensor, compared bitwise with the oracle.
   blocks): three steps from zero state.  The oracle runs free on its own state, so
   bitwise equality of every array after every step also shows the two sides in
   lockstep (S19): nothing drifts apart.
+* The hybrid operator on the 3B-class model: a 2% slice with 8-bit states, fp32
+  moments for the rest, and the bf16 copy of every updated weight, over two steps.
 
 Both sides take the same generator output: it is drawn once on the host, copied
 to HBM for the HIP path, and then updated in place by the oracle."""
@@ -185,3 +187,89 @@ def test_clip_stress_three_steps_every_block(code_map):
             assert m.hma[k][b] == 0 and m.hva[k][b] == 0
     # the reading of this workload: norm ~ 1.76e7 from the +-9984 outliers
     assert 1.5e7 < float(rnorm) < 2.0e7
+
+
+@pytest.mark.timeout(900)
+def test_full_3b_hybrid_slice_with_bf16_copy_every_element():
+    """The hybrid operator at full size with the fused bf16 copy (f1, f3): the 2% slice
+    that lt_select_8bit_slice picks keeps 8-bit states (dynamic map, the optimizer's
+    default), the other 98% of the parameters keep fp32 moments, and every tensor gets
+    a bf16 copy of its updated weights.  Two clipped steps from zero states, so the
+    second starts from nonzero moments.  After each, every weight, code, scale, fp32
+    moment and bf16 copy is compared bitwise with the oracle (the copy with the
+    oracle's rounding of its own weights)."""
+    import concurrent.futures as cf
+
+    w = synth.full_3b()
+    nt = synth.default_threads()
+    K, B = len(w.numels), w.block_size
+    mask, n8 = lt.lt_select_8bit_slice(w.numels, 0.02)
+    i8 = [k for k in range(K) if mask[k]]
+    i32 = [k for k in range(K) if not mask[k]]
+    assert i8 and i32 and 0 < n8 <= 0.02 * w.n_params
+    t0 = time.time()
+    hw = [w.weights(k, n_threads=nt) for k in range(K)]
+    params = [torch.from_numpy(x).to(DEV) for x in hw]
+    nb = {k: -(-w.numels[k] // B) for k in i8}
+    hmq = {k: np.zeros(w.numels[k], np.int8) for k in i8}
+    hvq = {k: np.zeros(w.numels[k], np.uint8) for k in i8}
+    hma = {k: np.zeros(nb[k], np.float32) for k in i8}
+    hva = {k: np.zeros(nb[k], np.float32) for k in i8}
+    hm = {k: np.zeros(w.numels[k], np.float32) for k in i32}
+    hv = {k: np.zeros(w.numels[k], np.float32) for k in i32}
+    mq = {k: torch.zeros(w.numels[k], dtype=torch.int8, device=DEV) for k in i8}
+    vq = {k: torch.zeros(w.numels[k], dtype=torch.uint8, device=DEV) for k in i8}
+    ma = {k: torch.zeros(nb[k], dtype=torch.float32, device=DEV) for k in i8}
+    va = {k: torch.zeros(nb[k], dtype=torch.float32, device=DEV) for k in i8}
+    m32 = {k: torch.zeros(w.numels[k], dtype=torch.float32, device=DEV) for k in i32}
+    v32 = {k: torch.zeros(w.numels[k], dtype=torch.float32, device=DEV) for k in i32}
+    wb = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in w.numels]
+    grads = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in w.numels]
+    S = torch.zeros(1, dtype=torch.float64, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    coef = torch.zeros(1, dtype=torch.float32, device=DEV)
+    h = _hyper(w)
+    _say(f"hybrid slice: {len(i8)} tensors ({n8} params) 8-bit, {len(i32)} fp32; "
+         f"generated and in HBM ({time.time() - t0:.1f} s)")
+    with cf.ThreadPoolExecutor(max_workers=nt) as pool:
+        for t in (1, 2):
+            hg = [w.grads(k, synth.grad_stream(t), n_threads=nt) for k in range(K)]
+            for d, x in zip(grads, hg):
+                d.copy_(torch.from_numpy(x.view(np.int16)).view(torch.bfloat16))
+            lt.lt_grad_sqnorm(grads, S, status)
+            lt.lt_clip_coef(S, w.max_norm, coef)
+            lt.lt_hybrid8bit_adamw_step([params[k] for k in i8], [grads[k] for k in i8],
+                                        [mq[k] for k in i8], [ma[k] for k in i8],
+                                        [vq[k] for k in i8], [va[k] for k in i8], B, step=t,
+                                        coef=coef, status=status, code_map=lt.LT_MAP_DYNAMIC,
+                                        params_bf16=[wb[k] for k in i8], **h)
+            lt.lt_adamw_fp32_step([params[k] for k in i32], [grads[k] for k in i32],
+                                  [m32[k] for k in i32], [v32[k] for k in i32], step=t,
+                                  coef=coef, status=status, params_bf16=[wb[k] for k in i32],
+                                  **h)
+            torch.cuda.synchronize()
+            _, rS, rst = oracle.grad_sqnorm(hg, n_threads=nt)
+            _, rcoef = oracle.clip_coef(rS, w.max_norm)
+            assert to_host(S)[0].hex() == rS.hex() and rst == oracle.STATUS_OK
+            assert to_host(coef)[0] == rcoef
+            oracle.hybrid8bit_adamw_step([hw[k] for k in i8], [hg[k] for k in i8],
+                                         [hmq[k] for k in i8], [hma[k] for k in i8],
+                                         [hvq[k] for k in i8], [hva[k] for k in i8], B, step=t,
+                                         coef=float(rcoef), status=rst, n_threads=nt,
+                                         code_map=oracle.MAP_DYNAMIC, **h)
+            list(pool.map(lambda k: oracle.adamw_fp32_step(hw[k], hg[k], hm[k], hv[k], step=t,
+                                                           coef=float(rcoef), **h), i32))
+            del hg
+            expect_wb = list(pool.map(lambda k: oracle.round_bf16(hw[k]), range(K)))
+            for k in range(K):
+                pairs = [("w", params[k], hw[k]), ("bf16 copy", wb[k], expect_wb[k])]
+                if mask[k]:
+                    pairs += [("m codes", mq[k], hmq[k]), ("m absmax", ma[k], hma[k]),
+                              ("v codes", vq[k], hvq[k]), ("v absmax", va[k], hva[k])]
+                else:
+                    pairs += [("m", m32[k], hm[k]), ("v", v32[k], hv[k])]
+                for name, dev, host in pairs:
+                    assert to_host(dev).tobytes() == host.tobytes(), \
+                        f"t = {t}: tensor {k} {name} differs"
+            _say(f"t = {t}: all {w.n_params} weights, their bf16 copies and every state bitwise "
+                 f"equal (coef {float(rcoef):.6g})")
