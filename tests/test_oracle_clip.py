@@ -37,7 +37,8 @@ def test_infinite_max_norm_means_no_clipping():
     for s in (0.0, 1e-30, 0.5, 1.0, 3.7e3, 1e300):
         norm, coef = oracle.clip_coef(s, math.inf)
         assert coef == np.float32(1.0)
-        assert norm == np.float32(math.sqrt(s))
+        with np.errstate(over="ignore"):  # sqrt(1e300) = 1e150 rounds to fp32 infinity
+            assert norm == np.float32(math.sqrt(s))
 
 
 def test_below_threshold_is_exactly_one():
