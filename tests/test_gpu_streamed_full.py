@@ -9,9 +9,10 @@ configuration bench.py times (27B-class decoder layers of hidden 5120, FFN 17408
   the oracle's.  (Pass 2 writes the shared host state of several layers, so its
   results are not checked here.)
 * Eight distinct layers (2.6e9 parameters, every tensor at its full size) from zero
-  state, with the gradients copied in twice and kept in HBM between the passes: S
-  and the coefficient bitwise, and the updated weights, codes and scales of every
-  block of every tensor against the oracle run over the same host data."""
+  state, with the gradients copied in twice (linear map) and kept in HBM between the
+  passes (dynamic map): S and the coefficient bitwise, and the updated weights, codes
+  and scales of every block of every tensor against the oracle run over the same
+  host data."""
 import time
 
 import numpy as np
@@ -103,8 +104,8 @@ def test_whole_model_norm_and_coefficient_as_benchmarked(host_model):
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("keep", [False, True])
-def test_eight_full_size_layers_against_oracle(host_model, keep):
+@pytest.mark.parametrize("keep,code_map", [(False, lt.LT_MAP_LINEAR), (True, lt.LT_MAP_DYNAMIC)])
+def test_eight_full_size_layers_against_oracle(host_model, keep, code_map):
     w8, h = host_model
     B = w8.block_size
     # fresh state: the weights from the generator, zero codes and scales
@@ -119,12 +120,12 @@ def test_eight_full_size_layers_against_oracle(host_model, keep):
     cs, hs, ds = torch.cuda.Stream(DEV), torch.cuda.Stream(DEV), torch.cuda.Stream(DEV)
     cs.wait_stream(torch.cuda.current_stream())
     _say(f"streamed step over 8 distinct full-size layers from zero state, t = 1, "
-         f"gradients kept in HBM: {keep}")
+         f"gradients kept in HBM: {keep}, code map {code_map}")
     lt.lt_streamed_hybrid8bit_adamw_step(h["w"], h["g"], h["mq"], h["ma"], h["vq"], h["va"],
                                          first, B, step=1, max_norm=w8.max_norm, ring_slots=3,
                                          sq_total=S, coef=coef, status=status, total_norm=norm,
                                          compute_stream=cs, h2d_stream=hs, d2h_stream=ds,
-                                         keep_grads=keep, **_hyper(w8))
+                                         keep_grads=keep, code_map=code_map, **_hyper(w8))
     cs.synchronize()
     _, S_o, st_o = oracle.grad_sqnorm([_grad_bits(g) for g in h["g"]], n_threads=n_threads)
     _, c_o = oracle.clip_coef(S_o, w8.max_norm)
@@ -138,9 +139,10 @@ def test_eight_full_size_layers_against_oracle(host_model, keep):
     ref_vq = [np.zeros(n, np.uint8) for n in w8.numels]
     ref_ma = [np.zeros(-(-n // B), np.float32) for n in w8.numels]
     ref_va = [np.zeros(-(-n // B), np.float32) for n in w8.numels]
+    omap = oracle.MAP_DYNAMIC if code_map == lt.LT_MAP_DYNAMIC else oracle.MAP_LINEAR
     oracle.hybrid8bit_adamw_step(ref_w, ref_g, ref_mq, ref_ma, ref_vq, ref_va, B, step=1,
                                  coef=float(c_o), status=st_o, n_threads=n_threads,
-                                 **_hyper(w8))
+                                 code_map=omap, **_hyper(w8))
     blocks = 0
     for k in range(len(w8.numels)):
         for name, got, want in (("w", h["w"][k], ref_w[k]), ("m codes", h["mq"][k], ref_mq[k]),
@@ -150,4 +152,5 @@ def test_eight_full_size_layers_against_oracle(host_model, keep):
             assert got.numpy().tobytes() == want.tobytes(), f"tensor {k}: {name} differs"
         blocks += ref_ma[k].size
     assert blocks == sum(-(-n // B) for n in w8.numels)
-    _say(f"all {blocks} blocks of the 8 layers bitwise equal (keep_grads {keep})")
+    _say(f"all {blocks} blocks of the 8 layers bitwise equal (keep_grads {keep}, "
+         f"code map {code_map})")
