@@ -133,60 +133,122 @@ def _total_blocks(w):
     return sum(-(-n // w.block_size) for n in w.numels)
 
 
-@pytest.mark.timeout(900)
-@pytest.mark.parametrize("code_map", [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC])
-def test_full_3b_model_every_block(code_map):
-    w = synth.full_3b()
-    m = Model(w, synth.default_threads())
-    g0 = m.host_grads(synth.STREAM_PRIOR_GRAD)
-    m.load(g0)
-    m.gpu_step(1, code_map, clip=False, lr=0.0)  # the states of one prior step
-    m.oracle_step(g0, 1, code_map, lr=0.0)
-    del g0
-    hg = m.host_grads(synth.grad_stream(w.step))
-    m.load(hg)
-    _say(f"GPU step at t = {w.step} (sum of squares, clip, fused step), code map {code_map}")
-    m.gpu_step(w.step, code_map)
-    rS, rst, rcoef, rnorm = m.check_norm(hg)
-    _say(f"S = {rS!r}, norm {float(rnorm):.6g}, coef {float(rcoef):.6g}: bitwise equal")
-    m.oracle_step(hg, w.step, code_map, coef=float(rcoef), status=rst)
-    n = m.compare_all(f"{w.name}, map {code_map}")
-    assert n == _total_blocks(w) == 1506760
-    _say(f"all {n} blocks of {len(w.numels)} tensors bitwise equal (w, codes, scales)")
+MAPS = [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC]
 
 
-@pytest.mark.timeout(900)
-@pytest.mark.parametrize("code_map", [lt.LT_MAP_LINEAR, lt.LT_MAP_DYNAMIC])
-def test_clip_stress_three_steps_every_block(code_map):
-    w = synth.clip_stress()
-    m = Model(w, synth.default_threads())
-    # all-zero blocks of the gradients (the same in every step), checked by name below
-    rng = np.random.default_rng(13)
-    zero_blocks = []
-    while len(zero_blocks) < 200:
-        k = int(rng.integers(0, len(w.numels)))
-        b = int(rng.integers(0, -(-w.numels[k] // w.block_size)))
-        if synth.block_is_zero(w.seed, k, b, w.grad_recipe.zero_mod):
-            zero_blocks.append((k, b))
-    for t in (1, 2, 3):
+def _release(m):
+    """Frees a model's device and host arrays when its class of tests is done."""
+    for name in ("params", "mq", "vq", "ma", "va", "grads", "hw", "hmq", "hvq", "hma", "hva"):
+        setattr(m, name, None)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+class TestFull3BModel:
+    """Each step is a test of its own, so that no test runs for minutes without
+    reporting (the dynamic map's oracle takes about a minute per step at this size).
+    The model is shared by the class; a test runs any earlier step it needs."""
+
+    @pytest.fixture(scope="class", params=MAPS, ids=["linear", "dynamic"])
+    def model(self, request):
+        m = Model(synth.full_3b(), synth.default_threads())
+        m.code_map, m.t_done = request.param, 0
+        yield m
+        _release(m)
+
+    @staticmethod
+    def _prior_step(m):
+        """The states of one prior step: t = 1 with lr = 0, on both sides."""
+        g0 = m.host_grads(synth.STREAM_PRIOR_GRAD)
+        m.load(g0)
+        m.gpu_step(1, m.code_map, clip=False, lr=0.0)
+        m.oracle_step(g0, 1, m.code_map, lr=0.0)
+        m.t_done = 1
+
+    @pytest.mark.timeout(900)
+    def test_prior_step_every_block(self, model):
+        m = model
+        if m.t_done == 0:
+            self._prior_step(m)
+        n = m.compare_all(f"{m.w.name}, map {m.code_map}, prior step")
+        assert n == _total_blocks(m.w) == 1506760
+        _say(f"prior step: all {n} blocks bitwise equal (map {m.code_map})")
+
+    @pytest.mark.timeout(900)
+    def test_clipped_step_every_block(self, model):
+        m, w = model, model.w
+        if m.t_done == 0:
+            self._prior_step(m)
+        assert m.t_done == 1
+        hg = m.host_grads(synth.grad_stream(w.step))
+        m.load(hg)
+        _say(f"GPU step at t = {w.step} (sum of squares, clip, fused step), code map {m.code_map}")
+        m.gpu_step(w.step, m.code_map)
+        rS, rst, rcoef, rnorm = m.check_norm(hg)
+        _say(f"S = {rS!r}, norm {float(rnorm):.6g}, coef {float(rcoef):.6g}: bitwise equal")
+        m.oracle_step(hg, w.step, m.code_map, coef=float(rcoef), status=rst)
+        m.t_done = w.step
+        n = m.compare_all(f"{w.name}, map {m.code_map}")
+        assert n == _total_blocks(w) == 1506760
+        _say(f"all {n} blocks of {len(w.numels)} tensors bitwise equal (w, codes, scales)")
+
+
+class TestClipStressThreeSteps:
+    """Three steps from zero state, one test each; the oracle runs free on its own
+    state, so bitwise equality after every step also shows lockstep."""
+
+    @pytest.fixture(scope="class", params=MAPS, ids=["linear", "dynamic"])
+    def model(self, request):
+        w = synth.clip_stress()
+        m = Model(w, synth.default_threads())
+        m.code_map, m.t_done = request.param, 0
+        # all-zero blocks of the gradients (the same in every step), checked by name
+        rng = np.random.default_rng(13)
+        m.zero_blocks = []
+        while len(m.zero_blocks) < 200:
+            k = int(rng.integers(0, len(w.numels)))
+            b = int(rng.integers(0, -(-w.numels[k] // w.block_size)))
+            if synth.block_is_zero(w.seed, k, b, w.grad_recipe.zero_mod):
+                m.zero_blocks.append((k, b))
+        yield m
+        _release(m)
+
+    @staticmethod
+    def _step(m, t, compare):
+        w = m.w
         hg = m.host_grads(synth.grad_stream(t))
         m.load(hg)
-        _say(f"step t = {t}: GPU, code map {code_map}")
-        m.gpu_step(t, code_map)
+        _say(f"step t = {t}: GPU, code map {m.code_map}")
+        m.gpu_step(t, m.code_map)
         rS, rst, rcoef, rnorm = m.check_norm(hg)
         _say(f"  S bitwise equal; norm {float(rnorm):.6g}, coef {float(rcoef):.6g}")
-        m.oracle_step(hg, t, code_map, coef=float(rcoef), status=rst)
+        m.oracle_step(hg, t, m.code_map, coef=float(rcoef), status=rst)
         del hg
-        n = m.compare_all(f"{w.name}, map {code_map}, t = {t}")
+        m.t_done = t
+        if not compare:
+            return rnorm
+        n = m.compare_all(f"{w.name}, map {m.code_map}, t = {t}")
         assert n == _total_blocks(w)
         _say(f"  all {n} blocks bitwise equal to the free-running oracle")
         B = w.block_size
-        for k, b in zero_blocks:
+        for k, b in m.zero_blocks:
             lo, hi = b * B, min(w.numels[k], (b + 1) * B)
             assert not m.hmq[k][lo:hi].any() and not m.hvq[k][lo:hi].any()
             assert m.hma[k][b] == 0 and m.hva[k][b] == 0
-    # the reading of this workload: norm ~ 1.76e7 from the +-9984 outliers
-    assert 1.5e7 < float(rnorm) < 2.0e7
+        return rnorm
+
+    def _run_to(self, m, t):
+        while m.t_done < t - 1:
+            self._step(m, m.t_done + 1, compare=False)
+        assert m.t_done == t - 1
+        return self._step(m, t, compare=True)
+
+    @pytest.mark.timeout(900)
+    @pytest.mark.parametrize("t", [1, 2, 3])
+    def test_step_every_block(self, model, t):
+        rnorm = self._run_to(model, t)
+        # the reading of this workload: norm ~ 1.76e7 from the +-9984 outliers
+        assert 1.5e7 < float(rnorm) < 2.0e7
 
 
 @pytest.mark.timeout(900)
